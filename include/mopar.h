@@ -1,0 +1,273 @@
+/*
+ * mopar.h -- C ABI of the MI355X (gfx950) sliced-inference library.
+ *
+ * The library implements the hot path of MOPAR (arXiv 2404.02445): a model
+ * cut vertically into slices of similar layers (Sec. III-C, strategy pi_S),
+ * each resource-dominant (RD) conv / GEMM split into k equal-size sub-slices
+ * along its output channels or features (Sec. III-C, strategy pi_P), and the
+ * activation at every split point handed to the next slice through a device
+ * buffer, optionally encoded by the one-layer autoencoder of Sec. III-D.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Status.    Every call returns a mopar_status.  On any non-zero status
+ *            nothing has been enqueued and no output has been written;
+ *            mopar_last_error() returns a description (thread-local).
+ * Memory.    The caller owns every byte: weights, inputs, outputs, code
+ *            buffers and the workspace are device pointers the caller
+ *            allocated; descriptors and plans are host memory the caller
+ *            owns.  The library never allocates device memory, never frees
+ *            caller memory and never synchronises the host.
+ * Streams.   `stream` is a hipStream_t passed as void* (NULL = the default
+ *            stream).  Work is enqueued asynchronously in call order.
+ * Alignment. Device pointers must be 16-byte aligned.
+ * Layouts.   Tensor descriptors give logical dims in canonical order:
+ *            images (N, C, H, W), flattened (N, F), sequences (B, S, F),
+ *            token ids (B, S).  Physically, the model input is stored as
+ *            described (images: NCHW float32; ids: int32), and every other
+ *            rank-4 tensor is stored channels-last (NHWC) in the model
+ *            dtype; rank-2/3 tensors are row-major.  Weight layouts are
+ *            given at mopar_op.
+ * Determinism. Plans and sub-slice ranges are pure functions of their
+ *            inputs; kernels use no atomics, so a forward pass is bitwise
+ *            reproducible, and the k-way sub-sliced RD kernels produce the
+ *            same bits as the unsplit kernel.
+ */
+#ifndef MOPAR_H
+#define MOPAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MOPAR_OK = 0,
+    MOPAR_E_ARG = 1,          /* null pointer, bad enum, inconsistent sizes        */
+    MOPAR_E_SHAPE = 2,        /* tensor shapes do not match the op                 */
+    MOPAR_E_DTYPE = 3,        /* dtype not supported for this op / model           */
+    MOPAR_E_UNSUPPORTED = 4,  /* valid request outside what the kernels implement  */
+    MOPAR_E_INFEASIBLE = 5,   /* no plan satisfies the slicing constraints         */
+    MOPAR_E_WORKSPACE = 6,    /* workspace or code buffer too small                */
+    MOPAR_E_HIP = 7           /* a HIP runtime call or kernel launch failed        */
+} mopar_status;
+
+typedef enum { MOPAR_F32 = 0, MOPAR_BF16 = 1, MOPAR_I32 = 2 } mopar_dtype;
+
+/* ------------------------------------------------------------------------ */
+/* Sub-slice ranges (Sec. III-C: eta equal-size sub-slices)                  */
+/* ------------------------------------------------------------------------ */
+
+/* Range [*lo, *hi) of sub-slice j when n outputs are split k ways: sizes
+ * n/k, with the first n mod k ranges one larger.  Needs 1 <= k <= n,
+ * 0 <= j < k; otherwise MOPAR_E_ARG. */
+int mopar_subslice_range(int32_t n, int32_t k, int32_t j, int32_t* lo, int32_t* hi);
+
+/* ------------------------------------------------------------------------ */
+/* Planning (Sec. III-B service profile, Sec. III-C HyPAD, Eq. 1-6, Alg. 1)  */
+/* ------------------------------------------------------------------------ */
+
+/* One planning node (layer): memory footprint M_l (bytes) and time t_l
+ * (seconds) of Eq. 1-3, the bytes of the tensor it hands to the next node,
+ * and the output width of its RD op(s) (smallest one; 0 = no RD op). */
+typedef struct {
+    double mem_bytes;
+    double time_s;
+    double out_bytes;
+    int32_t rd_width;
+    int32_t reserved;
+} mopar_layer_profile;
+
+/* Options of the partitioner; zero-initialise and set what you need. */
+typedef struct {
+    int32_t n_slices;           /* 0: the DP picks the count; > 0: exactly this many slices       */
+    int32_t k_max;              /* largest sub-slice count searched (>= 1; 0 is read as 1)        */
+    const uint8_t* allowed_cut; /* n-1 flags, cut after node j allowed; NULL: all, after node
+                                   elimination; when given, elimination is skipped               */
+    double elim_tau;            /* node-elimination threshold (Sec. III-C: 0.05); < 0 disables    */
+    double c_m;                 /* cost per unit memory x time (Eq. 6)                            */
+    double c_n;                 /* cost per unit transfer time (Eq. 6)                            */
+    double bw_Bps;              /* boundary bandwidth for t_c = (bytes / ratio) / bw (> 0)        */
+    const double* ratio;        /* n-1 compression ratios per cut position; NULL: 1               */
+    double lambda_bytes;        /* eta <= floor(M_g / lambda) when > 0 (Eq. 6 constraint)         */
+    const double* tp_table;     /* [n][k_max] measured t_p(l, eta); NULL: t_p = t_l               */
+    const double* ta_table;     /* [n][k_max] measured t_a(l, eta); NULL: 0                       */
+    const int32_t* k_override;  /* n entries; > 0 forces k for that node; NULL: none              */
+} mopar_plan_opts;
+
+/* A plan.  slice_end and k are caller-allocated arrays of n entries. */
+typedef struct {
+    int32_t n_layers;           /* n: set by the caller to the array capacity; checked            */
+    int32_t n_slices;           /* out                                                            */
+    int32_t* slice_end;         /* out: last node (0-based) of each slice                         */
+    int32_t* k;                 /* out: sub-slice count per node (1 = unsplit)                    */
+    double cost;                /* out: Eq. 6 objective of the chosen cuts                        */
+    double t_tau;               /* out: Eq. 5 latency with the chosen k and cuts                  */
+    double t_unsplit;           /* out: sum of t_l                                                */
+    int32_t latency_ok;         /* out: t_tau <= t_unsplit (Eq. 6, second constraint)             */
+    int32_t reserved;
+} mopar_plan;
+
+/* HyPAD on a chain of n planning nodes (Alg. 1): node elimination, DP over
+ * split points (ties keep the longest last slice), backtrack through the
+ * stored argmin, then the parallelism search per slice (Eq. 5; ties keep
+ * the smallest eta).  Pure host code, no device calls.  Errors: MOPAR_E_ARG
+ * (null pointers, n < 1, capacity too small, bad k_override),
+ * MOPAR_E_INFEASIBLE (fewer admissible cuts than n_slices - 1). */
+int mopar_plan_slices(const mopar_layer_profile* layers, int32_t n, const mopar_plan_opts* opts,
+                      mopar_plan* out);
+
+/* ------------------------------------------------------------------------ */
+/* Model description                                                         */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    int32_t dtype;              /* mopar_dtype */
+    int32_t rank;               /* 1..4 */
+    int64_t dims[4];            /* canonical order, see the header comment */
+} mopar_tensor_desc;
+
+typedef enum {
+    MOPAR_OP_CONV = 1,       /* in0 (N,C,H,W) -> out (N,Co,Ho,Wo); in1 optional residual (out shape)
+                                w: [Co][kh][kw][Cs] with Cs = C rounded up to the kernel's channel
+                                granule (8 for bf16, 4 for f32; extra channels zero); b: [Co]
+                                When in0 is the model input (NCHW float32) the library converts it
+                                to channels-last itself.                                          */
+    MOPAR_OP_LINEAR = 2,     /* in0 (..., K) or (N,C,H,W) flattened -> out (..., n_out);
+                                in1 optional residual; w: [n_out][K] (for an image input, K runs
+                                over (h, w, c) -- channels-last order); b: [n_out]                */
+    MOPAR_OP_MAXPOOL = 3,    /* kh x kw window, stride, pad (outside = -inf)                      */
+    MOPAR_OP_AVGPOOL = 4,    /* global average (N,C,H,W) -> (N,C)                                 */
+    MOPAR_OP_LAYERNORM = 5,  /* over the last dim of in0 (+ in1); w: gamma [F]; b: beta [F]; eps   */
+    MOPAR_OP_ATTENTION = 6,  /* in0 (B,S,3F) = [Q|K|V] -> out (B,S,F); heads; scale; head dim 64  */
+    MOPAR_OP_EMBED_BERT = 7, /* ids (B,S) -> LN(tok[id] + pos[s] + type[0]); w: tok [V][F];
+                                w2: pos [P][F]; w3: type [T][F]; w4: gamma; w5: beta; eps        */
+    MOPAR_OP_EMBED = 8,      /* ids (B,S) -> table[id]; w: table [V][F]                           */
+    MOPAR_OP_LSTM = 9        /* in0 (B,T,E) -> out (B,T,H) hidden sequence, h0 = c0 = 0;
+                                w: W_ih [4H][E], w2: W_hh [4H][H], b: b_ih [4H], w3: b_hh [4H];
+                                rows interleaved by unit: row 4u+g holds gate g (i,f,g,o) of
+                                hidden unit u.  c is kept in float32.                              */
+} mopar_op_kind;
+
+typedef enum { MOPAR_ACT_NONE = 0, MOPAR_ACT_RELU = 1, MOPAR_ACT_GELU = 2 } mopar_act;
+
+/* One operator.  Weight fields are byte offsets into the weight blob passed
+ * to mopar_model_create (-1 = absent); weights are in the model dtype. */
+typedef struct {
+    int32_t kind;               /* mopar_op_kind */
+    int32_t act;                /* mopar_act (conv, linear) */
+    int32_t layer;              /* planning node, non-decreasing over the op list */
+    int32_t branch;             /* 0: sequential chain (Eq. 1); >= 1: parallel branch (Eq. 2) */
+    int32_t pos;                /* position along its branch (Eq. 2) */
+    int32_t rd;                 /* 1: resource-dominant, split k ways as the plan says */
+    int32_t in0, in1, out;      /* tensor ids; in1 = -1 when absent */
+    int32_t kh, kw, stride, pad;
+    int32_t heads;
+    int32_t n_out;              /* conv C_out, linear N, LSTM hidden size */
+    int32_t reserved;
+    float eps;
+    float scale;
+    int64_t rows[3];            /* table rows: EMBED_BERT vocab, positions, token types; EMBED vocab */
+    int64_t w, b, w2, w3, w4, w5;
+} mopar_op;
+
+typedef struct {
+    int32_t dtype;              /* model dtype: MOPAR_F32 or MOPAR_BF16 */
+    int32_t n_tensors;
+    const mopar_tensor_desc* tensors;
+    int32_t n_ops;
+    const mopar_op* ops;
+    int32_t n_layers;
+    int32_t input, output;      /* tensor ids of the model input and output */
+} mopar_model_desc;
+
+typedef struct mopar_model_s* mopar_model_t;
+
+/* Validate the description and build host metadata (op dispatch, workspace
+ * layout).  `weights_dev` (device) must stay valid for the model's life;
+ * `weights_bytes` bounds every weight offset.  No device calls. */
+int mopar_model_create(const mopar_model_desc* desc, const void* weights_dev, size_t weights_bytes,
+                       mopar_model_t* out);
+void mopar_model_destroy(mopar_model_t model);
+
+/* Layer profiles (Eq. 1-4) of the model: op memory = bytes of parameters +
+ * inputs + output; op time = max(FLOP / peak, bytes / 8e12), peak 2.5e15
+ * (bf16) or 157.3e12 (f32) FLOP/s; FLOP counted for conv, linear, attention
+ * and LSTM.  `out` has n_layers entries. */
+int mopar_model_profile(mopar_model_t model, mopar_layer_profile* out);
+
+/* Bytes of device workspace mopar_slice_forward / mopar_model_forward need
+ * under `plan` (activations inside slices, boundary tensors, scratch). */
+int mopar_model_workspace_bytes(mopar_model_t model, const mopar_plan* plan, size_t* bytes);
+
+/* Run slice s of `plan`: the layers after the previous cut up to
+ * slice_end[s].  `in_dev` holds the slice input (the model input for s = 0,
+ * otherwise the boundary tensor leaving slice s-1, in its physical layout);
+ * `out_dev` receives the tensor leaving slice s.  RD ops of node l run as
+ * k[l] sub-slices of one launch. */
+int mopar_slice_forward(mopar_model_t model, const mopar_plan* plan, int32_t s, const void* in_dev,
+                        void* out_dev, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Boundary codec (Sec. III-D)                                               */
+/* ------------------------------------------------------------------------ */
+
+typedef enum { MOPAR_CODEC_RAW = 0, MOPAR_CODEC_AE = 1 } mopar_codec_kind;
+
+/* RAW: the code is the tensor's bytes (lossless, R = 1).
+ * AE:  at every position p (each (n,h,w) of an image, each token of a
+ *      sequence): code[p][e] = b_enc[e] + sum_c w_enc[e][c] x[p][c] and
+ *      y[p][c] = b_dec[c] + sum_e w_dec[c][e] code[p][e], stored in the
+ *      tensor's dtype; R = c / c_code.  Weights are device pointers in the
+ *      tensor dtype: w_enc [c_code][c], b_enc [c_code], w_dec [c][c_code],
+ *      b_dec [c].  c and c_code must be multiples of 8 (bf16) or 4 (f32). */
+typedef struct {
+    int32_t kind;
+    int32_t c, c_code;
+    int32_t reserved;
+    const void* w_enc;
+    const void* b_enc;
+    const void* w_dec;
+    const void* b_dec;
+} mopar_codec;
+
+/* Size in bytes of the code of tensor x. */
+int mopar_boundary_code_bytes(const mopar_codec* codec, const mopar_tensor_desc* x, size_t* bytes);
+
+/* Encode x (device, physical layout) into code_dev.  Channels are dims[1]
+ * for rank-4 tensors and the last dim otherwise. */
+int mopar_boundary_encode(const mopar_codec* codec, const mopar_tensor_desc* x, const void* x_dev,
+                          void* code_dev, void* stream);
+
+/* Decode code_dev into y (device), the inverse direction of encode. */
+int mopar_boundary_decode(const mopar_codec* codec, const mopar_tensor_desc* y, const void* code_dev,
+                          void* y_dev, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Whole model                                                               */
+/* ------------------------------------------------------------------------ */
+
+/* Sliced forward pass: for each slice s, decode code_bufs[s-1] into the
+ * slice input (s > 0), run the slice, and encode its output into
+ * code_bufs[s] (s < S-1), all on `stream` with no host round-trip (the
+ * device buffer and stream order stand for the share-memory directory and
+ * message channel of Sec. III-D).  `codecs` and `code_bufs` have S-1
+ * entries (may be NULL when S = 1); code_bufs[s] must hold
+ * mopar_boundary_code_bytes of that boundary. */
+int mopar_model_forward(mopar_model_t model, const mopar_plan* plan, const mopar_codec* codecs,
+                        const void* in_dev, void* out_dev, void* const* code_bufs, void* ws,
+                        size_t ws_bytes, void* stream);
+
+/* Description of the last error on this thread ("" when none). */
+const char* mopar_last_error(void);
+
+/* Library version string. */
+const char* mopar_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOPAR_H */

@@ -1,0 +1,107 @@
+// extern "C" entry points: argument checks live in the *_impl functions, this
+// file only turns C++ exceptions into status codes and keeps the error text.
+#include <exception>
+#include <string>
+
+#include "internal.h"
+
+namespace mopar {
+
+int plan_slices_impl(const mopar_layer_profile*, int32_t, const mopar_plan_opts*, mopar_plan*);
+int subslice_range_impl(int32_t, int32_t, int32_t, int32_t*, int32_t*);
+int model_create_impl(const mopar_model_desc*, const void*, size_t, mopar_model_t*);
+void model_destroy_impl(mopar_model_t);
+int model_profile_impl(const mopar_model_s*, mopar_layer_profile*);
+int workspace_bytes_impl(const mopar_model_s*, const mopar_plan*, size_t*);
+int slice_forward_impl(const mopar_model_s*, const mopar_plan*, int32_t, const void*, void*, void*, size_t, void*);
+int code_bytes_impl(const mopar_codec*, const mopar_tensor_desc*, size_t*);
+int encode_impl(const mopar_codec*, const mopar_tensor_desc*, const void*, void*, void*);
+int decode_impl(const mopar_codec*, const mopar_tensor_desc*, const void*, void*, void*);
+int model_forward_impl(const mopar_model_s*, const mopar_plan*, const mopar_codec*, const void*, void*, void* const*,
+                       void*, size_t, void*);
+
+static thread_local std::string g_error;
+
+int set_error(int status, const std::string& msg) {
+    g_error = msg;
+    return status;
+}
+
+int hip_check(hipError_t e, const char* what) {
+    if (e == hipSuccess) return MOPAR_OK;
+    return set_error(MOPAR_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+template <typename F>
+static int guarded(const char* who, F&& f) {
+    try {
+        g_error.clear();
+        return f();
+    } catch (const std::exception& e) {
+        return set_error(MOPAR_E_ARG, std::string(who) + ": " + e.what());
+    } catch (...) {
+        return set_error(MOPAR_E_ARG, std::string(who) + ": unknown exception");
+    }
+}
+
+}  // namespace mopar
+
+using namespace mopar;
+
+extern "C" {
+
+int mopar_subslice_range(int32_t n, int32_t k, int32_t j, int32_t* lo, int32_t* hi) {
+    return guarded("mopar_subslice_range", [&] { return subslice_range_impl(n, k, j, lo, hi); });
+}
+
+int mopar_plan_slices(const mopar_layer_profile* layers, int32_t n, const mopar_plan_opts* opts, mopar_plan* out) {
+    return guarded("mopar_plan_slices", [&] { return plan_slices_impl(layers, n, opts, out); });
+}
+
+int mopar_model_create(const mopar_model_desc* desc, const void* weights_dev, size_t weights_bytes,
+                       mopar_model_t* out) {
+    return guarded("mopar_model_create", [&] { return model_create_impl(desc, weights_dev, weights_bytes, out); });
+}
+
+void mopar_model_destroy(mopar_model_t model) { model_destroy_impl(model); }
+
+int mopar_model_profile(mopar_model_t model, mopar_layer_profile* out) {
+    return guarded("mopar_model_profile", [&] { return model_profile_impl(model, out); });
+}
+
+int mopar_model_workspace_bytes(mopar_model_t model, const mopar_plan* plan, size_t* bytes) {
+    return guarded("mopar_model_workspace_bytes", [&] { return workspace_bytes_impl(model, plan, bytes); });
+}
+
+int mopar_slice_forward(mopar_model_t model, const mopar_plan* plan, int32_t s, const void* in_dev, void* out_dev,
+                        void* ws, size_t ws_bytes, void* stream) {
+    return guarded("mopar_slice_forward",
+                   [&] { return slice_forward_impl(model, plan, s, in_dev, out_dev, ws, ws_bytes, stream); });
+}
+
+int mopar_boundary_code_bytes(const mopar_codec* codec, const mopar_tensor_desc* x, size_t* bytes) {
+    return guarded("mopar_boundary_code_bytes", [&] { return code_bytes_impl(codec, x, bytes); });
+}
+
+int mopar_boundary_encode(const mopar_codec* codec, const mopar_tensor_desc* x, const void* x_dev, void* code_dev,
+                          void* stream) {
+    return guarded("mopar_boundary_encode", [&] { return encode_impl(codec, x, x_dev, code_dev, stream); });
+}
+
+int mopar_boundary_decode(const mopar_codec* codec, const mopar_tensor_desc* y, const void* code_dev, void* y_dev,
+                          void* stream) {
+    return guarded("mopar_boundary_decode", [&] { return decode_impl(codec, y, code_dev, y_dev, stream); });
+}
+
+int mopar_model_forward(mopar_model_t model, const mopar_plan* plan, const mopar_codec* codecs, const void* in_dev,
+                        void* out_dev, void* const* code_bufs, void* ws, size_t ws_bytes, void* stream) {
+    return guarded("mopar_model_forward", [&] {
+        return model_forward_impl(model, plan, codecs, in_dev, out_dev, code_bufs, ws, ws_bytes, stream);
+    });
+}
+
+const char* mopar_last_error(void) { return g_error.c_str(); }
+
+const char* mopar_version(void) { return "mopar-mi355x 0.1 (gfx950)"; }
+
+}  // extern "C"

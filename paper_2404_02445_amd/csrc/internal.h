@@ -1,0 +1,76 @@
+// Internal declarations shared by the host code and the kernel launchers.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include <hip/hip_runtime.h>
+
+#include "../../include/mopar.h"
+
+namespace mopar {
+
+// Thread-local error text; set_error returns the status for `return set_error(...)`.
+int set_error(int status, const std::string& msg);
+int hip_check(hipError_t e, const char* what);
+
+// ---------------------------------------------------------------------------
+// Kernel launch parameters
+// ---------------------------------------------------------------------------
+
+// C[m, n] = act(sum_k A[m, k] * B[n, k] + bias[n] + res[m, n]) for the column
+// range of each sub-slice.  A is either a dense row-major matrix or the
+// implicit im2col view of an NHWC image (conv).  B is [N][K] row-major.
+struct GemmParams {
+    const void* A;
+    int64_t lda;            // dense A row stride, elements
+    // implicit-conv view of A (conv != 0)
+    int conv;
+    int img_h, img_w, cs;   // input H, W and channel storage stride
+    int out_h, out_w;       // output H, W
+    int kh, kw, stride, pad;
+    const void* B;          // [N][K]
+    const void* bias;       // [N] or null
+    const void* res;        // [M][ldc] or null
+    void* C;
+    int64_t ldc;
+    int64_t M;
+    int N, K;
+    int act;
+    int ksub;               // number of sub-slices (gridDim.z)
+    const void* bias2;      // optional second bias [N]
+    int out_f32;            // store C as float32 instead of the model dtype
+    int epi;                // EPI_STD or EPI_LSTM
+    // EPI_LSTM: columns 4u..4u+3 are gates i, f, g, o of hidden unit u.
+    const float* gx;        // [M][ldgx] float32 gate pre-activations added to the product
+    int64_t ldgx;
+    float* cstate;          // [M][N/4] float32 cell state, read then overwritten
+    // the new hidden state of unit u goes to C[m * ldc + u]
+};
+
+enum { EPI_STD = 0, EPI_LSTM = 1 };
+
+hipError_t launch_gemm(const GemmParams& p, int dtype, hipStream_t stream);
+
+// NCHW float32 -> NHWC (model dtype), channels padded with zeros to cs.
+hipError_t launch_nchw_to_nhwc(const float* x, void* y, int n, int c, int h, int w, int cs, int dtype,
+                               hipStream_t s);
+hipError_t launch_maxpool(const void* x, void* y, int n, int h, int w, int c, int k, int stride, int pad,
+                          int ho, int wo, int dtype, hipStream_t s);
+hipError_t launch_avgpool(const void* x, void* y, int n, int hw, int c, int dtype, hipStream_t s);
+hipError_t launch_layernorm(const void* x, const void* res, const void* g, const void* b, void* y,
+                            int64_t rows, int f, float eps, int dtype, hipStream_t s);
+hipError_t launch_embed_bert(const int32_t* ids, const void* tok, const void* pos, const void* type,
+                             const void* g, const void* b, void* y, int batch, int seq, int f, float eps,
+                             int dtype, hipStream_t s);
+hipError_t launch_embed(const int32_t* ids, const void* table, void* y, int64_t n, int f, int dtype,
+                        hipStream_t s);
+hipError_t launch_attention(const void* qkv, void* y, int batch, int seq, int heads, float scale, int dtype,
+                            hipStream_t s);
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s);
+
+size_t dtype_size(int dtype);
+
+}  // namespace mopar

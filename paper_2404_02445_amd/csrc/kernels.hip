@@ -1,0 +1,382 @@
+// Bandwidth-bound kernels of the sliced forward pass (gfx950, wave64):
+// input layout conversion, pooling, layer norm, embeddings, attention and the
+// raw boundary copy.  Accesses are 16-byte vectors along the contiguous
+// (channel / feature) dimension wherever the shape allows; reductions are
+// wave-level butterflies (no atomics, so results are reproducible).
+#include "internal.h"
+
+namespace mopar {
+
+template <typename T> struct Vec;   // 16-byte vector of T
+template <> struct Vec<__bf16> { static constexpr int N = 8; };
+template <> struct Vec<float> { static constexpr int N = 4; };
+
+__device__ __forceinline__ float to_f(__bf16 v) {
+    return __uint_as_float(static_cast<unsigned>(__builtin_bit_cast(unsigned short, v)) << 16);
+}
+__device__ __forceinline__ float to_f(float v) { return v; }
+
+template <typename T> __device__ __forceinline__ T from_f(float v) { return static_cast<T>(v); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+static inline unsigned blocks_for(int64_t n, int per_block) {
+    int64_t b = (n + per_block - 1) / per_block;
+    return static_cast<unsigned>(b < 1 ? 1 : b);
+}
+
+// ---------------------------------------------------------------------------
+// NCHW float32 (model input) -> NHWC in the model dtype, channels padded to cs.
+// One thread per pixel: C strided reads (coalesced across neighbouring w),
+// one cs-wide contiguous write.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void nchw_to_nhwc_kernel(const float* __restrict__ x, T* __restrict__ y, int n, int c, int h, int w,
+                                    int cs) {
+    const int64_t pix = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    const int64_t hw = static_cast<int64_t>(h) * w;
+    if (pix >= static_cast<int64_t>(n) * hw) return;
+    const int64_t img = pix / hw, r = pix - img * hw;
+    const float* src = x + img * c * hw + r;
+    T* dst = y + pix * cs;
+    for (int ch = 0; ch < cs; ++ch) dst[ch] = from_f<T>(ch < c ? src[ch * hw] : 0.0f);
+}
+
+hipError_t launch_nchw_to_nhwc(const float* x, void* y, int n, int c, int h, int w, int cs, int dtype,
+                               hipStream_t s) {
+    const int64_t pix = static_cast<int64_t>(n) * h * w;
+    if (dtype == MOPAR_BF16)
+        hipLaunchKernelGGL(nchw_to_nhwc_kernel<__bf16>, dim3(blocks_for(pix, 256)), dim3(256), 0, s, x,
+                           static_cast<__bf16*>(y), n, c, h, w, cs);
+    else
+        hipLaunchKernelGGL(nchw_to_nhwc_kernel<float>, dim3(blocks_for(pix, 256)), dim3(256), 0, s, x,
+                           static_cast<float*>(y), n, c, h, w, cs);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Max pool, NHWC: one thread per (output pixel, 16-byte channel group).
+// Window positions outside the image are skipped (they count as -inf).
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void maxpool_kernel(const T* __restrict__ x, T* __restrict__ y, int n, int h, int w, int c, int k,
+                               int stride, int pad, int ho, int wo) {
+    constexpr int V = Vec<T>::N;
+    const int groups = c / V;
+    const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    const int64_t total = static_cast<int64_t>(n) * ho * wo * groups;
+    if (t >= total) return;
+    const int g = static_cast<int>(t % groups);
+    const int64_t pix = t / groups;
+    const int ox = static_cast<int>(pix % wo);
+    const int oy = static_cast<int>((pix / wo) % ho);
+    const int64_t img = pix / (static_cast<int64_t>(wo) * ho);
+    float m[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) m[i] = -INFINITY;
+    for (int r = 0; r < k; ++r) {
+        const int iy = oy * stride - pad + r;
+        if (iy < 0 || iy >= h) continue;
+        for (int q = 0; q < k; ++q) {
+            const int ix = ox * stride - pad + q;
+            if (ix < 0 || ix >= w) continue;
+            const uint4 raw = *reinterpret_cast<const uint4*>(x + ((img * h + iy) * w + ix) * c + g * V);
+            const T* e = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+            for (int i = 0; i < V; ++i) m[i] = fmaxf(m[i], to_f(e[i]));
+        }
+    }
+    uint4 out;
+    T* o = reinterpret_cast<T*>(&out);
+#pragma unroll
+    for (int i = 0; i < V; ++i) o[i] = from_f<T>(m[i]);
+    *reinterpret_cast<uint4*>(y + pix * c + g * V) = out;
+}
+
+hipError_t launch_maxpool(const void* x, void* y, int n, int h, int w, int c, int k, int stride, int pad, int ho,
+                          int wo, int dtype, hipStream_t s) {
+    if (dtype == MOPAR_BF16) {
+        const int64_t total = static_cast<int64_t>(n) * ho * wo * (c / 8);
+        hipLaunchKernelGGL(maxpool_kernel<__bf16>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
+                           static_cast<const __bf16*>(x), static_cast<__bf16*>(y), n, h, w, c, k, stride, pad, ho, wo);
+    } else {
+        const int64_t total = static_cast<int64_t>(n) * ho * wo * (c / 4);
+        hipLaunchKernelGGL(maxpool_kernel<float>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
+                           static_cast<const float*>(x), static_cast<float*>(y), n, h, w, c, k, stride, pad, ho, wo);
+    }
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Global average pool, NHWC -> [N][C]: one thread per (n, c); reads are
+// coalesced across c.  fp32 sum in pixel order, then one division.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void avgpool_kernel(const T* __restrict__ x, T* __restrict__ y, int n, int hw, int c) {
+    const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (t >= static_cast<int64_t>(n) * c) return;
+    const int64_t img = t / c;
+    const int ch = static_cast<int>(t - img * c);
+    const T* p = x + img * hw * c + ch;
+    float s = 0.0f;
+    for (int i = 0; i < hw; ++i) s += to_f(p[static_cast<int64_t>(i) * c]);
+    y[t] = from_f<T>(s / static_cast<float>(hw));
+}
+
+hipError_t launch_avgpool(const void* x, void* y, int n, int hw, int c, int dtype, hipStream_t s) {
+    const int64_t total = static_cast<int64_t>(n) * c;
+    if (dtype == MOPAR_BF16)
+        hipLaunchKernelGGL(avgpool_kernel<__bf16>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
+                           static_cast<const __bf16*>(x), static_cast<__bf16*>(y), n, hw, c);
+    else
+        hipLaunchKernelGGL(avgpool_kernel<float>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
+                           static_cast<const float*>(x), static_cast<float*>(y), n, hw, c);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Layer norm over rows of F <= 64 * LN_MAXV elements: one wave per row, the
+// row held in registers, mean then centred variance by wave butterflies.
+// ---------------------------------------------------------------------------
+constexpr int LN_MAXV = 32;
+
+template <typename T>
+__device__ __forceinline__ void ln_row(float (&v)[LN_MAXV], int f, int lane, const T* g, const T* b, float eps,
+                                       T* out) {
+    float s = 0.0f;
+#pragma unroll
+    for (int i = 0; i < LN_MAXV; ++i)
+        if (lane + i * 64 < f) s += v[i];
+    const float mean = wave_sum(s) / static_cast<float>(f);
+    float q = 0.0f;
+#pragma unroll
+    for (int i = 0; i < LN_MAXV; ++i)
+        if (lane + i * 64 < f) {
+            const float d = v[i] - mean;
+            q += d * d;
+        }
+    const float var = wave_sum(q) / static_cast<float>(f);
+    const float inv = 1.0f / sqrtf(var + eps);
+#pragma unroll
+    for (int i = 0; i < LN_MAXV; ++i) {
+        const int col = lane + i * 64;
+        if (col < f) out[col] = from_f<T>((v[i] - mean) * inv * to_f(g[col]) + to_f(b[col]));
+    }
+}
+
+template <typename T>
+__global__ void layernorm_kernel(const T* __restrict__ x, const T* __restrict__ res, const T* __restrict__ g,
+                                 const T* __restrict__ b, T* __restrict__ y, int64_t rows, int f, float eps) {
+    const int lane = threadIdx.x & 63;
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * (blockDim.x / 64) + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    const T* xr = x + row * f;
+    const T* rr = res ? res + row * f : nullptr;
+    float v[LN_MAXV];
+#pragma unroll
+    for (int i = 0; i < LN_MAXV; ++i) {
+        const int col = lane + i * 64;
+        v[i] = col < f ? to_f(xr[col]) + (rr ? to_f(rr[col]) : 0.0f) : 0.0f;
+    }
+    ln_row<T>(v, f, lane, g, b, eps, y + row * f);
+}
+
+hipError_t launch_layernorm(const void* x, const void* res, const void* g, const void* b, void* y, int64_t rows,
+                            int f, float eps, int dtype, hipStream_t s) {
+    if (dtype == MOPAR_BF16)
+        hipLaunchKernelGGL(layernorm_kernel<__bf16>, dim3(blocks_for(rows, 4)), dim3(256), 0, s,
+                           static_cast<const __bf16*>(x), static_cast<const __bf16*>(res),
+                           static_cast<const __bf16*>(g), static_cast<const __bf16*>(b), static_cast<__bf16*>(y),
+                           rows, f, eps);
+    else
+        hipLaunchKernelGGL(layernorm_kernel<float>, dim3(blocks_for(rows, 4)), dim3(256), 0, s,
+                           static_cast<const float*>(x), static_cast<const float*>(res),
+                           static_cast<const float*>(g), static_cast<const float*>(b), static_cast<float*>(y), rows,
+                           f, eps);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// BERT embedding: v = tok[id] + pos[s] + type[0], then layer norm (one wave
+// per token).
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void embed_bert_kernel(const int32_t* __restrict__ ids, const T* __restrict__ tok,
+                                  const T* __restrict__ pos, const T* __restrict__ type, const T* __restrict__ g,
+                                  const T* __restrict__ b, T* __restrict__ y, int64_t rows, int seq, int f,
+                                  float eps) {
+    const int lane = threadIdx.x & 63;
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * (blockDim.x / 64) + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    const int sidx = static_cast<int>(row % seq);
+    const T* tr = tok + static_cast<int64_t>(ids[row]) * f;
+    const T* pr = pos + static_cast<int64_t>(sidx) * f;
+    float v[LN_MAXV];
+#pragma unroll
+    for (int i = 0; i < LN_MAXV; ++i) {
+        const int col = lane + i * 64;
+        v[i] = col < f ? (to_f(tr[col]) + to_f(pr[col])) + to_f(type[col]) : 0.0f;
+    }
+    ln_row<T>(v, f, lane, g, b, eps, y + row * f);
+}
+
+hipError_t launch_embed_bert(const int32_t* ids, const void* tok, const void* pos, const void* type, const void* g,
+                             const void* b, void* y, int batch, int seq, int f, float eps, int dtype,
+                             hipStream_t s) {
+    const int64_t rows = static_cast<int64_t>(batch) * seq;
+    if (dtype == MOPAR_BF16)
+        hipLaunchKernelGGL(embed_bert_kernel<__bf16>, dim3(blocks_for(rows, 4)), dim3(256), 0, s, ids,
+                           static_cast<const __bf16*>(tok), static_cast<const __bf16*>(pos),
+                           static_cast<const __bf16*>(type), static_cast<const __bf16*>(g),
+                           static_cast<const __bf16*>(b), static_cast<__bf16*>(y), rows, seq, f, eps);
+    else
+        hipLaunchKernelGGL(embed_bert_kernel<float>, dim3(blocks_for(rows, 4)), dim3(256), 0, s, ids,
+                           static_cast<const float*>(tok), static_cast<const float*>(pos),
+                           static_cast<const float*>(type), static_cast<const float*>(g),
+                           static_cast<const float*>(b), static_cast<float*>(y), rows, seq, f, eps);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Plain embedding gather: one thread per 16-byte chunk of an output row.
+// ---------------------------------------------------------------------------
+__global__ void embed_kernel(const int32_t* __restrict__ ids, const uint4* __restrict__ table,
+                             uint4* __restrict__ y, int64_t rows, int chunks) {
+    const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (t >= rows * chunks) return;
+    const int64_t row = t / chunks;
+    const int c = static_cast<int>(t - row * chunks);
+    y[t] = table[static_cast<int64_t>(ids[row]) * chunks + c];
+}
+
+hipError_t launch_embed(const int32_t* ids, const void* table, void* y, int64_t n, int f, int dtype,
+                        hipStream_t s) {
+    const int chunks = static_cast<int>(f * dtype_size(dtype) / 16);
+    hipLaunchKernelGGL(embed_kernel, dim3(blocks_for(n * chunks, 256)), dim3(256), 0, s, ids,
+                       static_cast<const uint4*>(table), static_cast<uint4*>(y), n, chunks);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Multi-head self-attention, head dim 64, seq <= 128.  One block per (b, h):
+// K and V of the head staged in LDS as fp32; one thread per query row runs
+// the softmax online (running max and normaliser) and accumulates P.V in
+// registers.  Scores and probabilities never leave registers.
+// ---------------------------------------------------------------------------
+constexpr int ATT_D = 64;
+constexpr int ATT_MAXS = 128;
+
+template <typename T>
+__global__ __launch_bounds__(ATT_MAXS) void attention_kernel(const T* __restrict__ qkv, T* __restrict__ y, int seq,
+                                                             int heads, float scale) {
+    __shared__ float ks[ATT_MAXS][ATT_D];   // read as broadcasts: no padding needed
+    __shared__ float vs[ATT_MAXS][ATT_D];
+    const int b = blockIdx.x / heads, h = blockIdx.x % heads;
+    const int f = heads * ATT_D;
+    const T* base = qkv + static_cast<int64_t>(b) * seq * 3 * f;
+    for (int idx = threadIdx.x; idx < seq * ATT_D; idx += blockDim.x) {
+        const int r = idx / ATT_D, e = idx % ATT_D;
+        ks[r][e] = to_f(base[static_cast<int64_t>(r) * 3 * f + f + h * ATT_D + e]);
+        vs[r][e] = to_f(base[static_cast<int64_t>(r) * 3 * f + 2 * f + h * ATT_D + e]);
+    }
+    __syncthreads();
+    const int i = threadIdx.x;
+    if (i >= seq) return;
+    float q[ATT_D], o[ATT_D];
+    const T* qr = base + static_cast<int64_t>(i) * 3 * f + h * ATT_D;
+#pragma unroll
+    for (int e = 0; e < ATT_D; ++e) {
+        q[e] = to_f(qr[e]);
+        o[e] = 0.0f;
+    }
+    float mx = -INFINITY, den = 0.0f;
+    for (int jj = 0; jj < seq; ++jj) {
+        float sc = 0.0f;
+#pragma unroll
+        for (int e = 0; e < ATT_D; ++e) sc += q[e] * ks[jj][e];
+        sc *= scale;
+        const float mnew = fmaxf(mx, sc);
+        const float corr = __expf(mx - mnew);
+        const float pj = __expf(sc - mnew);
+        den = den * corr + pj;
+#pragma unroll
+        for (int e = 0; e < ATT_D; ++e) o[e] = o[e] * corr + pj * vs[jj][e];
+        mx = mnew;
+    }
+    const float inv = 1.0f / den;
+    T* yr = y + (static_cast<int64_t>(b) * seq + i) * f + h * ATT_D;
+#pragma unroll
+    for (int e = 0; e < ATT_D; ++e) yr[e] = from_f<T>(o[e] * inv);
+}
+
+hipError_t launch_attention(const void* qkv, void* y, int batch, int seq, int heads, float scale, int dtype,
+                            hipStream_t s) {
+    if (dtype == MOPAR_BF16)
+        hipLaunchKernelGGL(attention_kernel<__bf16>, dim3(batch * heads), dim3(ATT_MAXS), 0, s,
+                           static_cast<const __bf16*>(qkv), static_cast<__bf16*>(y), seq, heads, scale);
+    else
+        hipLaunchKernelGGL(attention_kernel<float>, dim3(batch * heads), dim3(ATT_MAXS), 0, s,
+                           static_cast<const float*>(qkv), static_cast<float*>(y), seq, heads, scale);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Raw copy (the lossless boundary codec) and zero fill, 16-byte vectors with a
+// byte tail.
+// ---------------------------------------------------------------------------
+__global__ void copy_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst, int64_t n16) {
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n16;
+         i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+        dst[i] = src[i];
+}
+__global__ void copy_tail_kernel(const unsigned char* src, unsigned char* dst, int64_t n) {
+    const int64_t i = threadIdx.x;
+    if (i < n) dst[i] = src[i];
+}
+__global__ void fill_zero_kernel(uint4* __restrict__ dst, int64_t n16) {
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n16;
+         i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+        dst[i] = make_uint4(0, 0, 0, 0);
+}
+__global__ void fill_zero_tail_kernel(unsigned char* dst, int64_t n) {
+    const int64_t i = threadIdx.x;
+    if (i < n) dst[i] = 0;
+}
+
+static unsigned stream_blocks(int64_t n16) {
+    int64_t b = (n16 + 255) / 256;
+    if (b > 256 * 16) b = 256 * 16;     // grid-stride beyond 16 blocks per CU
+    return static_cast<unsigned>(b < 1 ? 1 : b);
+}
+
+hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s) {
+    const int64_t n16 = static_cast<int64_t>(bytes / 16);
+    if (n16 > 0)
+        hipLaunchKernelGGL(copy_kernel, dim3(stream_blocks(n16)), dim3(256), 0, s, static_cast<const uint4*>(src),
+                           static_cast<uint4*>(dst), n16);
+    const int64_t tail = static_cast<int64_t>(bytes % 16);
+    if (tail)
+        hipLaunchKernelGGL(copy_tail_kernel, dim3(1), dim3(16), 0, s,
+                           static_cast<const unsigned char*>(src) + n16 * 16,
+                           static_cast<unsigned char*>(dst) + n16 * 16, tail);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
+    const int64_t n16 = static_cast<int64_t>(bytes / 16);
+    if (n16 > 0)
+        hipLaunchKernelGGL(fill_zero_kernel, dim3(stream_blocks(n16)), dim3(256), 0, s, static_cast<uint4*>(p), n16);
+    const int64_t tail = static_cast<int64_t>(bytes % 16);
+    if (tail)
+        hipLaunchKernelGGL(fill_zero_tail_kernel, dim3(1), dim3(16), 0, s,
+                           static_cast<unsigned char*>(p) + n16 * 16, tail);
+    return hipGetLastError();
+}
+
+size_t dtype_size(int dtype) { return dtype == MOPAR_BF16 ? 2 : 4; }
+
+}  // namespace mopar

@@ -1,0 +1,756 @@
+// Model description, service profile (Eq. 1-4), workspace layout and the
+// sliced executor: slices run op by op on one stream, RD ops as k
+// sub-slices of one launch, and slice boundaries pass through the codec.
+#include <algorithm>
+#include <cmath>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+namespace mopar {
+
+int plan_slices_impl(const mopar_layer_profile* L, int32_t n, const mopar_plan_opts* o, mopar_plan* out);
+
+namespace {
+
+constexpr double kPeakBf16 = 2.5e15, kPeakF32 = 157.3e12, kPeakBytes = 8.0e12;
+
+int64_t numel(const mopar_tensor_desc& t) {
+    int64_t n = 1;
+    for (int i = 0; i < t.rank; ++i) n *= t.dims[i];
+    return n;
+}
+
+size_t elt_bytes(int dtype) { return dtype == MOPAR_BF16 ? 2 : 4; }
+
+int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+struct TempReq {
+    size_t bytes;
+};
+
+}  // namespace
+
+struct OpInfo {
+    int cs = 0;                    // conv: input channel storage stride (padded for the model input)
+    bool input_is_model = false;   // conv: reads the NCHW float32 model input
+    int64_t K = 0, M = 0;          // GEMM sizes (conv / linear)
+    std::vector<size_t> temps;     // scratch buffers needed while this op runs
+    std::vector<size_t> temp_off;  // their workspace offsets
+};
+
+}  // namespace mopar
+
+struct mopar_model_s {
+    int dtype;
+    std::vector<mopar_tensor_desc> tensors;
+    std::vector<mopar_op> ops;
+    std::vector<mopar::OpInfo> info;
+    int n_layers;
+    int input, output;
+    const unsigned char* weights;
+    size_t weights_bytes;
+    std::vector<int> layer_first, layer_last;   // op index range per planning node
+    std::vector<int> layer_out;                 // tensor leaving each node
+    std::vector<size_t> offset;                 // workspace offset per tensor (SIZE_MAX: not in ws)
+    size_t ws_bytes;
+};
+
+namespace mopar {
+namespace {
+
+
+bool shape_eq(const mopar_tensor_desc& t, std::initializer_list<int64_t> d) {
+    if (t.rank != static_cast<int>(d.size())) return false;
+    int i = 0;
+    for (int64_t v : d)
+        if (t.dims[i++] != v) return false;
+    return true;
+}
+
+std::string op_name(const mopar_model_s& m, int i) {
+    return "op " + std::to_string(i) + " (kind " + std::to_string(m.ops[i].kind) + ")";
+}
+
+// parameter element count of an op (logical shapes; conv counts C, not the padded Cs)
+int64_t param_elems(const mopar_model_s& m, const mopar_op& op) {
+    const auto& in = m.tensors[op.in0];
+    switch (op.kind) {
+        case MOPAR_OP_CONV: return static_cast<int64_t>(op.n_out) * in.dims[1] * op.kh * op.kw + op.n_out;
+        case MOPAR_OP_LINEAR: {
+            const int64_t K = in.rank == 4 ? in.dims[1] * in.dims[2] * in.dims[3] : in.dims[in.rank - 1];
+            return static_cast<int64_t>(op.n_out) * K + op.n_out;
+        }
+        case MOPAR_OP_LAYERNORM: return 2 * in.dims[in.rank - 1];
+        case MOPAR_OP_EMBED_BERT: {
+            const int64_t f = m.tensors[op.out].dims[2];
+            return (op.rows[0] + op.rows[1] + op.rows[2]) * f + 2 * f;
+        }
+        case MOPAR_OP_EMBED: return op.rows[0] * m.tensors[op.out].dims[2];
+        case MOPAR_OP_LSTM: {
+            const int64_t e = in.dims[2], h = op.n_out;
+            return 4 * h * e + 4 * h * h + 8 * h;
+        }
+        default: return 0;
+    }
+}
+
+}  // namespace
+
+// Operator profile: memory = bytes of parameters + inputs + output; time =
+// max(FLOP / peak, bytes / HBM bandwidth); FLOP only for contractions.
+static void op_profile(const mopar_model_s& m, const mopar_op& op, double* mem, double* time) {
+    const int64_t pb = param_elems(m, op) * static_cast<int64_t>(elt_bytes(m.dtype));
+    int64_t ib = numel(m.tensors[op.in0]) * static_cast<int64_t>(elt_bytes(m.tensors[op.in0].dtype));
+    if (op.in1 >= 0) ib += numel(m.tensors[op.in1]) * static_cast<int64_t>(elt_bytes(m.tensors[op.in1].dtype));
+    const auto& o = m.tensors[op.out];
+    const int64_t ob = numel(o) * static_cast<int64_t>(elt_bytes(o.dtype));
+    const auto& in = m.tensors[op.in0];
+    int64_t flop = 0;
+    switch (op.kind) {
+        case MOPAR_OP_CONV: flop = 2 * numel(o) * in.dims[1] * op.kh * op.kw; break;
+        case MOPAR_OP_LINEAR: {
+            const int64_t K = in.rank == 4 ? in.dims[1] * in.dims[2] * in.dims[3] : in.dims[in.rank - 1];
+            flop = 2 * numel(o) * K;
+            break;
+        }
+        case MOPAR_OP_ATTENTION: flop = 4 * o.dims[0] * o.dims[1] * o.dims[1] * o.dims[2]; break;
+        case MOPAR_OP_LSTM: flop = 2 * o.dims[0] * o.dims[1] * 4 * o.dims[2] * (in.dims[2] + o.dims[2]); break;
+        default: break;
+    }
+    *mem = static_cast<double>(pb + ib + ob);
+    const double peak = m.dtype == MOPAR_BF16 ? kPeakBf16 : kPeakF32;
+    *time = std::fmax(static_cast<double>(flop) / peak, *mem / kPeakBytes);
+}
+
+int model_profile_impl(const mopar_model_s* m, mopar_layer_profile* out) {
+    if (!m || !out) return set_error(MOPAR_E_ARG, "mopar_model_profile: null argument");
+    for (int l = 0; l < m->n_layers; ++l) {
+        double mc = 0.0, tc = 0.0;
+        std::map<int, std::vector<std::pair<int, int>>> at_pos;   // pos -> (branch, op)
+        int rdw = 0;
+        for (int i = m->layer_first[l]; i <= m->layer_last[l]; ++i) {
+            const auto& op = m->ops[i];
+            if (op.rd) rdw = rdw == 0 ? op.n_out : std::min(rdw, op.n_out);
+            if (op.branch == 0) {
+                double mm, tt;
+                op_profile(*m, op, &mm, &tt);
+                mc = std::fmax(mc, mm);
+                tc = tc + tt;
+            } else {
+                at_pos[op.pos].push_back({op.branch, i});
+            }
+        }
+        double mb = 0.0, tb = 0.0;
+        for (auto& kv : at_pos) {                    // positions ascending
+            auto v = kv.second;
+            std::stable_sort(v.begin(), v.end(), [](auto a, auto b) { return a.first < b.first; });
+            double sm = 0.0, mt = 0.0;
+            for (auto& bo : v) {
+                double mm, tt;
+                op_profile(*m, m->ops[bo.second], &mm, &tt);
+                sm = sm + mm;
+                mt = std::fmax(mt, tt);
+            }
+            mb = std::fmax(mb, sm);
+            tb = tb + mt;
+        }
+        const auto& t = m->tensors[m->layer_out[l]];
+        out[l].mem_bytes = std::fmax(mc, mb);
+        out[l].time_s = tc + tb;
+        out[l].out_bytes = static_cast<double>(numel(t) * static_cast<int64_t>(elt_bytes(t.dtype)));
+        out[l].rd_width = rdw;
+        out[l].reserved = 0;
+    }
+    return MOPAR_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Validation and workspace layout
+// ---------------------------------------------------------------------------
+
+static int validate_and_build(mopar_model_s& m) {
+    const int nt = static_cast<int>(m.tensors.size());
+    const int epc = m.dtype == MOPAR_BF16 ? 8 : 4;       // channel granule of the GEMM loads
+    const size_t es = elt_bytes(m.dtype);
+    auto tid_ok = [&](int t) { return t >= 0 && t < nt; };
+    if (!tid_ok(m.input) || !tid_ok(m.output) || m.input == m.output)
+        return set_error(MOPAR_E_ARG, "model: bad input/output tensor id");
+    for (int t = 0; t < nt; ++t) {
+        const auto& d = m.tensors[t];
+        if (d.rank < 1 || d.rank > 4) return set_error(MOPAR_E_SHAPE, "tensor " + std::to_string(t) + ": rank");
+        for (int i = 0; i < d.rank; ++i)
+            if (d.dims[i] < 1) return set_error(MOPAR_E_SHAPE, "tensor " + std::to_string(t) + ": dims must be >= 1");
+        if (d.dtype != m.dtype && !(t == m.input && (d.dtype == MOPAR_F32 || d.dtype == MOPAR_I32)))
+            return set_error(MOPAR_E_DTYPE, "tensor " + std::to_string(t) + ": dtype must be the model dtype");
+    }
+    std::vector<int> producer(nt, -1);
+    int prev_layer = -1;
+    m.layer_first.assign(m.n_layers, -1);
+    m.layer_last.assign(m.n_layers, -1);
+    m.info.assign(m.ops.size(), OpInfo{});
+    auto wcheck = [&](int64_t off, int64_t elems, const std::string& what) -> bool {
+        if (off < 0 || off % 16 != 0) return false;
+        const int64_t bytes = elems * static_cast<int64_t>(es);
+        return static_cast<uint64_t>(off) + static_cast<uint64_t>(bytes) <= m.weights_bytes;
+        (void)what;
+    };
+    for (int i = 0; i < static_cast<int>(m.ops.size()); ++i) {
+        const auto& op = m.ops[i];
+        auto& inf = m.info[i];
+        const std::string nm = op_name(m, i);
+        if (op.layer < 0 || op.layer >= m.n_layers || op.layer < prev_layer)
+            return set_error(MOPAR_E_ARG, nm + ": layer index out of range or decreasing");
+        if (op.layer != prev_layer) {
+            if (op.layer != prev_layer + 1) return set_error(MOPAR_E_ARG, nm + ": a planning node has no ops");
+            m.layer_first[op.layer] = i;
+        }
+        m.layer_last[op.layer] = i;
+        prev_layer = op.layer;
+        if (op.branch < 0 || (op.branch > 0 && op.pos < 1)) return set_error(MOPAR_E_ARG, nm + ": branch/pos");
+        if (!tid_ok(op.in0) || !tid_ok(op.out) || (op.in1 != -1 && !tid_ok(op.in1)))
+            return set_error(MOPAR_E_ARG, nm + ": tensor id out of range");
+        if (producer[op.out] != -1 || op.out == m.input)
+            return set_error(MOPAR_E_ARG, nm + ": output tensor written twice");
+        for (int t : {op.in0, op.in1}) {
+            if (t < 0) continue;
+            if (t != m.input && producer[t] < 0)
+                return set_error(MOPAR_E_ARG, nm + ": reads a tensor before it is produced");
+            // single-input planning nodes: every op reads tensors of its own node, or the
+            // tensor leaving the previous node (or the model input for node 0)
+            if (t == m.input) {
+                if (op.layer != 0) return set_error(MOPAR_E_ARG, nm + ": only node 0 may read the model input");
+            } else {
+                const int pl = m.ops[producer[t]].layer;
+                if (pl != op.layer && !(pl == op.layer - 1 && t == m.ops[m.layer_last[pl]].out))
+                    return set_error(MOPAR_E_ARG, nm + ": reads a tensor that does not cross the node boundary");
+            }
+        }
+        if (op.in1 >= 0 && op.kind != MOPAR_OP_CONV && op.kind != MOPAR_OP_LINEAR && op.kind != MOPAR_OP_LAYERNORM)
+            return set_error(MOPAR_E_ARG, nm + ": second input only for conv, linear, layernorm");
+        if (op.act < 0 || op.act > 2) return set_error(MOPAR_E_ARG, nm + ": act");
+        if (op.rd && op.kind != MOPAR_OP_CONV && op.kind != MOPAR_OP_LINEAR)
+            return set_error(MOPAR_E_ARG, nm + ": only conv and linear ops can be resource-dominant");
+        const auto& x = m.tensors[op.in0];
+        const auto& y = m.tensors[op.out];
+        const bool xin = op.in0 == m.input;
+        if (xin && x.dtype == MOPAR_I32 && op.kind != MOPAR_OP_EMBED && op.kind != MOPAR_OP_EMBED_BERT)
+            return set_error(MOPAR_E_DTYPE, nm + ": token ids feed only embeddings");
+        if (xin && x.dtype == MOPAR_F32 && m.dtype == MOPAR_BF16 && op.kind != MOPAR_OP_CONV)
+            return set_error(MOPAR_E_UNSUPPORTED, nm + ": a float32 image input feeds only a conv");
+        switch (op.kind) {
+            case MOPAR_OP_CONV: {
+                if (x.rank != 4 || op.kh < 1 || op.kw < 1 || op.stride < 1 || op.pad < 0 || op.n_out < 1)
+                    return set_error(MOPAR_E_SHAPE, nm + ": conv geometry");
+                const int64_t ho = (x.dims[2] + 2 * op.pad - op.kh) / op.stride + 1;
+                const int64_t wo = (x.dims[3] + 2 * op.pad - op.kw) / op.stride + 1;
+                if (ho < 1 || wo < 1 || !shape_eq(y, {x.dims[0], op.n_out, ho, wo}))
+                    return set_error(MOPAR_E_SHAPE, nm + ": conv output shape");
+                if (op.in1 >= 0 && !shape_eq(m.tensors[op.in1], {x.dims[0], op.n_out, ho, wo}))
+                    return set_error(MOPAR_E_SHAPE, nm + ": residual shape");
+                inf.input_is_model = xin;
+                if (xin && x.dtype != MOPAR_F32) return set_error(MOPAR_E_DTYPE, nm + ": image input must be f32");
+                if (!xin && x.dims[1] % epc != 0)
+                    return set_error(MOPAR_E_UNSUPPORTED, nm + ": input channels must be a multiple of " +
+                                                              std::to_string(epc));
+                inf.cs = static_cast<int>(xin ? round_up(x.dims[1], epc) : x.dims[1]);
+                inf.K = static_cast<int64_t>(op.kh) * op.kw * inf.cs;
+                inf.M = x.dims[0] * ho * wo;
+                if (!wcheck(op.w, op.n_out * inf.K, "w") || !wcheck(op.b, op.n_out, "b"))
+                    return set_error(MOPAR_E_ARG, nm + ": weight offsets out of range or not 16-byte aligned");
+                if (xin) inf.temps.push_back(static_cast<size_t>(x.dims[0] * x.dims[2] * x.dims[3] * inf.cs) * es);
+                break;
+            }
+            case MOPAR_OP_LINEAR: {
+                const int64_t K = x.rank == 4 ? x.dims[1] * x.dims[2] * x.dims[3] : x.dims[x.rank - 1];
+                const int64_t M = numel(x) / K;
+                if (op.n_out < 1 || numel(y) != M * op.n_out || y.dims[y.rank - 1] != op.n_out)
+                    return set_error(MOPAR_E_SHAPE, nm + ": linear output shape");
+                if (x.rank != 4 && (y.rank != x.rank || !std::equal(x.dims, x.dims + x.rank - 1, y.dims)))
+                    return set_error(MOPAR_E_SHAPE, nm + ": linear leading dims");
+                if (op.in1 >= 0 && numel(m.tensors[op.in1]) != numel(y))
+                    return set_error(MOPAR_E_SHAPE, nm + ": residual shape");
+                if (K % epc != 0) return set_error(MOPAR_E_UNSUPPORTED, nm + ": K must be a multiple of " + std::to_string(epc));
+                inf.K = K;
+                inf.M = M;
+                if (!wcheck(op.w, op.n_out * K, "w") || !wcheck(op.b, op.n_out, "b"))
+                    return set_error(MOPAR_E_ARG, nm + ": weight offsets out of range or not 16-byte aligned");
+                break;
+            }
+            case MOPAR_OP_MAXPOOL: {
+                if (x.rank != 4 || op.kh < 1 || op.kh != op.kw || op.stride < 1 || op.pad < 0 || 2 * op.pad > op.kh)
+                    return set_error(MOPAR_E_SHAPE, nm + ": pool geometry (square window, pad <= k/2)");
+                const int64_t ho = (x.dims[2] + 2 * op.pad - op.kh) / op.stride + 1;
+                const int64_t wo = (x.dims[3] + 2 * op.pad - op.kw) / op.stride + 1;
+                if (!shape_eq(y, {x.dims[0], x.dims[1], ho, wo}))
+                    return set_error(MOPAR_E_SHAPE, nm + ": pool output shape");
+                if (x.dims[1] % epc != 0) return set_error(MOPAR_E_UNSUPPORTED, nm + ": channels granule");
+                break;
+            }
+            case MOPAR_OP_AVGPOOL:
+                if (x.rank != 4 || !shape_eq(y, {x.dims[0], x.dims[1]}))
+                    return set_error(MOPAR_E_SHAPE, nm + ": avgpool shapes");
+                break;
+            case MOPAR_OP_LAYERNORM: {
+                const int64_t f = x.dims[x.rank - 1];
+                if (numel(y) != numel(x) || y.dims[y.rank - 1] != f) return set_error(MOPAR_E_SHAPE, nm + ": LN shapes");
+                if (op.in1 >= 0 && numel(m.tensors[op.in1]) != numel(x)) return set_error(MOPAR_E_SHAPE, nm + ": LN residual");
+                if (f > 2048) return set_error(MOPAR_E_UNSUPPORTED, nm + ": LN width > 2048");
+                if (!wcheck(op.w, f, "g") || !wcheck(op.b, f, "b"))
+                    return set_error(MOPAR_E_ARG, nm + ": weight offsets out of range or not 16-byte aligned");
+                break;
+            }
+            case MOPAR_OP_ATTENTION: {
+                if (x.rank != 3 || op.heads < 1 || x.dims[2] != 3 * 64 * static_cast<int64_t>(op.heads) ||
+                    !shape_eq(y, {x.dims[0], x.dims[1], 64 * static_cast<int64_t>(op.heads)}))
+                    return set_error(MOPAR_E_SHAPE, nm + ": attention needs (B,S,3*64*heads) -> (B,S,64*heads)");
+                if (x.dims[1] > 128) return set_error(MOPAR_E_UNSUPPORTED, nm + ": attention seq > 128");
+                break;
+            }
+            case MOPAR_OP_EMBED_BERT: {
+                if (!xin || x.dtype != MOPAR_I32 || x.rank != 2 || y.rank != 3 || y.dims[0] != x.dims[0] ||
+                    y.dims[1] != x.dims[1])
+                    return set_error(MOPAR_E_SHAPE, nm + ": embedding needs ids (B,S) -> (B,S,F)");
+                const int64_t f = y.dims[2];
+                if (op.rows[0] < 1 || op.rows[1] < x.dims[1] || op.rows[2] < 1 || f > 2048)
+                    return set_error(MOPAR_E_SHAPE, nm + ": table rows (positions must cover seq)");
+                if (!wcheck(op.w, op.rows[0] * f, "tok") || !wcheck(op.w2, op.rows[1] * f, "pos") ||
+                    !wcheck(op.w3, op.rows[2] * f, "type") || !wcheck(op.w4, f, "g") || !wcheck(op.w5, f, "b"))
+                    return set_error(MOPAR_E_ARG, nm + ": weight offsets out of range or not 16-byte aligned");
+                break;
+            }
+            case MOPAR_OP_EMBED: {
+                if (!xin || x.dtype != MOPAR_I32 || y.rank != x.rank + 1 || y.dims[0] != x.dims[0])
+                    return set_error(MOPAR_E_SHAPE, nm + ": embedding needs ids -> (..., F)");
+                const int64_t f = y.dims[y.rank - 1];
+                if ((f * static_cast<int64_t>(es)) % 16 != 0) return set_error(MOPAR_E_UNSUPPORTED, nm + ": row bytes % 16");
+                if (op.rows[0] < 1 || !wcheck(op.w, op.rows[0] * f, "table"))
+                    return set_error(MOPAR_E_ARG, nm + ": weight offsets out of range or not 16-byte aligned");
+                break;
+            }
+            case MOPAR_OP_LSTM: {
+                if (x.rank != 3 || op.n_out < 1 || !shape_eq(y, {x.dims[0], x.dims[1], op.n_out}))
+                    return set_error(MOPAR_E_SHAPE, nm + ": LSTM (B,T,E) -> (B,T,H)");
+                const int64_t e = x.dims[2], h = op.n_out;
+                if (e % epc != 0 || h % epc != 0) return set_error(MOPAR_E_UNSUPPORTED, nm + ": E and H granule");
+                if (!wcheck(op.w, 4 * h * e, "w_ih") || !wcheck(op.w2, 4 * h * h, "w_hh") || !wcheck(op.b, 4 * h, "b_ih") ||
+                    !wcheck(op.w3, 4 * h, "b_hh"))
+                    return set_error(MOPAR_E_ARG, nm + ": weight offsets out of range or not 16-byte aligned");
+                const int64_t bt = x.dims[0] * x.dims[1];
+                inf.temps.push_back(static_cast<size_t>(bt * 4 * h) * 4);       // input projection, f32
+                inf.temps.push_back(static_cast<size_t>(x.dims[0] * h) * 4);    // cell state, f32
+                inf.temps.push_back(static_cast<size_t>(x.dims[0] * h) * es);   // h_0 = 0
+                break;
+            }
+            default: return set_error(MOPAR_E_ARG, nm + ": unknown op kind");
+        }
+        producer[op.out] = i;
+    }
+    if (prev_layer != m.n_layers - 1) return set_error(MOPAR_E_ARG, "model: a planning node has no ops");
+    if (producer[m.output] != static_cast<int>(m.ops.size()) - 1)
+        return set_error(MOPAR_E_ARG, "model: the output must be produced by the last op");
+    m.layer_out.resize(m.n_layers);
+    for (int l = 0; l < m.n_layers; ++l) m.layer_out[l] = m.ops[m.layer_last[l]].out;
+
+    // workspace: every tensor except the model input and output gets a slot, live from
+    // its producer to its last reader; op scratch lives for its op.  First-fit reuse.
+    std::vector<int> last_use(nt, -1);
+    for (int i = 0; i < static_cast<int>(m.ops.size()); ++i)
+        for (int t : {m.ops[i].in0, m.ops[i].in1})
+            if (t >= 0) last_use[t] = i;
+    struct Block { size_t off, size; int until; };
+    std::vector<Block> live;
+    size_t top = 0;
+    auto alloc = [&](size_t bytes, int until) {
+        bytes = (bytes + 255) / 256 * 256;
+        std::sort(live.begin(), live.end(), [](const Block& a, const Block& b) { return a.off < b.off; });
+        size_t cur = 0;
+        for (const auto& b : live) {
+            if (b.off >= cur + bytes) break;
+            cur = std::max(cur, b.off + b.size);
+        }
+        live.push_back({cur, bytes, until});
+        top = std::max(top, cur + bytes);
+        return cur;
+    };
+    m.offset.assign(nt, SIZE_MAX);
+    for (int i = 0; i < static_cast<int>(m.ops.size()); ++i) {
+        live.erase(std::remove_if(live.begin(), live.end(), [&](const Block& b) { return b.until < i; }), live.end());
+        auto& inf = m.info[i];
+        inf.temp_off.clear();
+        for (size_t tb : inf.temps) inf.temp_off.push_back(alloc(tb, i));
+        const int t = m.ops[i].out;
+        if (t != m.output) {
+            const size_t bytes = static_cast<size_t>(numel(m.tensors[t])) * es;
+            m.offset[t] = alloc(bytes, std::max(last_use[t], i));
+        }
+    }
+    m.ws_bytes = top;
+    return MOPAR_OK;
+}
+
+int model_create_impl(const mopar_model_desc* d, const void* weights, size_t wbytes, mopar_model_t* out) {
+    if (!d || !out) return set_error(MOPAR_E_ARG, "mopar_model_create: null argument");
+    *out = nullptr;
+    if (d->dtype != MOPAR_F32 && d->dtype != MOPAR_BF16)
+        return set_error(MOPAR_E_DTYPE, "mopar_model_create: model dtype must be f32 or bf16");
+    if (d->n_tensors < 2 || !d->tensors || d->n_ops < 1 || !d->ops || d->n_layers < 1)
+        return set_error(MOPAR_E_ARG, "mopar_model_create: empty model");
+    if (!weights && wbytes) return set_error(MOPAR_E_ARG, "mopar_model_create: null weights");
+    auto* m = new mopar_model_s();
+    m->dtype = d->dtype;
+    m->tensors.assign(d->tensors, d->tensors + d->n_tensors);
+    m->ops.assign(d->ops, d->ops + d->n_ops);
+    m->n_layers = d->n_layers;
+    m->input = d->input;
+    m->output = d->output;
+    m->weights = static_cast<const unsigned char*>(weights);
+    m->weights_bytes = wbytes;
+    const int rc = validate_and_build(*m);
+    if (rc != MOPAR_OK) {
+        delete m;
+        return rc;
+    }
+    *out = m;
+    return MOPAR_OK;
+}
+
+void model_destroy_impl(mopar_model_t m) { delete m; }
+
+// ---------------------------------------------------------------------------
+// Plans against a model
+// ---------------------------------------------------------------------------
+
+static int check_plan(const mopar_model_s* m, const mopar_plan* p, const char* who) {
+    if (!m || !p || !p->slice_end || !p->k) return set_error(MOPAR_E_ARG, std::string(who) + ": null model or plan");
+    if (p->n_layers != m->n_layers) return set_error(MOPAR_E_ARG, std::string(who) + ": plan is for another model");
+    if (p->n_slices < 1 || p->n_slices > m->n_layers) return set_error(MOPAR_E_ARG, std::string(who) + ": n_slices");
+    int prev = -1;
+    for (int s = 0; s < p->n_slices; ++s) {
+        if (p->slice_end[s] <= prev || p->slice_end[s] >= m->n_layers)
+            return set_error(MOPAR_E_ARG, std::string(who) + ": slice_end must increase");
+        prev = p->slice_end[s];
+    }
+    if (prev != m->n_layers - 1) return set_error(MOPAR_E_ARG, std::string(who) + ": last slice must end at the last node");
+    for (int l = 0; l < m->n_layers; ++l) {
+        int minw = 0;
+        for (int i = m->layer_first[l]; i <= m->layer_last[l]; ++i)
+            if (m->ops[i].rd) minw = minw == 0 ? m->ops[i].n_out : std::min(minw, m->ops[i].n_out);
+        if (p->k[l] < 1 || (p->k[l] > 1 && (minw == 0 || p->k[l] > minw)))
+            return set_error(MOPAR_E_ARG, std::string(who) + ": k[" + std::to_string(l) + "] invalid for that node");
+    }
+    return MOPAR_OK;
+}
+
+int workspace_bytes_impl(const mopar_model_s* m, const mopar_plan* p, size_t* bytes) {
+    if (!bytes) return set_error(MOPAR_E_ARG, "mopar_model_workspace_bytes: null output");
+    const int rc = check_plan(m, p, "mopar_model_workspace_bytes");
+    if (rc) return rc;
+    *bytes = m->ws_bytes;
+    return MOPAR_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Execution
+// ---------------------------------------------------------------------------
+
+struct Ptrs {
+    const mopar_model_s* m;
+    unsigned char* ws;
+    const void* in_ptr;   // pointer bound to tensor in_tid
+    int in_tid;
+    void* out_ptr;        // pointer bound to tensor out_tid
+    int out_tid;
+    void* get(int t) const {
+        if (t == in_tid) return const_cast<void*>(in_ptr);
+        if (t == out_tid) return out_ptr;
+        return ws + m->offset[t];
+    }
+};
+
+static const void* W(const mopar_model_s& m, int64_t off) { return off < 0 ? nullptr : m.weights + off; }
+
+static hipError_t run_op(const mopar_model_s& m, int i, const Ptrs& P, int ksub, hipStream_t s) {
+    const auto& op = m.ops[i];
+    const auto& inf = m.info[i];
+    const auto& x = m.tensors[op.in0];
+    const auto& y = m.tensors[op.out];
+    const int dt = m.dtype;
+    switch (op.kind) {
+        case MOPAR_OP_CONV: {
+            const void* src = P.get(op.in0);
+            if (inf.input_is_model) {
+                void* tmp = P.ws + inf.temp_off[0];
+                hipError_t e = launch_nchw_to_nhwc(static_cast<const float*>(src), tmp, static_cast<int>(x.dims[0]),
+                                                   static_cast<int>(x.dims[1]), static_cast<int>(x.dims[2]),
+                                                   static_cast<int>(x.dims[3]), inf.cs, dt, s);
+                if (e != hipSuccess) return e;
+                src = tmp;
+            }
+            GemmParams g{};
+            g.A = src;
+            g.conv = 1;
+            g.img_h = static_cast<int>(x.dims[2]);
+            g.img_w = static_cast<int>(x.dims[3]);
+            g.cs = inf.cs;
+            g.out_h = static_cast<int>(y.dims[2]);
+            g.out_w = static_cast<int>(y.dims[3]);
+            g.kh = op.kh;
+            g.kw = op.kw;
+            g.stride = op.stride;
+            g.pad = op.pad;
+            g.B = W(m, op.w);
+            g.bias = W(m, op.b);
+            g.res = op.in1 >= 0 ? P.get(op.in1) : nullptr;
+            g.C = P.get(op.out);
+            g.ldc = op.n_out;
+            g.M = inf.M;
+            g.N = op.n_out;
+            g.K = static_cast<int>(inf.K);
+            g.act = op.act;
+            g.ksub = ksub;
+            return launch_gemm(g, dt, s);
+        }
+        case MOPAR_OP_LINEAR: {
+            GemmParams g{};
+            g.A = P.get(op.in0);
+            g.lda = inf.K;
+            g.B = W(m, op.w);
+            g.bias = W(m, op.b);
+            g.res = op.in1 >= 0 ? P.get(op.in1) : nullptr;
+            g.C = P.get(op.out);
+            g.ldc = op.n_out;
+            g.M = inf.M;
+            g.N = op.n_out;
+            g.K = static_cast<int>(inf.K);
+            g.act = op.act;
+            g.ksub = ksub;
+            return launch_gemm(g, dt, s);
+        }
+        case MOPAR_OP_MAXPOOL:
+            return launch_maxpool(P.get(op.in0), P.get(op.out), static_cast<int>(x.dims[0]), static_cast<int>(x.dims[2]),
+                                  static_cast<int>(x.dims[3]), static_cast<int>(x.dims[1]), op.kh, op.stride, op.pad,
+                                  static_cast<int>(y.dims[2]), static_cast<int>(y.dims[3]), dt, s);
+        case MOPAR_OP_AVGPOOL:
+            return launch_avgpool(P.get(op.in0), P.get(op.out), static_cast<int>(x.dims[0]),
+                                  static_cast<int>(x.dims[2] * x.dims[3]), static_cast<int>(x.dims[1]), dt, s);
+        case MOPAR_OP_LAYERNORM: {
+            const int64_t f = x.dims[x.rank - 1];
+            return launch_layernorm(P.get(op.in0), op.in1 >= 0 ? P.get(op.in1) : nullptr, W(m, op.w), W(m, op.b),
+                                    P.get(op.out), numel(x) / f, static_cast<int>(f), op.eps, dt, s);
+        }
+        case MOPAR_OP_ATTENTION:
+            return launch_attention(P.get(op.in0), P.get(op.out), static_cast<int>(x.dims[0]),
+                                    static_cast<int>(x.dims[1]), op.heads, op.scale, dt, s);
+        case MOPAR_OP_EMBED_BERT:
+            return launch_embed_bert(static_cast<const int32_t*>(P.get(op.in0)), W(m, op.w), W(m, op.w2), W(m, op.w3),
+                                     W(m, op.w4), W(m, op.w5), P.get(op.out), static_cast<int>(x.dims[0]),
+                                     static_cast<int>(x.dims[1]), static_cast<int>(y.dims[2]), op.eps, dt, s);
+        case MOPAR_OP_EMBED:
+            return launch_embed(static_cast<const int32_t*>(P.get(op.in0)), W(m, op.w), P.get(op.out), numel(x),
+                                static_cast<int>(y.dims[y.rank - 1]), dt, s);
+        case MOPAR_OP_LSTM: {
+            const int B = static_cast<int>(x.dims[0]), T = static_cast<int>(x.dims[1]), E = static_cast<int>(x.dims[2]);
+            const int H = op.n_out;
+            float* gx = reinterpret_cast<float*>(P.ws + inf.temp_off[0]);
+            float* cst = reinterpret_cast<float*>(P.ws + inf.temp_off[1]);
+            void* h0 = P.ws + inf.temp_off[2];
+            hipError_t e = launch_fill_zero(cst, static_cast<size_t>(B) * H * 4, s);
+            if (e == hipSuccess) e = launch_fill_zero(h0, static_cast<size_t>(B) * H * dtype_size(dt), s);
+            if (e != hipSuccess) return e;
+            // input projection for all steps: gx = x W_ih^T + b_ih + b_hh (float32)
+            GemmParams g{};
+            g.A = P.get(op.in0);
+            g.lda = E;
+            g.B = W(m, op.w);
+            g.bias = W(m, op.b);
+            g.bias2 = W(m, op.w3);
+            g.C = gx;
+            g.ldc = 4 * H;
+            g.M = static_cast<int64_t>(B) * T;
+            g.N = 4 * H;
+            g.K = E;
+            g.ksub = 1;
+            g.out_f32 = 1;
+            e = launch_gemm(g, dt, s);
+            if (e != hipSuccess) return e;
+            // recurrence: one GEMM per step with the cell update fused in its epilogue
+            unsigned char* hseq = static_cast<unsigned char*>(P.get(op.out));
+            const size_t es = dtype_size(dt);
+            for (int t = 0; t < T; ++t) {
+                GemmParams r{};
+                r.A = t == 0 ? h0 : hseq + static_cast<size_t>(t - 1) * H * es;
+                r.lda = t == 0 ? H : static_cast<int64_t>(T) * H;
+                r.B = W(m, op.w2);
+                r.C = hseq + static_cast<size_t>(t) * H * es;
+                r.ldc = static_cast<int64_t>(T) * H;
+                r.M = B;
+                r.N = 4 * H;
+                r.K = H;
+                r.ksub = 1;
+                r.epi = EPI_LSTM;
+                r.gx = gx + static_cast<size_t>(t) * 4 * H;
+                r.ldgx = static_cast<int64_t>(T) * 4 * H;
+                r.cstate = cst;
+                e = launch_gemm(r, dt, s);
+                if (e != hipSuccess) return e;
+            }
+            return hipSuccess;
+        }
+        default: return hipErrorInvalidValue;
+    }
+}
+
+static int run_layers(const mopar_model_s& m, const mopar_plan& p, int l0, int l1, const Ptrs& P, hipStream_t s) {
+    for (int l = l0; l <= l1; ++l)
+        for (int i = m.layer_first[l]; i <= m.layer_last[l]; ++i) {
+            const int ksub = m.ops[i].rd ? p.k[l] : 1;
+            const hipError_t e = run_op(m, i, P, ksub, s);
+            if (e != hipSuccess) return hip_check(e, "kernel launch");
+        }
+    return MOPAR_OK;
+}
+
+int slice_forward_impl(const mopar_model_s* m, const mopar_plan* p, int32_t s, const void* in, void* out, void* ws,
+                       size_t ws_bytes, void* stream) {
+    int rc = check_plan(m, p, "mopar_slice_forward");
+    if (rc) return rc;
+    if (s < 0 || s >= p->n_slices) return set_error(MOPAR_E_ARG, "mopar_slice_forward: slice index out of range");
+    if (!in || !out) return set_error(MOPAR_E_ARG, "mopar_slice_forward: null input or output");
+    if (m->ws_bytes && (!ws || ws_bytes < m->ws_bytes))
+        return set_error(MOPAR_E_WORKSPACE, "mopar_slice_forward: workspace smaller than mopar_model_workspace_bytes");
+    const int l0 = s == 0 ? 0 : p->slice_end[s - 1] + 1, l1 = p->slice_end[s];
+    Ptrs P{m, static_cast<unsigned char*>(ws), in, s == 0 ? m->input : m->layer_out[l0 - 1], out, m->layer_out[l1]};
+    return run_layers(*m, *p, l0, l1, P, static_cast<hipStream_t>(stream));
+}
+
+// ---------------------------------------------------------------------------
+// Boundary codec
+// ---------------------------------------------------------------------------
+
+static int codec_geometry(const mopar_codec* c, const mopar_tensor_desc* x, int64_t* positions, int* channels,
+                          const char* who) {
+    if (!c || !x) return set_error(MOPAR_E_ARG, std::string(who) + ": null codec or descriptor");
+    if (x->rank < 1 || x->rank > 4) return set_error(MOPAR_E_SHAPE, std::string(who) + ": rank");
+    for (int i = 0; i < x->rank; ++i)
+        if (x->dims[i] < 1) return set_error(MOPAR_E_SHAPE, std::string(who) + ": dims must be >= 1");
+    if (x->dtype != MOPAR_F32 && x->dtype != MOPAR_BF16) return set_error(MOPAR_E_DTYPE, std::string(who) + ": dtype");
+    const int64_t ch = x->rank == 4 ? x->dims[1] : x->dims[x->rank - 1];
+    *channels = static_cast<int>(ch);
+    *positions = numel(*x) / ch;
+    if (c->kind == MOPAR_CODEC_RAW) return MOPAR_OK;
+    if (c->kind != MOPAR_CODEC_AE) return set_error(MOPAR_E_ARG, std::string(who) + ": codec kind");
+    if (c->c != ch) return set_error(MOPAR_E_SHAPE, std::string(who) + ": codec channels differ from the tensor's");
+    const int g = x->dtype == MOPAR_BF16 ? 8 : 4;   // 16-byte granule of the GEMM loads
+    if (c->c_code < 1 || c->c % g != 0 || c->c_code % g != 0)
+        return set_error(MOPAR_E_UNSUPPORTED, std::string(who) + ": c and c_code must be multiples of " +
+                                                  std::to_string(g));
+    if (!c->w_enc || !c->w_dec) return set_error(MOPAR_E_ARG, std::string(who) + ": null codec weights");
+    return MOPAR_OK;
+}
+
+int code_bytes_impl(const mopar_codec* c, const mopar_tensor_desc* x, size_t* bytes) {
+    int64_t pos;
+    int ch;
+    if (!bytes) return set_error(MOPAR_E_ARG, "mopar_boundary_code_bytes: null output");
+    const int rc = codec_geometry(c, x, &pos, &ch, "mopar_boundary_code_bytes");
+    if (rc) return rc;
+    const int64_t per = c->kind == MOPAR_CODEC_RAW ? ch : c->c_code;
+    *bytes = static_cast<size_t>(pos * per) * elt_bytes(x->dtype);
+    return MOPAR_OK;
+}
+
+static hipError_t codec_apply(const mopar_codec& c, int dtype, int64_t pos, int ch, const void* src, void* dst,
+                              bool encode, hipStream_t s) {
+    if (c.kind == MOPAR_CODEC_RAW) return launch_copy(src, dst, static_cast<size_t>(pos * ch) * elt_bytes(dtype), s);
+    GemmParams g{};
+    g.A = src;
+    g.lda = encode ? c.c : c.c_code;
+    g.B = encode ? c.w_enc : c.w_dec;
+    g.bias = encode ? c.b_enc : c.b_dec;
+    g.C = dst;
+    g.ldc = encode ? c.c_code : c.c;
+    g.M = pos;
+    g.N = encode ? c.c_code : c.c;
+    g.K = encode ? c.c : c.c_code;
+    g.ksub = 1;
+    return launch_gemm(g, dtype, s);
+}
+
+int encode_impl(const mopar_codec* c, const mopar_tensor_desc* x, const void* xd, void* code, void* stream) {
+    int64_t pos;
+    int ch;
+    int rc = codec_geometry(c, x, &pos, &ch, "mopar_boundary_encode");
+    if (rc) return rc;
+    if (!xd || !code) return set_error(MOPAR_E_ARG, "mopar_boundary_encode: null device pointer");
+    return hip_check(codec_apply(*c, x->dtype, pos, ch, xd, code, true, static_cast<hipStream_t>(stream)),
+                     "mopar_boundary_encode");
+}
+
+int decode_impl(const mopar_codec* c, const mopar_tensor_desc* y, const void* code, void* yd, void* stream) {
+    int64_t pos;
+    int ch;
+    int rc = codec_geometry(c, y, &pos, &ch, "mopar_boundary_decode");
+    if (rc) return rc;
+    if (!yd || !code) return set_error(MOPAR_E_ARG, "mopar_boundary_decode: null device pointer");
+    return hip_check(codec_apply(*c, y->dtype, pos, ch, code, yd, false, static_cast<hipStream_t>(stream)),
+                     "mopar_boundary_decode");
+}
+
+// ---------------------------------------------------------------------------
+// Whole model
+// ---------------------------------------------------------------------------
+
+int model_forward_impl(const mopar_model_s* m, const mopar_plan* p, const mopar_codec* codecs, const void* in,
+                       void* out, void* const* code_bufs, void* ws, size_t ws_bytes, void* stream) {
+    int rc = check_plan(m, p, "mopar_model_forward");
+    if (rc) return rc;
+    if (!in || !out) return set_error(MOPAR_E_ARG, "mopar_model_forward: null input or output");
+    if (m->ws_bytes && (!ws || ws_bytes < m->ws_bytes))
+        return set_error(MOPAR_E_WORKSPACE, "mopar_model_forward: workspace smaller than mopar_model_workspace_bytes");
+    const int S = p->n_slices;
+    if (S > 1 && (!codecs || !code_bufs)) return set_error(MOPAR_E_ARG, "mopar_model_forward: codecs / code buffers");
+    // validate every codec against its boundary before enqueuing anything
+    for (int s = 0; s + 1 < S; ++s) {
+        const auto& t = m->tensors[m->layer_out[p->slice_end[s]]];
+        int64_t pos;
+        int ch;
+        rc = codec_geometry(&codecs[s], &t, &pos, &ch, "mopar_model_forward");
+        if (rc) return rc;
+        if (!code_bufs[s]) return set_error(MOPAR_E_ARG, "mopar_model_forward: null code buffer");
+    }
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    Ptrs P{m, static_cast<unsigned char*>(ws), in, m->input, out, m->output};
+    int l0 = 0;
+    for (int s = 0; s < S; ++s) {
+        const int l1 = p->slice_end[s];
+        if (s > 0) {   // decode the previous boundary into this slice's input
+            const int bt = m->layer_out[l0 - 1];
+            const auto& t = m->tensors[bt];
+            int64_t pos;
+            int ch;
+            codec_geometry(&codecs[s - 1], &t, &pos, &ch, "mopar_model_forward");
+            rc = hip_check(codec_apply(codecs[s - 1], t.dtype, pos, ch, code_bufs[s - 1], P.get(bt), false, st),
+                           "boundary decode");
+            if (rc) return rc;
+        }
+        rc = run_layers(*m, *p, l0, l1, P, st);
+        if (rc) return rc;
+        if (s + 1 < S) {   // encode this slice's output into the boundary buffer
+            const int bt = m->layer_out[l1];
+            const auto& t = m->tensors[bt];
+            int64_t pos;
+            int ch;
+            codec_geometry(&codecs[s], &t, &pos, &ch, "mopar_model_forward");
+            rc = hip_check(codec_apply(codecs[s], t.dtype, pos, ch, P.get(bt), code_bufs[s], true, st),
+                           "boundary encode");
+            if (rc) return rc;
+        }
+        l0 = l1 + 1;
+    }
+    return MOPAR_OK;
+}
+
+}  // namespace mopar

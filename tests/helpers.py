@@ -1,0 +1,37 @@
+"""Shared helpers of the test suite: small model builders and the error metric."""
+import numpy as np
+
+import synth
+
+# Shrunken variants of the five workloads: every kernel path of the full-size
+# model, several tiles and a ragged tail, and a CPU oracle that finishes in
+# seconds.  Channel counts at the cuts keep C / 8 a multiple of the codec granule.
+SMALL = {
+    1: dict(hw=16),
+    2: dict(batch=2, hw=64, blocks=(1, 2, 2, 1), widths=(16, 32, 32, 64), n_cls=37),
+    3: dict(batch=2, hw=64, arch=(16, "M", 32, "M", 64, 64, "M", 64, "M", 128, "M"), fc=(200, 96), n_cls=37,
+            cut_after_pools=(3, 5)),
+    4: dict(batch=2, seq=40, layers=3, hidden=128, heads=2, ffn=256, vocab=300, max_pos=64, slice_every=1),
+    5: dict(batch=3, seq=9, hidden=64, emb=64, vocab=301),
+}
+
+
+def rel_err(got, ref):
+    """max |got - ref| / max |ref| over the tensor (the per-tensor relative error)."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    den = np.abs(ref).max()
+    return float(np.abs(got - ref).max() / (den if den > 0 else 1.0))
+
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def codec_ratios(model, cuts):
+    """Ratio 8 where the code width stays a multiple of the 16-byte granule, else 4."""
+    g = 8 if model.dtype == "bf16" else 4
+    out = []
+    for li in cuts:
+        c = synth.boundary_channels(model, li)
+        out.append(8 if (c % 8 == 0 and (c // 8) % g == 0) else 4)
+    return out

@@ -1,0 +1,169 @@
+"""Host-side checks of the HIP library (no GPU): it loads, exports every symbol
+of include/mopar.h, and its host logic (planner, profile, sub-slice ranges,
+validation) agrees with the oracle bit for bit.  No kernel is launched."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from oracle import plan as OP
+
+P = pytest.importorskip("paper_2404_02445_amd")
+from paper_2404_02445_amd import _lib as L  # noqa: E402
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_library_exports_every_header_symbol():
+    hdr = open(os.path.join(ROOT, "include", "mopar.h")).read()
+    names = set(re.findall(r"^\s*(?:int|void|const char\*)\s+(mopar_\w+)\s*\(", hdr, re.M))
+    assert len(names) >= 13
+    assert names == set(L.SIGNATURES)
+    lib = P.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+    assert b"gfx950" in lib.mopar_version()
+
+
+def test_subslice_range_matches_oracle():
+    for n in [1, 5, 16, 64, 301, 4096]:
+        for k in range(1, min(n, 9) + 1):
+            for j in range(k):
+                assert P.mopar_subslice_range(n, k, j) == oracle.subslice_range(n, k, j)
+    for bad in [(4, 5, 0), (4, 0, 0), (4, 2, 2), (4, 2, -1)]:
+        with pytest.raises(P.MoparError):
+            P.mopar_subslice_range(*bad)
+
+
+def _rand_prof(rng, n):
+    return [(rng.uniform(1, 100), rng.uniform(0.1, 10), rng.uniform(1, 1000), int(rng.integers(0, 3)) * 32)
+            for _ in range(n)]
+
+
+@pytest.mark.parametrize("n", [1, 2, 4, 7, 12, 21])
+def test_planner_bitwise_equal_to_oracle(n):
+    rng = np.random.default_rng(n)
+    for trial in range(40):
+        prof = _rand_prof(rng, n)
+        lp = [OP.LayerProfile(*p) for p in prof]
+        kmax = int(rng.integers(1, 5))
+        kw = dict(n_slices=int(rng.integers(0, n + 1)), elim_tau=[-1.0, 0.05, 0.3][trial % 3],
+                  c_m=float(rng.uniform(0.5, 2)), c_n=float(rng.uniform(0, 3)), bw=float(rng.uniform(1, 100)),
+                  ratio=[float(rng.choice([1, 8, 64])) for _ in range(n - 1)] if trial % 2 else None,
+                  k_max=kmax, lambda_bytes=float(rng.choice([0.0, 20.0])))
+        if trial % 4 == 1:
+            kw["allowed_cut"] = [int(v) for v in rng.integers(0, 2, n - 1)]
+        if trial % 5 == 2:
+            kw["tp_table"] = rng.uniform(0.1, 5, (n, kmax)).tolist()
+            kw["ta_table"] = rng.uniform(0, 1, (n, kmax)).tolist()
+        opts = OP.PlanOpts(**{k: v for k, v in kw.items() if k != "bw"}, bw=kw["bw"])
+        try:
+            want = OP.plan_slices(lp, opts)
+        except OP.Infeasible:
+            with pytest.raises(P.MoparError) as ei:
+                P.mopar_plan_slices(prof, **kw)
+            assert ei.value.status == L.MOPAR_E_INFEASIBLE
+            continue
+        got = P.mopar_plan_slices(prof, **kw)
+        assert got.slice_end == want.slice_end
+        assert got.k == want.k
+        assert got.cost == want.cost and got.t_tau == want.t_tau and got.t_unsplit == want.t_unsplit
+        assert got.latency_ok == want.latency_ok
+
+
+def test_planner_error_paths():
+    prof = [(10.0, 1.0, 5.0, 0), (20.0, 1.0, 5.0, 64)]
+    with pytest.raises(P.MoparError) as e:
+        P.mopar_plan_slices(prof, k_override=[2, 0])        # k on a node without an RD op
+    assert e.value.status == L.MOPAR_E_ARG
+    with pytest.raises(P.MoparError) as e:
+        P.mopar_plan_slices(prof, k_override=[0, 65])       # wider than the RD op
+    assert e.value.status == L.MOPAR_E_ARG
+    with pytest.raises(P.MoparError) as e:
+        P.mopar_plan_slices(prof, n_slices=2, allowed_cut=[0])
+    assert e.value.status == L.MOPAR_E_INFEASIBLE
+    with pytest.raises(P.MoparError):
+        P.mopar_plan_slices([(0.0, 1.0, 1.0, 0)])           # zero memory footprint
+    with pytest.raises(P.MoparError):
+        P.mopar_plan_slices(prof, bw=0.0)
+    assert P.mopar_plan_slices(prof, n_slices=2).slice_end == [0, 1]
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_model_profile_and_plan_equal_oracle(cfg):
+    kw = {} if cfg != 3 else dict(batch=2, hw=64)
+    m = synth.build(cfg, **kw)
+    sm = P.SlicedModel(m, device="cpu")          # create validates and plans; nothing runs
+    got = sm.profile()
+    want = OP.layer_profiles(m)
+    assert [tuple(g) for g in got] == [(w.mem_bytes, w.time_s, w.out_bytes, w.rd_width) for w in want]
+    s = m.slicing
+    pl = sm.plan()
+    po = OP.plan_slices(want, OP.PlanOpts(n_slices=s["n_slices"], allowed_cut=s["allowed_cut"],
+                                          elim_tau=s["elim_tau"], k_override=s["k_override"]))
+    assert (pl.slice_end, pl.k, pl.cost, pl.t_tau) == (po.slice_end, po.k, po.cost, po.t_tau)
+    assert sm.workspace_bytes(pl) > 0
+
+
+def test_model_create_validation_errors():
+    m = synth.build(1)
+    tens, ops, blob = P.binding._pack(m)
+    host = np.zeros(blob.size, dtype=np.uint8)
+
+    def create(ops_arr, n_layers=len(m.layers), wbytes=blob.size, output=m.output_tid):
+        d = L.ModelDesc()
+        d.dtype = L.MOPAR_F32
+        d.n_tensors, d.tensors = len(m.tensors), ctypes.cast(tens, ctypes.POINTER(L.TensorDesc))
+        d.n_ops, d.ops = len(m.ops), ctypes.cast(ops_arr, ctypes.POINTER(L.Op))
+        d.n_layers, d.input, d.output = n_layers, m.input_tid, output
+        h = ctypes.c_void_p()
+        st = P.lib().mopar_model_create(ctypes.byref(d), host.ctypes.data_as(ctypes.c_void_p), wbytes,
+                                        ctypes.byref(h))
+        if st == 0:
+            P.lib().mopar_model_destroy(h)
+        return st
+
+    assert create(ops) == 0
+    bad = (L.Op * len(m.ops))(*ops)
+    bad[1].w = blob.size                           # weight offset past the blob
+    assert create(bad) == L.MOPAR_E_ARG
+    bad = (L.Op * len(m.ops))(*ops)
+    bad[0].n_out = 17                              # output shape no longer matches
+    assert create(bad) == L.MOPAR_E_SHAPE
+    bad = (L.Op * len(m.ops))(*ops)
+    bad[3].in0 = bad[5].out                        # reads a tensor before it is produced
+    assert create(bad) == L.MOPAR_E_ARG
+    bad = (L.Op * len(m.ops))(*ops)
+    bad[2].rd = 1                                  # a pool cannot be an RD op
+    assert create(bad) == L.MOPAR_E_ARG
+    assert create(ops, n_layers=len(m.layers) + 1) == L.MOPAR_E_ARG
+    assert create(ops, wbytes=16) == L.MOPAR_E_ARG
+    assert b"op" in P.lib().mopar_last_error()
+
+
+def test_plan_model_mismatch_rejected():
+    m = synth.build(1)
+    sm = P.SlicedModel(m, device="cpu")
+    bad = P.make_plan(len(m.layers), [3, 9], [1] * len(m.layers))
+    bad.raw.k[2] = 2                               # k > 1 on a pool node
+    with pytest.raises(P.MoparError):
+        sm.workspace_bytes(bad)
+    bad2 = P.make_plan(len(m.layers), [5, 4, 9], [1] * len(m.layers))
+    with pytest.raises(P.MoparError):
+        sm.workspace_bytes(bad2)
+
+
+def test_codec_code_bytes_host_only():
+    raw = P.make_codec("raw")
+    assert P.mopar_boundary_code_bytes(raw, (8, 256, 56, 56), "bf16") == 8 * 256 * 56 * 56 * 2
+    ae = L.Codec()
+    ae.kind, ae.c, ae.c_code, ae.w_enc, ae.w_dec = L.CODEC_AE, 256, 32, 16, 16   # non-null dummies
+    assert P.mopar_boundary_code_bytes(ae, (8, 256, 56, 56), "bf16") == 8 * 32 * 56 * 56 * 2
+    assert P.mopar_boundary_code_bytes(ae, (32, 128, 256), "bf16") == 32 * 128 * 32 * 2
+    ae.c = 128
+    with pytest.raises(P.MoparError):
+        P.mopar_boundary_code_bytes(ae, (8, 256, 56, 56), "bf16")
