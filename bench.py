@@ -1,0 +1,248 @@
+"""Benchmark of the sliced-inference hot path on one MI355X.
+
+Workload (default): ResNet-50-shaped CNN, bf16, batch 8, 3x224x224 inputs,
+cut into 4 slices at the stage boundaries, every bottleneck's 3x3 conv (the
+resource-dominant op) split into k = 4 sub-slices, autoencoder codecs with
+R = 8 at the 3 boundaries.  One step = one pass of the whole hot path over one
+batch: the layer profile and the partitioning plan (host), then the sliced
+forward pass with boundary encode/decode (device).
+
+Prints one JSON line.  Options: --steps K --warmup W --gpus N (only 1).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+PEAK_HBM_GBS = 8000.0
+
+
+def op_flops(m, op):
+    """Algorithmic FLOP of a contraction op (2 x multiply-adds), 0 otherwise."""
+    T = m.tensors
+    out = T[op["out"]]["shape"]
+    n_out = 1
+    for s in out:
+        n_out *= s
+    k = op["kind"]
+    if k == "conv":
+        return 2 * n_out * T[op["inputs"][0]]["shape"][1] * op["kh"] * op["kw"]
+    if k == "linear":
+        return 2 * n_out * op["nin"]
+    return 0
+
+
+def numel(shape):
+    n = 1
+    for s in shape:
+        n *= s
+    return n
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=2, help="workload 1..5 (default 2: ResNet-50, batch 8)")
+    ap.add_argument("--codec", choices=["ae", "raw"], default="ae")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle CPU baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-op-timing", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="also run a raw boundary copy of this many MiB per step (counter calibration)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(slices and sub-slices run on one device); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2404_02445_amd as P
+    import synth
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    m = synth.build(args.config)
+    x_host = synth.make_input(m)
+    sm = P.SlicedModel(m, device=dev)
+    s = m.slicing
+    plan_kw = dict(n_slices=s["n_slices"], allowed_cut=s["allowed_cut"], elim_tau=s["elim_tau"],
+                   k_override=s["k_override"])
+    plan = sm.plan()
+    cuts = plan.slice_end[:-1]
+    cw = synth.make_codec_weights(m, cuts, ratio=m.codec_ratio) if args.codec == "ae" else None
+    codecs, keep = sm.codecs(plan, args.codec, cw)
+    codes = sm.alloc_codes(plan, codecs)
+    ws = sm.alloc_workspace(plan)
+    out = sm.alloc_output()
+    x = torch.from_numpy(x_host).to(dev)
+    stream = torch.cuda.current_stream()
+    calib = None
+    if args.calibrate_copy_mib:
+        nb = args.calibrate_copy_mib << 20
+        calib = (torch.empty(nb, dtype=torch.uint8, device=dev), torch.empty(nb, dtype=torch.uint8, device=dev))
+
+    def step():
+        prof = sm.profile()                                   # a1-a2: layer profiles (Eq. 1-4)
+        pl = P.mopar_plan_slices(prof, **plan_kw)             # a3-a4: HyPAD plan and sub-slice counts
+        sm.forward(pl, x, out, codecs, codes, ws)             # a5-a10: sliced forward with codec hand-off
+        return pl
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # --- timed region: exactly K steps ------------------------------------------------
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    evs[0].record(stream)
+    for i in range(args.steps):
+        step()
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
+    total_ms = evs[0].elapsed_time(evs[-1])
+    ms_per_step = total_ms / args.steps
+    value = m.batch * args.steps / (total_ms / 1e3)
+
+    # planning cost on the host (already inside the steps above, overlapped with the GPU)
+    tp0 = time.perf_counter()
+    for _ in range(20):
+        P.mopar_plan_slices(sm.profile(), **plan_kw)
+    plan_us = (time.perf_counter() - tp0) / 20 * 1e6
+
+    res = {
+        "metric": "inferences/s per sliced model at 1 GPU; RD-op MFMA util %; boundary codec GB/s",
+        "value": round(value, 2),
+        "unit": "inferences/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": m.dtype,
+        "data": "synthetic (seeded N(0,1) inputs, random-init weights of the named architecture)",
+        "config": {"workload": f"{m.name}: {m.dtype}, batch {m.batch}, {plan.n_slices} slices at "
+                               f"{cuts}, RD k={max(plan.k)}, {args.codec} codec"
+                               + (f" R={m.codec_ratio}" if args.codec == "ae" else ""),
+                   "batch": m.batch, "slices": plan.n_slices, "k": plan.k, "codec": args.codec},
+        "latency_ms": {"p50": round(statistics.median(per_step), 4),
+                       "p95": round(float(np.percentile(per_step, 95)), 4)},
+        "wall_s_timed_region": round(wall, 4),
+        "host_plan_us": round(plan_us, 1),
+    }
+
+    # --- per-op timing pass (HIP events on the launch stream, same steps) ----------------
+    if not args.no_op_timing:
+        sm.set_timing(True)
+        n_t = min(args.steps, 20)
+        gemm_ms = rd_ms = 0.0
+        gemm_fl = rd_fl = 0
+        gemm_launches = 0
+        enc_ms = [0.0] * len(cuts)
+        dec_ms = [0.0] * len(cuts)
+        bw_ms = 0.0
+        bw_bytes = 0
+        es = 2 if m.dtype == "bf16" else 4
+        for _ in range(n_t):
+            step()
+            ops_ms, cut_ms = sm.op_times()
+            for i, op in enumerate(m.ops):
+                t = ops_ms[i]
+                if op["kind"] in ("conv", "linear"):
+                    f = op_flops(m, op)
+                    gemm_ms += t
+                    gemm_fl += f
+                    gemm_launches += 1
+                    if op.get("rd"):
+                        rd_ms += t
+                        rd_fl += f
+                else:
+                    bw_ms += t
+                    ins = sum(numel(m.tensors[tt]["shape"]) for tt in op["inputs"])
+                    bw_bytes += (ins + numel(m.tensors[op["out"]]["shape"])) * es
+            for c, (e, d) in enumerate(cut_ms):
+                enc_ms[c] += e
+                dec_ms[c] += d
+        sm.set_timing(False)
+        # codec traffic: read the tensor + write the code (encode) and back (decode), weights once
+        codec = []
+        for c, li in enumerate(cuts):
+            shp = m.tensors[m.layer_output_tid(li)]["shape"]
+            tb = numel(shp) * es
+            cbytes = tb // (m.codec_ratio if args.codec == "ae" else 1)
+            wb = 0
+            if args.codec == "ae":
+                ch = synth.boundary_channels(m, li)
+                wb = (2 * ch * (ch // m.codec_ratio) + ch + ch // m.codec_ratio) * es
+            e_avg, d_avg = enc_ms[c] / n_t, dec_ms[c] / n_t
+            codec.append({"cut_after": m.layers[li], "tensor_MB": round(tb / 1e6, 3),
+                          "encode_us": round(e_avg * 1e3, 2), "decode_us": round(d_avg * 1e3, 2),
+                          "encode_GBs": round((tb + cbytes + wb / 2) / (e_avg * 1e-3) / 1e9, 1),
+                          "decode_GBs": round((tb + cbytes + wb / 2) / (d_avg * 1e-3) / 1e9, 1)})
+        gemm_avg_ms = gemm_ms / max(gemm_launches, 1)
+        achieved = gemm_fl / (gemm_ms * 1e-3) / 1e12
+        peak = PEAK_TFLOPS[m.dtype]
+        res["roofline"] = {
+            "bound": "mfma", "kernel": "gemm_kernel (all conv / linear launches of a step)",
+            "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4), "traffic": None,
+            "flop_per_launch": round(gemm_fl / max(gemm_launches, 1)),
+            "avg_launch_us": round(gemm_avg_ms * 1e3, 2),
+            "launches_per_step": gemm_launches // n_t,
+        }
+        res["rd_mfma_util"] = {"achieved_TFLOPs": round(rd_fl / (rd_ms * 1e-3) / 1e12, 2) if rd_ms else None,
+                               "frac_of_peak": round(rd_fl / (rd_ms * 1e-3) / 1e12 / peak, 4) if rd_ms else None,
+                               "rd_ms_per_step": round(rd_ms / n_t, 4)}
+        res["codec"] = codec
+        res["bandwidth_ops"] = {"ms_per_step": round(bw_ms / n_t, 4),
+                                "GBs": round(bw_bytes / (bw_ms * 1e-3) / 1e9, 1) if bw_ms else None}
+        res["gemm_ms_per_step"] = round(gemm_ms / n_t, 4)
+
+    if calib is not None:   # known-size raw copies: the reference for HBM counter scaling
+        raw = P.make_codec("raw")
+        n = calib[0].numel() // 2
+        for _ in range(3):
+            P.mopar_boundary_encode(raw, (n,), "bf16", calib[0], calib[1])
+        torch.cuda.synchronize()
+
+    # --- CPU baseline: the oracle on a bounded sample of the same workload -------------
+    if not args.no_cpu_baseline:
+        import oracle
+        cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+        os.environ.setdefault("OMP_NUM_THREADS", str(cores))
+        oracle.lib()
+        done = 0
+        t0 = time.perf_counter()
+        while True:
+            oracle.forward(m, x_host, k=plan.k, cuts=cuts, codecs=cw, sample=[done % m.batch])
+            done += 1
+            if time.perf_counter() - t0 >= args.cpu_seconds:
+                break
+        el = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": round(done / el, 4), "unit": "inferences/s", "cores": cores,
+                               "kind": "oracle",
+                               "sample": f"{done} single-image forward(s) of the same sliced workload "
+                                         f"(same plan, codecs and weights), {el:.1f} s"}
+    print(json.dumps(res))
+
+
+if __name__ == "__main__":
+    main()

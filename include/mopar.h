@@ -260,6 +260,27 @@ int mopar_model_forward(mopar_model_t model, const mopar_plan* plan, const mopar
                         const void* in_dev, void* out_dev, void* const* code_bufs, void* ws,
                         size_t ws_bytes, void* stream);
 
+/* ------------------------------------------------------------------------ */
+/* Measurement                                                               */
+/* ------------------------------------------------------------------------ */
+
+/* Per-op timing.  While enabled, every op of mopar_slice_forward /
+ * mopar_model_forward (an LSTM op counts as one, all its launches included)
+ * and every boundary encode / decode of mopar_model_forward is bracketed by
+ * two HIP events recorded on the launch stream.  Enabling creates the
+ * events (no device memory); disabling destroys them.  Not thread-safe
+ * with respect to concurrent forwards on the same model. */
+int mopar_model_set_timing(mopar_model_t model, int32_t enable);
+
+/* Number of timing slots: n_ops + 2 * (n_layers - 1).  Slot i < n_ops is op
+ * i; slot n_ops + 2*c is the encode and n_ops + 2*c + 1 the decode of cut c
+ * (the c-th split point of the last forward). */
+int mopar_model_timing_slots(mopar_model_t model, int32_t* n);
+
+/* Wait for the events of the last timed forward and write each slot's
+ * duration in milliseconds to ms[0..n-1] (-1 for slots that did not run). */
+int mopar_model_op_times(mopar_model_t model, float* ms, int32_t n);
+
 /* Description of the last error on this thread ("" when none). */
 const char* mopar_last_error(void);
 

@@ -347,6 +347,21 @@ class SlicedModel:
                                         _ptr(ws), 0 if ws is None else ws.numel(), _stream_ptr(stream)))
         return out
 
+    # -- measurement -----------------------------------------------------------
+    def set_timing(self, enable=True):
+        check(lib().mopar_model_set_timing(self.handle, 1 if enable else 0))
+
+    def op_times(self):
+        """Per-slot milliseconds of the last timed forward: (op times, [(encode, decode) per cut])."""
+        n = L.c_i32()
+        check(lib().mopar_model_timing_slots(self.handle, ctypes.byref(n)))
+        arr = (L.c_f32 * n.value)()
+        check(lib().mopar_model_op_times(self.handle, arr, n.value))
+        nops = len(self.spec.ops)
+        ops = list(arr[:nops])
+        cuts = [(arr[nops + 2 * c], arr[nops + 2 * c + 1]) for c in range((n.value - nops) // 2)]
+        return ops, [c for c in cuts if c[0] >= 0 or c[1] >= 0]
+
     def slice_forward(self, plan, s, x, out, ws, stream=None):
         check(lib().mopar_slice_forward(self.handle, ctypes.byref(plan.raw), s, _ptr(x), _ptr(out), _ptr(ws),
                                         ws.numel(), _stream_ptr(stream)))

@@ -20,6 +20,10 @@ int decode_impl(const mopar_codec*, const mopar_tensor_desc*, const void*, void*
 int model_forward_impl(const mopar_model_s*, const mopar_plan*, const mopar_codec*, const void*, void*, void* const*,
                        void*, size_t, void*);
 
+int set_timing_impl(mopar_model_s*, int32_t);
+int timing_slots_impl(const mopar_model_s*, int32_t*);
+int op_times_impl(const mopar_model_s*, float*, int32_t);
+
 static thread_local std::string g_error;
 
 int set_error(int status, const std::string& msg) {
@@ -98,6 +102,18 @@ int mopar_model_forward(mopar_model_t model, const mopar_plan* plan, const mopar
     return guarded("mopar_model_forward", [&] {
         return model_forward_impl(model, plan, codecs, in_dev, out_dev, code_bufs, ws, ws_bytes, stream);
     });
+}
+
+int mopar_model_set_timing(mopar_model_t model, int32_t enable) {
+    return guarded("mopar_model_set_timing", [&] { return set_timing_impl(model, enable); });
+}
+
+int mopar_model_timing_slots(mopar_model_t model, int32_t* n) {
+    return guarded("mopar_model_timing_slots", [&] { return timing_slots_impl(model, n); });
+}
+
+int mopar_model_op_times(mopar_model_t model, float* ms, int32_t n) {
+    return guarded("mopar_model_op_times", [&] { return op_times_impl(model, ms, n); });
 }
 
 const char* mopar_last_error(void) { return g_error.c_str(); }

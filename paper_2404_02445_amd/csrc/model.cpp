@@ -56,6 +56,13 @@ struct mopar_model_s {
     std::vector<int> layer_out;                 // tensor leaving each node
     std::vector<size_t> offset;                 // workspace offset per tensor (SIZE_MAX: not in ws)
     size_t ws_bytes;
+    // measurement: event pairs per timing slot (ops, then encode/decode per cut)
+    std::vector<hipEvent_t> ev_start, ev_stop;
+    std::vector<char> ev_used;
+    ~mopar_model_s() {
+        for (auto e : ev_start) (void)hipEventDestroy(e);
+        for (auto e : ev_stop) (void)hipEventDestroy(e);
+    }
 };
 
 namespace mopar {
@@ -603,13 +610,81 @@ static hipError_t run_op(const mopar_model_s& m, int i, const Ptrs& P, int ksub,
     }
 }
 
+// Runs `fn` (which enqueues work on s), bracketed by the events of `slot` when timing is on.
+template <typename F>
+static hipError_t timed(const mopar_model_s& mc, int slot, hipStream_t s, F&& fn) {
+    auto& m = const_cast<mopar_model_s&>(mc);
+    const bool on = !m.ev_start.empty() && slot >= 0 && slot < static_cast<int>(m.ev_start.size());
+    if (on) {
+        const hipError_t e = hipEventRecord(m.ev_start[slot], s);
+        if (e != hipSuccess) return e;
+    }
+    const hipError_t e = fn();
+    if (e != hipSuccess) return e;
+    if (on) {
+        m.ev_used[slot] = 1;
+        return hipEventRecord(m.ev_stop[slot], s);
+    }
+    return hipSuccess;
+}
+
+static void reset_timing(const mopar_model_s& mc) {
+    auto& m = const_cast<mopar_model_s&>(mc);
+    std::fill(m.ev_used.begin(), m.ev_used.end(), 0);
+}
+
 static int run_layers(const mopar_model_s& m, const mopar_plan& p, int l0, int l1, const Ptrs& P, hipStream_t s) {
     for (int l = l0; l <= l1; ++l)
         for (int i = m.layer_first[l]; i <= m.layer_last[l]; ++i) {
             const int ksub = m.ops[i].rd ? p.k[l] : 1;
-            const hipError_t e = run_op(m, i, P, ksub, s);
+            const hipError_t e = timed(m, i, s, [&] { return run_op(m, i, P, ksub, s); });
             if (e != hipSuccess) return hip_check(e, "kernel launch");
         }
+    return MOPAR_OK;
+}
+
+int set_timing_impl(mopar_model_s* m, int32_t enable) {
+    if (!m) return set_error(MOPAR_E_ARG, "mopar_model_set_timing: null model");
+    for (auto e : m->ev_start) (void)hipEventDestroy(e);
+    for (auto e : m->ev_stop) (void)hipEventDestroy(e);
+    m->ev_start.clear();
+    m->ev_stop.clear();
+    m->ev_used.clear();
+    if (!enable) return MOPAR_OK;
+    const size_t n = m->ops.size() + 2 * static_cast<size_t>(m->n_layers - 1);
+    for (size_t i = 0; i < n; ++i) {
+        hipEvent_t a, b;
+        int rc = hip_check(hipEventCreate(&a), "hipEventCreate");
+        if (rc) return rc;
+        rc = hip_check(hipEventCreate(&b), "hipEventCreate");
+        if (rc) {
+            (void)hipEventDestroy(a);
+            return rc;
+        }
+        m->ev_start.push_back(a);
+        m->ev_stop.push_back(b);
+    }
+    m->ev_used.assign(n, 0);
+    return MOPAR_OK;
+}
+
+int timing_slots_impl(const mopar_model_s* m, int32_t* n) {
+    if (!m || !n) return set_error(MOPAR_E_ARG, "mopar_model_timing_slots: null argument");
+    *n = static_cast<int32_t>(m->ops.size() + 2 * static_cast<size_t>(m->n_layers - 1));
+    return MOPAR_OK;
+}
+
+int op_times_impl(const mopar_model_s* m, float* ms, int32_t n) {
+    if (!m || !ms) return set_error(MOPAR_E_ARG, "mopar_model_op_times: null argument");
+    if (m->ev_start.empty()) return set_error(MOPAR_E_ARG, "mopar_model_op_times: timing is not enabled");
+    for (int32_t i = 0; i < n; ++i) {
+        ms[i] = -1.0f;
+        if (i >= static_cast<int32_t>(m->ev_start.size()) || !m->ev_used[i]) continue;
+        int rc = hip_check(hipEventSynchronize(m->ev_stop[i]), "hipEventSynchronize");
+        if (rc) return rc;
+        rc = hip_check(hipEventElapsedTime(&ms[i], m->ev_start[i], m->ev_stop[i]), "hipEventElapsedTime");
+        if (rc) return rc;
+    }
     return MOPAR_OK;
 }
 
@@ -623,6 +698,7 @@ int slice_forward_impl(const mopar_model_s* m, const mopar_plan* p, int32_t s, c
         return set_error(MOPAR_E_WORKSPACE, "mopar_slice_forward: workspace smaller than mopar_model_workspace_bytes");
     const int l0 = s == 0 ? 0 : p->slice_end[s - 1] + 1, l1 = p->slice_end[s];
     Ptrs P{m, static_cast<unsigned char*>(ws), in, s == 0 ? m->input : m->layer_out[l0 - 1], out, m->layer_out[l1]};
+    reset_timing(*m);
     return run_layers(*m, *p, l0, l1, P, static_cast<hipStream_t>(stream));
 }
 
@@ -723,6 +799,8 @@ int model_forward_impl(const mopar_model_s* m, const mopar_plan* p, const mopar_
     }
     const hipStream_t st = static_cast<hipStream_t>(stream);
     Ptrs P{m, static_cast<unsigned char*>(ws), in, m->input, out, m->output};
+    reset_timing(*m);
+    const int slot0 = static_cast<int>(m->ops.size());
     int l0 = 0;
     for (int s = 0; s < S; ++s) {
         const int l1 = p->slice_end[s];
@@ -732,7 +810,9 @@ int model_forward_impl(const mopar_model_s* m, const mopar_plan* p, const mopar_
             int64_t pos;
             int ch;
             codec_geometry(&codecs[s - 1], &t, &pos, &ch, "mopar_model_forward");
-            rc = hip_check(codec_apply(codecs[s - 1], t.dtype, pos, ch, code_bufs[s - 1], P.get(bt), false, st),
+            rc = hip_check(timed(*m, slot0 + 2 * (s - 1) + 1, st,
+                                 [&] { return codec_apply(codecs[s - 1], t.dtype, pos, ch, code_bufs[s - 1], P.get(bt),
+                                                          false, st); }),
                            "boundary decode");
             if (rc) return rc;
         }
@@ -744,7 +824,9 @@ int model_forward_impl(const mopar_model_s* m, const mopar_plan* p, const mopar_
             int64_t pos;
             int ch;
             codec_geometry(&codecs[s], &t, &pos, &ch, "mopar_model_forward");
-            rc = hip_check(codec_apply(codecs[s], t.dtype, pos, ch, P.get(bt), code_bufs[s], true, st),
+            rc = hip_check(timed(*m, slot0 + 2 * s, st,
+                                 [&] { return codec_apply(codecs[s], t.dtype, pos, ch, P.get(bt), code_bufs[s], true,
+                                                          st); }),
                            "boundary encode");
             if (rc) return rc;
         }

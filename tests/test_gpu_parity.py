@@ -19,6 +19,9 @@ P = pytest.importorskip("paper_2404_02445_amd")
 
 
 def _np(t):
+    """Device tensor -> numpy in canonical order (rank-4 tensors are stored channels-last)."""
+    if t.dim() == 4:
+        t = P.boundary_to_canonical(t.reshape(-1), tuple(t.shape))
     return t.float().cpu().numpy() if t.dtype == torch.bfloat16 else t.cpu().numpy()
 
 
@@ -239,8 +242,8 @@ def test_codec_ae_parity(dt, shape, ratio):
     P.mopar_boundary_decode(cd, shape, dt, code, y)
     torch.cuda.synchronize()
     cshape = (shape[0], shape[2], shape[3], c // ratio) if len(shape) == 4 else shape[:-1] + (c // ratio,)
-    code_gpu = _np(code).reshape(cshape)
-    y_gpu = _np(y).reshape(x_phys.shape)
+    code_gpu = code.float().cpu().numpy().reshape(cshape)     # physical layout, transposed below
+    y_gpu = y.float().cpu().numpy().reshape(x_phys.shape)
     if len(shape) == 4:
         code_gpu = code_gpu.transpose(0, 3, 1, 2)
         y_gpu = y_gpu.transpose(0, 3, 1, 2)
