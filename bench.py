@@ -57,6 +57,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-op-timing", action="store_true")
+    ap.add_argument("--op-report", action="store_true", help="print per-op times (ms) to stderr")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run a raw boundary copy of this many MiB per step (counter calibration)")
     args = ap.parse_args()
@@ -161,9 +162,12 @@ def main():
         bw_ms = 0.0
         bw_bytes = 0
         es = 2 if m.dtype == "bf16" else 4
+        per_op = [0.0] * len(m.ops)
         for _ in range(n_t):
             step()
             ops_ms, cut_ms = sm.op_times()
+            for i, t in enumerate(ops_ms):
+                per_op[i] += t / n_t
             for i, op in enumerate(m.ops):
                 t = ops_ms[i]
                 if op["kind"] in ("conv", "linear"):
@@ -182,6 +186,13 @@ def main():
                 enc_ms[c] += e
                 dec_ms[c] += d
         sm.set_timing(False)
+        if args.op_report:
+            for i, op in enumerate(m.ops):
+                sh = m.tensors[op["out"]]["shape"]
+                f = op_flops(m, op)
+                tf = f / (per_op[i] * 1e-3) / 1e12 if per_op[i] > 0 and f else 0.0
+                print(f"op {i:3d} {op['name']:<14} {op['kind']:<9} k={plan.k[op['layer']] if op.get('rd') else 1} "
+                      f"out={sh} {per_op[i] * 1e3:8.2f} us {tf:7.1f} TF/s", file=sys.stderr)
         # codec traffic: read the tensor + write the code (encode) and back (decode), weights once
         codec = []
         for c, li in enumerate(cuts):

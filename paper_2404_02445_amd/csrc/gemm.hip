@@ -4,45 +4,79 @@
 //
 //   C[m, n] = epilogue( sum_k A[m, k] * B[n, k] )
 //
-// A is [M][K]: either a dense row-major matrix or the im2col view of an NHWC
-// image (k runs over (r, s, c) with c fastest).  B is [N][K] row-major.
+// A is [M][K]: a dense row-major matrix or the im2col view of an NHWC image
+// (k runs over (r, s, c) with c fastest).  B is [N][K] row-major.
 //
-// Horizontal sub-slicing (the k equal-size sub-slices of an RD operator):
-// blockIdx.z selects the sub-slice, whose output columns [lo, hi) and weight
-// rows [lo, hi) follow the same split as mopar_subslice_range; each sub-slice
-// is tiled on its own and masked at hi.  The K loop -- stage depth, MFMA
-// shape, chunk order -- depends only on K and the dtype, never on the tile
-// shape or the sub-slice, so every output element goes through the same
-// sequence of fp32 operations whatever k is: sub-sliced output equals the
-// unsplit output bit for bit.
+// Horizontal sub-slicing (the k equal-size sub-slices of an RD operator): a
+// block's sub-slice index selects output columns [lo, hi) and weight rows
+// [lo, hi), split as mopar_subslice_range does; each sub-slice is tiled on its
+// own and masked at hi.  The K loop -- stage depth, MFMA shape, chunk order,
+// split-K boundaries and the order partial sums are added -- depends only on
+// (M, N, K) and the dtype, never on the tile shape or the sub-slice, so every
+// output element goes through the same fp32 operations whatever k is:
+// sub-sliced output equals the unsplit output bit for bit.
 //
-// Data path: each thread streams 16-byte chunks of A and B rows from HBM into
-// registers one stage ahead, parks them in LDS (double buffered, rows padded
-// by one chunk so the 16 lanes of an MFMA fragment read hit distinct banks),
-// and four waves run v_mfma_f32_16x16x32_bf16 (bf16) or
-// v_mfma_f32_16x16x4_f32 (fp32) on their wave tile.  The MFMA is issued with
-// the weight fragment as the first operand, so each lane ends up holding four
-// consecutive output columns of one row: bias, residual, activation, the LSTM
-// cell and the store all work on 4-wide vectors.
+// Data path.  Operands stream from HBM straight into LDS with
+// global_load_lds_dwordx4 (16 bytes per lane, no VGPR staging), NS stages deep.
+// LDS is fragment-major: for every 16-row block and 32-wide k step, the 64
+// lanes' MFMA fragments sit in one contiguous kilobyte, in lane order -- the
+// order the DMA writes them and the order ds_read_b128 reads them back, so
+// both sides are conflict-free.  Out-of-range chunks (image padding, M/N/K
+// tails) are loaded from a zero page, so every lane issues the same number of
+// loads and the wait counts are exact.  Four waves run v_mfma_f32_16x16x32_bf16
+// (bf16) or v_mfma_f32_16x16x4_f32 (fp32) on their wave tile, with the weight
+// fragment as the first operand: each lane ends up holding four consecutive
+// output columns of one row, so bias, residual, activation, the LSTM cell and
+// the store work on 4-wide vectors.
+//
+// Blocks are numbered so that the eight XCDs (which take blocks round-robin)
+// each receive a contiguous run of tiles sharing A rows, for L2 reuse.
+#include <type_traits>
+
 #include "internal.h"
 
 namespace mopar {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef const __attribute__((address_space(1))) void* gptr_t;
 
 template <typename T> struct Elt;
 template <> struct Elt<__bf16> { static constexpr int EPC = 8; };   // elements per 16-byte chunk
 template <> struct Elt<float> { static constexpr int EPC = 4; };
 
-constexpr int CH = 8;          // 16-byte chunks of each row per LDS stage (128 bytes)
-constexpr int RS = CH + 1;     // LDS row stride in chunks (one chunk of padding)
+// 16 zero bytes: the source of every out-of-range chunk.
+__device__ __attribute__((aligned(16))) const unsigned int kZeroChunk[4] = {0u, 0u, 0u, 0u};
 
 __device__ __forceinline__ float ld_f(const __bf16* p, int64_t i) {
     unsigned short u = reinterpret_cast<const unsigned short*>(p)[i];
     return __uint_as_float(static_cast<unsigned>(u) << 16);
 }
 __device__ __forceinline__ float ld_f(const float* p, int64_t i) { return p[i]; }
+
+// four consecutive elements (vector load when aligned)
+template <typename T>
+__device__ __forceinline__ void ld4(const T* p, int64_t i, int nvalid, float* v) {
+    if constexpr (sizeof(T) == 2) {
+        if (nvalid == 4 && (i & 3) == 0) {
+            const uint2 r = *reinterpret_cast<const uint2*>(p + i);
+            v[0] = __uint_as_float(r.x << 16);
+            v[1] = __uint_as_float(r.x & 0xffff0000u);
+            v[2] = __uint_as_float(r.y << 16);
+            v[3] = __uint_as_float(r.y & 0xffff0000u);
+            return;
+        }
+    } else {
+        if (nvalid == 4 && (i & 3) == 0) {
+            const f32x4 r = *reinterpret_cast<const f32x4*>(p + i);
+            v[0] = r[0], v[1] = r[1], v[2] = r[2], v[3] = r[3];
+            return;
+        }
+    }
+    for (int q = 0; q < 4; ++q) v[q] = q < nvalid ? ld_f(p, i + q) : 0.0f;
+}
 
 __device__ __forceinline__ float sigmoidf_(float v) { return 1.0f / (1.0f + __expf(-v)); }
 
@@ -53,125 +87,201 @@ __device__ __forceinline__ float act_f(float v, int act) {
 }
 
 template <typename T>
-__device__ __forceinline__ void store4(T* c, int64_t idx, const float* v, int nvalid, bool vec_ok);
-
-template <>
-__device__ __forceinline__ void store4<__bf16>(__bf16* c, int64_t idx, const float* v, int nvalid, bool vec_ok) {
-    if (nvalid == 4 && vec_ok) {
-        typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-        bf16x4 o = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
-        *reinterpret_cast<bf16x4*>(c + idx) = o;
+__device__ __forceinline__ void store4(T* c, int64_t idx, const float* v, int nvalid) {
+    if constexpr (sizeof(T) == 2) {
+        if (nvalid == 4 && (idx & 3) == 0) {
+            const bf16x4 o = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
+            *reinterpret_cast<bf16x4*>(c + idx) = o;
+            return;
+        }
     } else {
-        for (int i = 0; i < nvalid; ++i) c[idx + i] = (__bf16)v[i];
+        if (nvalid == 4 && (idx & 3) == 0) {
+            *reinterpret_cast<f32x4*>(c + idx) = f32x4{v[0], v[1], v[2], v[3]};
+            return;
+        }
+    }
+    for (int q = 0; q < nvalid; ++q) c[idx + q] = static_cast<T>(v[q]);
+}
+
+// bias, second bias, residual, activation and the store of 4 consecutive columns
+template <typename T>
+__device__ __forceinline__ void epilogue4(const GemmParams& p, int64_t m, int n, int nvalid, float* v) {
+    float t[4], bias[4] = {0.f, 0.f, 0.f, 0.f}, rsd[4] = {0.f, 0.f, 0.f, 0.f};
+    if (p.bias) ld4(static_cast<const T*>(p.bias), n, nvalid, bias);
+    if (p.bias2) {
+        ld4(static_cast<const T*>(p.bias2), n, nvalid, t);
+        for (int q = 0; q < 4; ++q) bias[q] += t[q];
+    }
+    if (p.res) ld4(static_cast<const T*>(p.res), m * p.ldc + n, nvalid, rsd);
+    for (int q = 0; q < 4; ++q) v[q] = act_f((v[q] + bias[q]) + rsd[q], p.act);
+    const int64_t idx = m * p.ldc + n;
+    if (p.out_f32)
+        store4<float>(static_cast<float*>(p.C), idx, v, nvalid);
+    else
+        store4<T>(static_cast<T*>(p.C), idx, v, nvalid);
+}
+
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+// LDS fragment reads.  They are issued as inline asm so the compiler does not
+// treat them as readers of the in-flight LDS DMA (it would otherwise drain every
+// outstanding global_load_lds before each read, collapsing the pipeline to one
+// stage); completion is awaited explicitly with lds_wait(), and pin() ties each
+// value to that wait so no use can be scheduled above it.
+__device__ __forceinline__ u32x4 lds_read16(unsigned addr) {
+    u32x4 v;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr));
+    return v;
+}
+__device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+__device__ __forceinline__ void pin(u32x4& v) { asm volatile("" : "+v"(v)); }
+
+// wait until at most `r` of this wave's stages (L loads each) are still in flight
+template <int L>
+__device__ __forceinline__ void wait_stages(int r) {
+    switch (r) {
+        case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+        case 1: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(L) : "memory"); break;
+        case 2: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * L) : "memory"); break;
+        default: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * L) : "memory"); break;
     }
 }
 
-template <>
-__device__ __forceinline__ void store4<float>(float* c, int64_t idx, const float* v, int nvalid, bool vec_ok) {
-    if (nvalid == 4 && vec_ok) {
-        *reinterpret_cast<f32x4*>(c + idx) = f32x4{v[0], v[1], v[2], v[3]};
-    } else {
-        for (int i = 0; i < nvalid; ++i) c[idx + i] = v[i];
-    }
-}
-
-template <typename T, int BM, int BN, int WM, int WN>
+template <typename T, int BM, int BN, int WM, int WN, int NS, bool CONV>
 __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
     constexpr int EPC = Elt<T>::EPC;
-    constexpr int BK = CH * EPC;              // K elements per stage
-    constexpr int TM = BM / WM, TN = BN / WN; // wave tile
-    constexpr int FM = TM / 16, FN = TN / 16; // 16x16 MFMA tiles per wave
-    constexpr int NCHUNK = (BM + BN) * CH;
-    constexpr int PER = (NCHUNK + 255) / 256;
-    static_assert(WM * WN == 4 && FM >= 1 && FN >= 1, "tile");
+    constexpr int BK = 8 * EPC;                 // K elements per stage: two 32-wide (bf16) k steps
+    constexpr int TM = BM / WM, TN = BN / WN;   // wave tile
+    constexpr int FM = TM / 16, FN = TN / 16;   // 16x16 MFMA tiles per wave
+    constexpr int NBA = BM / 16 * 2, NBB = BN / 16 * 2;
+    constexpr int NBLK = NBA + NBB;             // 1 KB fragment blocks per stage
+    constexpr int LMAX = (NBLK + 3) / 4, LMIN = NBLK / 4;
+    constexpr int STAGE = NBLK * 64;            // uint4 per stage
+    static_assert(WM * WN == 4 && FM >= 1 && FN >= 1 && NS >= 2 && NS <= 5 && LMIN >= 1, "tile");
+    static_assert((NS - 2) * LMIN <= 63, "vmcnt range");
 
-    __shared__ uint4 lds[2][(BM + BN) * RS];
+    __shared__ uint4 lds[NS * STAGE];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wm = wave / WN, wn = wave % WN;
 
-    // sub-slice j owns columns [n_lo, n_hi)
-    const int j = blockIdx.z;
+    // --- block -> (m tile, split, sub-slice, n tile), XCD-grouped -------------------------
+    const int width = (p.N + p.ksub - 1) / p.ksub;
+    const int mt = static_cast<int>((p.M + BM - 1) / BM), nt = (width + BN - 1) / BN;
+    const int total = mt * p.splits * p.ksub * nt;
+    const int per_xcd = (total + 7) / 8;
+    int t = static_cast<int>(blockIdx.x % 8) * per_xcd + static_cast<int>(blockIdx.x / 8);
+    if (t >= total) return;
+    const int nti = t % nt;
+    t /= nt;
+    const int j = t % p.ksub;
+    t /= p.ksub;
+    const int split = t % p.splits;
+    const int mti = t / p.splits;
+
     const int q = p.N / p.ksub, rr = p.N % p.ksub;
     const int n_lo = j * q + min(j, rr), n_hi = (j + 1) * q + min(j + 1, rr);
-    const int n0 = n_lo + blockIdx.y * BN;
-    if (n0 >= n_hi) return;                   // block-uniform: this tile lies past the sub-slice
-    const int64_t m0 = static_cast<int64_t>(blockIdx.x) * BM;
+    const int n0 = n_lo + nti * BN;
+    if (n0 >= n_hi) return;                     // block-uniform, before any barrier
+    const int64_t m0 = static_cast<int64_t>(mti) * BM;
+
+    const int nk = (p.K + BK - 1) / BK;
+    const int kt0 = static_cast<int>(static_cast<int64_t>(nk) * split / p.splits);
+    const int kt1 = static_cast<int>(static_cast<int64_t>(nk) * (split + 1) / p.splits);
 
     const T* __restrict__ Ap = static_cast<const T*>(p.A);
     const T* __restrict__ Bp = static_cast<const T*>(p.B);
+    const gptr_t zero = (gptr_t)(kZeroChunk);
 
-    // --- per-thread load assignment: chunk column fixed, PER rows ---------------------
-    const int col = tid % CH;
-    const T* rowptr[PER];        // dense A / B: row base; conv A: image base
-    int hb[PER], wb[PER];        // conv A: top-left input coordinate of the row's window
-    bool rvalid[PER];
-    bool is_a[PER];
+    // --- this lane's rows in the blocks its wave loads ------------------------------------
+    const int chunk_lo = lane >> 4;             // chunk within the k step
+    const T* rowp[LMAX];
+    int hb[LMAX], wb[LMAX];
+    bool rv[LMAX];
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
-        const int row = tid / CH + i * (256 / CH);
-        rvalid[i] = false;
-        is_a[i] = row < BM;
-        rowptr[i] = nullptr;
+    for (int i = 0; i < LMAX; ++i) {
+        const int blk = wave + 4 * i;
+        rv[i] = false;
+        rowp[i] = Bp;
         hb[i] = wb[i] = 0;
-        if (row >= BM + BN) continue;
-        if (row < BM) {
+        if (blk >= NBLK) continue;
+        if (blk < NBA) {
+            const int row = (blk >> 1) * 16 + (lane & 15);
             const int64_t m = m0 + row;
-            if (m >= p.M) continue;
-            rvalid[i] = true;
-            if (p.conv) {
+            rv[i] = m < p.M;
+            const int64_t mc = rv[i] ? m : 0;
+            if (CONV) {
                 const int64_t hw = static_cast<int64_t>(p.out_h) * p.out_w;
-                const int64_t img = m / hw;
-                const int rem = static_cast<int>(m - img * hw);
-                const int ho = rem / p.out_w, wo = rem - (rem / p.out_w) * p.out_w;
-                rowptr[i] = Ap + img * p.img_h * p.img_w * static_cast<int64_t>(p.cs);
+                const int64_t img = mc / hw;
+                const int rem = static_cast<int>(mc - img * hw);
+                const int ho = rem / p.out_w, wo = rem - ho * p.out_w;
+                rowp[i] = Ap + img * p.img_h * p.img_w * static_cast<int64_t>(p.cs);
                 hb[i] = ho * p.stride - p.pad;
                 wb[i] = wo * p.stride - p.pad;
             } else {
-                rowptr[i] = Ap + m * p.lda;
+                rowp[i] = Ap + mc * p.lda;
             }
         } else {
-            const int n = n0 + (row - BM);
-            if (n >= n_hi) continue;
-            rvalid[i] = true;
-            rowptr[i] = Bp + static_cast<int64_t>(n) * p.K;
+            const int row = ((blk - NBA) >> 1) * 16 + (lane & 15);
+            const int n = n0 + row;
+            rv[i] = n < n_hi;
+            rowp[i] = Bp + static_cast<int64_t>(rv[i] ? n : n0) * p.K;
         }
     }
 
-    uint4 stage[PER];
-    auto load_stage = [&](int kt) {
-        const int k = kt * BK + col * EPC;
-        const bool kin = k < p.K;
-        // conv: decompose k -> (tap row rr, tap col ss, channel ci); one chunk never
-        // straddles taps because cs is a multiple of EPC
-        int dr = 0, ds = 0, ci = 0;
-        if (p.conv && kin) {
-            const int tap = k / p.cs;
-            ci = k - tap * p.cs;
-            dr = tap / p.kw;
-            ds = tap - dr * p.kw;
-        }
+    // im2col coordinates (tap row, tap column, channel) of this lane's two chunk
+    // columns, advanced incrementally by one stage (BK = dq * cs + dc elements)
+    int tr[2] = {0, 0}, tcol[2] = {0, 0}, tci[2] = {0, 0};
+    int dq = 0, dc = 0;
+    if (CONV) {
+        dq = BK / p.cs;
+        dc = BK - dq * p.cs;
 #pragma unroll
-        for (int i = 0; i < PER; ++i) {
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (rvalid[i] && kin) {
-                if (is_a[i] && p.conv) {
-                    const int hi = hb[i] + dr, wi = wb[i] + ds;
-                    if (hi >= 0 && hi < p.img_h && wi >= 0 && wi < p.img_w)
-                        v = *reinterpret_cast<const uint4*>(
-                            rowptr[i] + (static_cast<int64_t>(hi) * p.img_w + wi) * p.cs + ci);
-                } else {
-                    v = *reinterpret_cast<const uint4*>(rowptr[i] + k);
-                }
+        for (int ks = 0; ks < 2; ++ks) {
+            const int k = kt0 * BK + (ks * 4 + chunk_lo) * EPC;
+            const int tap = k / p.cs;
+            tci[ks] = k - tap * p.cs;
+            tr[ks] = tap / p.kw;
+            tcol[ks] = tap - tr[ks] * p.kw;
+        }
+    }
+    auto advance = [&]() {
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            tci[ks] += dc;
+            int dt = dq;
+            if (tci[ks] >= p.cs) {
+                tci[ks] -= p.cs;
+                ++dt;
             }
-            stage[i] = v;
+            tcol[ks] += dt;
+            while (tcol[ks] >= p.kw) {
+                tcol[ks] -= p.kw;
+                ++tr[ks];
+            }
         }
     };
-    auto store_stage = [&](int buf) {
+
+    // issue the loads of stage kt (coordinates must be those of stage kt) into LDS buffer buf
+    auto issue = [&](int kt, int buf) {
 #pragma unroll
-        for (int i = 0; i < PER; ++i) {
-            const int row = tid / CH + i * (256 / CH);
-            if (row < BM + BN) lds[buf][row * RS + col] = stage[i];
+        for (int i = 0; i < LMAX; ++i) {
+            const int blk = wave + 4 * i;
+            if (blk >= NBLK) continue;          // wave-uniform
+            const int ks = blk & 1;
+            const int k = kt * BK + (ks * 4 + chunk_lo) * EPC;
+            bool ok = rv[i] && k < p.K;
+            const T* addr;
+            if (CONV && blk < NBA) {
+                const int hi = hb[i] + tr[ks], wi = wb[i] + tcol[ks];
+                ok = ok && static_cast<unsigned>(hi) < static_cast<unsigned>(p.img_h) &&
+                     static_cast<unsigned>(wi) < static_cast<unsigned>(p.img_w);
+                addr = rowp[i] + static_cast<int64_t>((hi * p.img_w + wi) * p.cs + tci[ks]);
+            } else {
+                addr = rowp[i] + k;
+            }
+            const gptr_t src = ok ? (gptr_t)(addr) : zero;
+            __builtin_amdgcn_global_load_lds(src, (lds_ptr_t)(&lds[buf * STAGE + blk * 64]), 16, 0, 0);
         }
     };
 
@@ -181,122 +291,276 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
 #pragma unroll
         for (int b = 0; b < FN; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int nk = (p.K + BK - 1) / BK;
-    load_stage(0);
-    store_stage(0);
-    __syncthreads();
-
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < nk) load_stage(kt + 1);
-        const uint4* L = lds[buf];
+    // --- epilogue operands, fetched now so their latency hides under the main loop ---------
+    int64_t mrow[FM];
+    int ncol[FN], nval[FN];
 #pragma unroll
-        for (int ks = 0; ks < CH / 4; ++ks) {
-            const int chunk = ks * 4 + (lane >> 4);
-            uint4 af[FM], bf[FN];
+    for (int a = 0; a < FM; ++a) mrow[a] = m0 + wm * TM + a * 16 + (lane & 15);
 #pragma unroll
-            for (int a = 0; a < FM; ++a) af[a] = L[(wm * TM + a * 16 + (lane & 15)) * RS + chunk];
-#pragma unroll
-            for (int b = 0; b < FN; ++b) bf[b] = L[(BM + wn * TN + b * 16 + (lane & 15)) * RS + chunk];
-#pragma unroll
-            for (int a = 0; a < FM; ++a)
-#pragma unroll
-                for (int b = 0; b < FN; ++b) {
-                    if constexpr (sizeof(T) == 2) {
-                        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                            __builtin_bit_cast(bf16x8, bf[b]), __builtin_bit_cast(bf16x8, af[a]), acc[a][b], 0, 0, 0);
-                    } else {
-                        const f32x4 av = __builtin_bit_cast(f32x4, af[a]);
-                        const f32x4 bv = __builtin_bit_cast(f32x4, bf[b]);
-#pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(bv[e], av[e], acc[a][b], 0, 0, 0);
-                    }
-                }
-        }
-        if (kt + 1 < nk) store_stage(buf ^ 1);
-        __syncthreads();
+    for (int b = 0; b < FN; ++b) {
+        ncol[b] = n0 + wn * TN + b * 16 + (lane >> 4) * 4;
+        nval[b] = max(0, min(4, n_hi - ncol[b]));
     }
-
-    // --- epilogue: lane holds rows m, columns n..n+3 --------------------------------------
-    const T* bias = static_cast<const T*>(p.bias);
-    const T* bias2 = static_cast<const T*>(p.bias2);
-    const T* res = static_cast<const T*>(p.res);
+    const bool direct = p.splits == 1 && p.epi == EPI_STD;   // this block finishes its outputs
+    // residual kept packed (raw bits of 4 elements) so the prefetch costs few registers
+    typedef typename std::conditional<sizeof(T) == 2, uint2, uint4>::type Raw4;
+    Raw4 rraw[FM][FN];
+    const bool have_res = direct && p.res != nullptr;
 #pragma unroll
-    for (int a = 0; a < FM; ++a) {
-        const int64_t m = m0 + wm * TM + a * 16 + (lane & 15);
-        if (m >= p.M) continue;
+    for (int a = 0; a < FM; ++a)
 #pragma unroll
         for (int b = 0; b < FN; ++b) {
-            const int n = n0 + wn * TN + b * 16 + (lane >> 4) * 4;
-            if (n >= n_hi) continue;
-            const int nvalid = min(4, n_hi - n);
-            float v[4];
+            const bool ok = have_res && mrow[a] < p.M && nval[b] == 4;
+            const int64_t idx = ok ? mrow[a] * p.ldc + ncol[b] : 0;
+            rraw[a][b] = Raw4{};
+            if (ok && (idx & 3) == 0) rraw[a][b] = *reinterpret_cast<const Raw4*>(static_cast<const T*>(p.res) + idx);
+        }
+
+    // prologue: NS-1 stages in flight (coordinates then stand at stage kt0 + NS - 1)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) v[i] = acc[a][b][i];
-            if (p.epi == EPI_LSTM) {
-                // gates i, f, g, o of unit n / 4 (n is a multiple of 4 and nvalid == 4)
-                const f32x4 g4 = *reinterpret_cast<const f32x4*>(p.gx + m * p.ldgx + n);
-                const float gi = v[0] + g4[0], gf = v[1] + g4[1], gg = v[2] + g4[2], go = v[3] + g4[3];
-                const int u = n >> 2;
-                float* cp = p.cstate + m * (p.N >> 2) + u;
-                const float c = sigmoidf_(gf) * *cp + sigmoidf_(gi) * tanhf(gg);
-                *cp = c;
-                const float h = sigmoidf_(go) * tanhf(c);
-                static_cast<T*>(p.C)[m * p.ldc + u] = static_cast<T>(h);
-                continue;
-            }
+    for (int s = 0; s < NS - 1; ++s) {
+        if (kt0 + s < kt1) issue(kt0 + s, s);
+        if (CONV) advance();
+    }
+
+    // LDS byte address of this lane's slot in fragment block 0 of stage 0
+    const unsigned lds0 = static_cast<unsigned>(reinterpret_cast<size_t>((lds_ptr_t)(&lds[0]))) + lane * 16;
+    auto read_frags = [&](unsigned sbase, int ks, u32x4 (&af)[FM], u32x4 (&bf)[FN]) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                if (i < nvalid) {
-                    if (bias) v[i] += ld_f(bias, n + i);
-                    if (bias2) v[i] += ld_f(bias2, n + i);
-                    if (res) v[i] += ld_f(res, m * p.ldc + n + i);
-                    v[i] = act_f(v[i], p.act);
+        for (int a = 0; a < FM; ++a) af[a] = lds_read16(sbase + ((((wm * TM + a * 16) >> 4) * 2 + ks) * 64) * 16);
+#pragma unroll
+        for (int b = 0; b < FN; ++b) bf[b] = lds_read16(sbase + ((NBA + ((wn * TN + b * 16) >> 4) * 2 + ks) * 64) * 16);
+    };
+    auto mfmas = [&](u32x4 (&af)[FM], u32x4 (&bf)[FN]) {
+#pragma unroll
+        for (int a = 0; a < FM; ++a)
+#pragma unroll
+            for (int b = 0; b < FN; ++b) {
+                if constexpr (sizeof(T) == 2) {
+                    acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(bf16x8, bf[b]), __builtin_bit_cast(bf16x8, af[a]), acc[a][b], 0, 0, 0);
+                } else {
+                    const f32x4 av = __builtin_bit_cast(f32x4, af[a]);
+                    const f32x4 bv = __builtin_bit_cast(f32x4, bf[b]);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(bv[e], av[e], acc[a][b], 0, 0, 0);
                 }
             }
-            const int64_t idx = m * p.ldc + n;
-            if (p.out_f32)
-                store4<float>(static_cast<float*>(p.C), idx, v, nvalid, (idx & 3) == 0);
-            else
-                store4<T>(static_cast<T*>(p.C), idx, v, nvalid, (idx & 3) == 0);
+    };
+
+    for (int kt = kt0; kt < kt1; ++kt) {
+        const int buf = (kt - kt0) % NS;
+        const int later = min(NS - 2, kt1 - 1 - kt);   // stages issued after this one
+        wait_stages<LMIN>(later);                      // this wave's share of stage kt has landed
+        __builtin_amdgcn_s_barrier();                  // every wave's share has; stage kt-1 fully consumed
+        if (kt + NS - 1 < kt1) {
+            issue(kt + NS - 1, (kt - kt0 + NS - 1) % NS);
+            if (CONV) advance();
+        }
+        const unsigned sbase = lds0 + buf * STAGE * 16;
+        u32x4 a0[FM], b0[FN], a1[FM], b1[FN];
+        read_frags(sbase, 0, a0, b0);
+        lds_wait();
+#pragma unroll
+        for (int a = 0; a < FM; ++a) pin(a0[a]);
+#pragma unroll
+        for (int b = 0; b < FN; ++b) pin(b0[b]);
+        read_frags(sbase, 1, a1, b1);                  // second k step loads under the first's MFMAs
+        mfmas(a0, b0);
+        lds_wait();
+#pragma unroll
+        for (int a = 0; a < FM; ++a) pin(a1[a]);
+#pragma unroll
+        for (int b = 0; b < FN; ++b) pin(b1[b]);
+        mfmas(a1, b1);
+    }
+
+    // --- epilogue: lane holds row m, columns n..n+3 ----------------------------------------
+    // Every operand was loaded before the first store (stores could alias the loads, so
+    // interleaving them would serialise one memory round trip per tile).
+    if (p.splits > 1) {                       // raw partial sums; the reduce kernel finishes
+#pragma unroll
+        for (int a = 0; a < FM; ++a)
+#pragma unroll
+            for (int b = 0; b < FN; ++b) {
+                if (mrow[a] >= p.M || nval[b] == 0) continue;
+                float* dst = p.partial + (static_cast<int64_t>(split) * p.M + mrow[a]) * p.N + ncol[b];
+                if (nval[b] == 4 && ((reinterpret_cast<uintptr_t>(dst) & 15) == 0))
+                    *reinterpret_cast<f32x4*>(dst) = acc[a][b];
+                else
+                    for (int e = 0; e < nval[b]; ++e) dst[e] = acc[a][b][e];
+            }
+        return;
+    }
+    if (p.epi == EPI_LSTM) {
+        // gates i, f, g, o of unit n / 4 (n is a multiple of 4 and the whole group is valid)
+        f32x4 g4[FM][FN];
+        float cprev[FM][FN];
+#pragma unroll
+        for (int a = 0; a < FM; ++a)
+#pragma unroll
+            for (int b = 0; b < FN; ++b) {
+                const bool ok = mrow[a] < p.M && nval[b] == 4;
+                const int64_t mm = ok ? mrow[a] : 0;
+                const int nn = ok ? ncol[b] : 0;
+                g4[a][b] = *reinterpret_cast<const f32x4*>(p.gx + mm * p.ldgx + nn);
+                cprev[a][b] = p.cstate[mm * (p.N >> 2) + (nn >> 2)];
+            }
+#pragma unroll
+        for (int a = 0; a < FM; ++a)
+#pragma unroll
+            for (int b = 0; b < FN; ++b) {
+                if (mrow[a] >= p.M || nval[b] != 4) continue;
+                const f32x4 v = acc[a][b] + g4[a][b];
+                const float c = sigmoidf_(v[1]) * cprev[a][b] + sigmoidf_(v[0]) * tanhf(v[2]);
+                const int u = ncol[b] >> 2;
+                p.cstate[mrow[a] * (p.N >> 2) + u] = c;
+                static_cast<T*>(p.C)[mrow[a] * p.ldc + u] = static_cast<T>(sigmoidf_(v[3]) * tanhf(c));
+            }
+        return;
+    }
+    float bias[FN][4];
+#pragma unroll
+    for (int b = 0; b < FN; ++b) {
+        for (int q = 0; q < 4; ++q) bias[b][q] = 0.0f;
+        if (nval[b] > 0) {
+            float t2[4];
+            if (p.bias) ld4(static_cast<const T*>(p.bias), ncol[b], nval[b], bias[b]);
+            if (p.bias2) {
+                ld4(static_cast<const T*>(p.bias2), ncol[b], nval[b], t2);
+                for (int q = 0; q < 4; ++q) bias[b][q] += t2[q];
+            }
         }
     }
+#pragma unroll
+    for (int a = 0; a < FM; ++a)
+#pragma unroll
+        for (int b = 0; b < FN; ++b) {
+            if (mrow[a] >= p.M || nval[b] == 0) continue;
+            float rsd[4] = {0.f, 0.f, 0.f, 0.f};
+            if (have_res) {
+                const int64_t idx = mrow[a] * p.ldc + ncol[b];
+                if (nval[b] == 4 && (idx & 3) == 0) {
+                    if constexpr (sizeof(T) == 2) {
+                        const uint2 r = rraw[a][b];
+                        rsd[0] = __uint_as_float(r.x << 16);
+                        rsd[1] = __uint_as_float(r.x & 0xffff0000u);
+                        rsd[2] = __uint_as_float(r.y << 16);
+                        rsd[3] = __uint_as_float(r.y & 0xffff0000u);
+                    } else {
+                        const uint4 r = rraw[a][b];
+                        rsd[0] = __uint_as_float(r.x), rsd[1] = __uint_as_float(r.y);
+                        rsd[2] = __uint_as_float(r.z), rsd[3] = __uint_as_float(r.w);
+                    }
+                } else {
+                    ld4(static_cast<const T*>(p.res), idx, nval[b], rsd);
+                }
+            }
+            float v[4];
+            for (int q = 0; q < 4; ++q) v[q] = act_f((acc[a][b][q] + bias[b][q]) + rsd[q], p.act);
+            const int64_t idx = mrow[a] * p.ldc + ncol[b];
+            if (p.out_f32)
+                store4<float>(static_cast<float*>(p.C), idx, v, nval[b]);
+            else
+                store4<T>(static_cast<T*>(p.C), idx, v, nval[b]);
+        }
+}
+
+// Split-K finish: sum the partials in split order, then the usual epilogue.
+template <typename T>
+__global__ void splitk_reduce_kernel(const GemmParams p) {
+    const int groups = (p.N + 3) / 4;
+    const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (t >= p.M * groups) return;
+    const int64_t m = t / groups;
+    const int n = static_cast<int>(t - m * groups) * 4;
+    const int nvalid = min(4, p.N - n);
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    const int64_t plane = p.M * static_cast<int64_t>(p.N);
+    const float* src = p.partial + m * p.N + n;
+    if (nvalid == 4 && (p.N & 3) == 0) {
+        f32x4 part[16];                       // splits <= 16: all loads in flight together
+#pragma unroll
+        for (int s = 0; s < 16; ++s)
+            if (s < p.splits) part[s] = *reinterpret_cast<const f32x4*>(src + s * plane);
+#pragma unroll
+        for (int s = 0; s < 16; ++s)
+            if (s < p.splits)
+                for (int e = 0; e < 4; ++e) v[e] += part[s][e];
+    } else {
+        for (int s = 0; s < p.splits; ++s)
+            for (int e = 0; e < nvalid; ++e) v[e] += src[s * plane + e];
+    }
+    epilogue4<T>(p, m, n, nvalid, v);
 }
 
 // ---------------------------------------------------------------------------
 // Tile selection.  All shapes share the K loop, so the choice only affects
-// speed, never the bits of the result.
+// speed, never the bits of a result.
 // ---------------------------------------------------------------------------
 
-template <typename T, int BM, int BN, int WM, int WN>
-static hipError_t launch_cfg(const GemmParams& p, int width, hipStream_t s) {
-    dim3 grid(static_cast<unsigned>((p.M + BM - 1) / BM), static_cast<unsigned>((width + BN - 1) / BN),
-              static_cast<unsigned>(p.ksub));
-    hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN>), grid, dim3(256), 0, s, p);
+constexpr int kCUs = 256;
+
+int gemm_splits(int64_t M, int N, int K, int dtype, int epi) {
+    if (epi != EPI_STD) return 1;
+    const int bk = dtype == MOPAR_BF16 ? 64 : 32;
+    const int64_t nk = (K + bk - 1) / bk;
+    const int64_t tiles = ((M + 63) / 64) * ((N + 63) / 64);   // reference tiling, independent of k
+    int s = 1;
+    while (s < 16 && tiles * s < kCUs && nk / (2 * s) >= 4) s *= 2;
+    return s;
+}
+
+template <typename T, int BM, int BN, int WM, int WN, int NS>
+static hipError_t launch_cfg(const GemmParams& p, int width, hipStream_t st) {
+    const int64_t total = ((p.M + BM - 1) / BM) * ((width + BN - 1) / BN) * p.ksub * p.splits;
+    const int64_t grid = (total + 7) / 8 * 8;
+    if (p.conv)
+        hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, NS, true>), dim3(static_cast<unsigned>(grid)), dim3(256), 0,
+                           st, p);
+    else
+        hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, NS, false>), dim3(static_cast<unsigned>(grid)), dim3(256),
+                           0, st, p);
     return hipGetLastError();
 }
 
 template <typename T>
-static hipError_t dispatch(const GemmParams& p, hipStream_t s) {
+static hipError_t dispatch(const GemmParams& p, hipStream_t st) {
     const int width = (p.N + p.ksub - 1) / p.ksub;   // widest sub-slice
-    if (p.epi == EPI_LSTM || p.M <= 64) {
-        if (p.M <= 16) return launch_cfg<T, 16, 64, 1, 4>(p, width, s);
-        if (width >= 64 && p.epi != EPI_LSTM) return launch_cfg<T, 64, 64, 2, 2>(p, width, s);
-        return launch_cfg<T, 64, 16, 4, 1>(p, width, s);
+    if (p.M <= 16) return launch_cfg<T, 16, 64, 1, 4, 4>(p, width, st);
+    if (p.M <= 64 || p.epi == EPI_LSTM) {
+        if (width >= 64 && p.epi != EPI_LSTM) return launch_cfg<T, 64, 64, 2, 2, 4>(p, width, st);
+        return launch_cfg<T, 64, 16, 4, 1, 4>(p, width, st);
     }
     const int64_t mt = (p.M + 127) / 128;
-    auto blocks = [&](int bn) { return mt * ((width + bn - 1) / bn) * p.ksub; };
-    if (width >= 128 && blocks(128) >= 512) return launch_cfg<T, 128, 128, 2, 2>(p, width, s);
-    if (width >= 64 && blocks(64) >= 256) return launch_cfg<T, 128, 64, 2, 2>(p, width, s);
-    if (width >= 32) return launch_cfg<T, 128, 32, 4, 1>(p, width, s);
-    return launch_cfg<T, 128, 16, 4, 1>(p, width, s);
+    auto blocks = [&](int64_t bm_tiles, int bn) { return bm_tiles * ((width + bn - 1) / bn) * p.ksub * p.splits; };
+    if (width >= 128 && blocks(mt, 128) >= kCUs) return launch_cfg<T, 128, 128, 2, 2, 2>(p, width, st);
+    if (width >= 64 && blocks(mt, 64) >= kCUs) return launch_cfg<T, 128, 64, 2, 2, 3>(p, width, st);
+    if (width >= 64) return launch_cfg<T, 64, 64, 2, 2, 4>(p, width, st);
+    if (width >= 32) {
+        if (blocks(mt, 32) >= kCUs) return launch_cfg<T, 128, 32, 4, 1, 3>(p, width, st);
+        return launch_cfg<T, 64, 32, 2, 2, 4>(p, width, st);
+    }
+    if (blocks(mt, 16) >= kCUs) return launch_cfg<T, 128, 16, 4, 1, 4>(p, width, st);
+    return launch_cfg<T, 64, 16, 4, 1, 4>(p, width, st);
 }
 
-hipError_t launch_gemm(const GemmParams& p, int dtype, hipStream_t stream) {
+hipError_t launch_gemm(const GemmParams& params, int dtype, hipStream_t stream) {
+    GemmParams p = params;
+    if (p.splits < 1) p.splits = 1;
+    if (p.ksub < 1) p.ksub = 1;
     if (p.M <= 0 || p.N <= 0) return hipSuccess;
-    if (dtype == MOPAR_BF16) return dispatch<__bf16>(p, stream);
-    return dispatch<float>(p, stream);
+    if (p.splits < 1 || (p.splits > 1 && (!p.partial || p.epi != EPI_STD))) return hipErrorInvalidValue;
+    hipError_t e = dtype == MOPAR_BF16 ? dispatch<__bf16>(p, stream) : dispatch<float>(p, stream);
+    if (e != hipSuccess || p.splits == 1) return e;
+    const int64_t n = p.M * ((p.N + 3) / 4);
+    const unsigned blocks = static_cast<unsigned>((n + 255) / 256);
+    if (dtype == MOPAR_BF16)
+        hipLaunchKernelGGL(splitk_reduce_kernel<__bf16>, dim3(blocks), dim3(256), 0, stream, p);
+    else
+        hipLaunchKernelGGL(splitk_reduce_kernel<float>, dim3(blocks), dim3(256), 0, stream, p);
+    return hipGetLastError();
 }
 
 }  // namespace mopar

@@ -47,7 +47,17 @@ struct GemmParams {
     int64_t ldgx;
     float* cstate;          // [M][N/4] float32 cell state, read then overwritten
     // the new hidden state of unit u goes to C[m * ldc + u]
+    int splits;             // split-K factor (>= 1); > 1 needs `partial`
+    float* partial;         // [splits][M][N] float32 partial sums (split-K only)
 };
+
+// Split-K factor used for an (M, N, K) product.  A function of the shape
+// only -- never of the sub-slice count -- so sub-sliced launches reduce in
+// the same order as the unsplit one.
+int gemm_splits(int64_t M, int N, int K, int dtype, int epi);
+inline size_t gemm_partial_bytes(int64_t M, int N, int splits) {
+    return splits > 1 ? static_cast<size_t>(splits) * static_cast<size_t>(M) * static_cast<size_t>(N) * 4 : 0;
+}
 
 enum { EPI_STD = 0, EPI_LSTM = 1 };
 

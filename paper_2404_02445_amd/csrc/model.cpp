@@ -34,6 +34,8 @@ struct TempReq {
 }  // namespace
 
 struct OpInfo {
+    int splits = 1;                // conv / linear: split-K factor of the GEMM
+    int partial_temp = -1;         // index into temps of the split-K partial sums
     int cs = 0;                    // conv: input channel storage stride (padded for the model input)
     bool input_is_model = false;   // conv: reads the NCHW float32 model input
     int64_t K = 0, M = 0;          // GEMM sizes (conv / linear)
@@ -268,6 +270,11 @@ static int validate_and_build(mopar_model_s& m) {
                 if (!wcheck(op.w, op.n_out * inf.K, "w") || !wcheck(op.b, op.n_out, "b"))
                     return set_error(MOPAR_E_ARG, nm + ": weight offsets out of range or not 16-byte aligned");
                 if (xin) inf.temps.push_back(static_cast<size_t>(x.dims[0] * x.dims[2] * x.dims[3] * inf.cs) * es);
+                inf.splits = gemm_splits(inf.M, op.n_out, static_cast<int>(inf.K), m.dtype, EPI_STD);
+                if (inf.splits > 1) {
+                    inf.partial_temp = static_cast<int>(inf.temps.size());
+                    inf.temps.push_back(gemm_partial_bytes(inf.M, op.n_out, inf.splits));
+                }
                 break;
             }
             case MOPAR_OP_LINEAR: {
@@ -284,6 +291,11 @@ static int validate_and_build(mopar_model_s& m) {
                 inf.M = M;
                 if (!wcheck(op.w, op.n_out * K, "w") || !wcheck(op.b, op.n_out, "b"))
                     return set_error(MOPAR_E_ARG, nm + ": weight offsets out of range or not 16-byte aligned");
+                inf.splits = gemm_splits(M, op.n_out, static_cast<int>(K), m.dtype, EPI_STD);
+                if (inf.splits > 1) {
+                    inf.partial_temp = static_cast<int>(inf.temps.size());
+                    inf.temps.push_back(gemm_partial_bytes(M, op.n_out, inf.splits));
+                }
                 break;
             }
             case MOPAR_OP_MAXPOOL: {
@@ -518,6 +530,8 @@ static hipError_t run_op(const mopar_model_s& m, int i, const Ptrs& P, int ksub,
             g.K = static_cast<int>(inf.K);
             g.act = op.act;
             g.ksub = ksub;
+            g.splits = inf.splits;
+            g.partial = inf.partial_temp >= 0 ? reinterpret_cast<float*>(P.ws + inf.temp_off[inf.partial_temp]) : nullptr;
             return launch_gemm(g, dt, s);
         }
         case MOPAR_OP_LINEAR: {
@@ -534,6 +548,8 @@ static hipError_t run_op(const mopar_model_s& m, int i, const Ptrs& P, int ksub,
             g.K = static_cast<int>(inf.K);
             g.act = op.act;
             g.ksub = ksub;
+            g.splits = inf.splits;
+            g.partial = inf.partial_temp >= 0 ? reinterpret_cast<float*>(P.ws + inf.temp_off[inf.partial_temp]) : nullptr;
             return launch_gemm(g, dt, s);
         }
         case MOPAR_OP_MAXPOOL:
