@@ -40,6 +40,18 @@ def op_flops(m, op):
     return 0
 
 
+def codec_ratios(m, cuts):
+    """Compression ratio per cut: R = 8 where the code width stays a multiple of the 16-byte
+    granule (8 bf16 / 4 fp32 channels), else 4."""
+    import synth
+    g = 8 if m.dtype == "bf16" else 4
+    out = []
+    for li in cuts:
+        c = synth.boundary_channels(m, li)
+        out.append(8 if (c % 8 == 0 and (c // 8) % g == 0) else 4)
+    return out
+
+
 def numel(shape):
     n = 1
     for s in shape:
@@ -58,6 +70,11 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-op-timing", action="store_true")
     ap.add_argument("--op-report", action="store_true", help="print per-op times (ms) to stderr")
+    ap.add_argument("--pipeline", type=int, default=2, metavar="D",
+                    help="run batches through the slice pipeline with D code slots per cut (0: sequential)")
+    ap.add_argument("--replicas", type=int, default=3,
+                    help="pipeline instances of the sliced model (3 instances + torch's stream = 4 hardware queues)")
+    ap.add_argument("--stream-per-slice", type=int, default=0, help="1: one stream per slice, 0: one per instance")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run a raw boundary copy of this many MiB per step (counter calibration)")
     args = ap.parse_args()
@@ -84,7 +101,8 @@ def main():
                    k_override=s["k_override"])
     plan = sm.plan()
     cuts = plan.slice_end[:-1]
-    cw = synth.make_codec_weights(m, cuts, ratio=m.codec_ratio) if args.codec == "ae" else None
+    ratios = codec_ratios(m, cuts)
+    cw = synth.make_codec_weights(m, cuts, ratio=ratios) if args.codec == "ae" else None
     codecs, keep = sm.codecs(plan, args.codec, cw)
     codes = sm.alloc_codes(plan, codecs)
     ws = sm.alloc_workspace(plan)
@@ -102,24 +120,55 @@ def main():
         sm.forward(pl, x, out, codecs, codes, ws)             # a5-a10: sliced forward with codec hand-off
         return pl
 
+    def sequential_run(steps):
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        evs[0].record(stream)
+        for i in range(steps):
+            step()
+            evs[i + 1].record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        per = [evs[i].elapsed_time(evs[i + 1]) for i in range(steps)]
+        return evs[0].elapsed_time(evs[-1]), wall, per
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
+    pipe = None
+    if args.pipeline:
+        pipe = sm.pipeline(plan, args.codec, cw, depth=args.pipeline, replicas=args.replicas,
+                           stream_per_slice=bool(args.stream_per_slice))
+
+        def pstep():
+            prof = sm.profile()
+            pl = P.mopar_plan_slices(prof, **plan_kw)
+            pipe.submit(x, out)
+            return pl
+
+        for _ in range(args.warmup):
+            pstep()
+        torch.cuda.synchronize()
+
     # --- timed region: exactly K steps ------------------------------------------------
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    evs[0].record(stream)
-    for i in range(args.steps):
-        step()
-        evs[i + 1].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
-    total_ms = evs[0].elapsed_time(evs[-1])
+    if pipe is None:
+        total_ms, wall, per_step = sequential_run(args.steps)
+    else:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            pstep()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        total_ms = wall * 1e3
+        seq_ms, _, per_step = sequential_run(args.steps)   # per-batch latency, one at a time
+        seq_value = m.batch * args.steps / (seq_ms / 1e3)
     ms_per_step = total_ms / args.steps
     value = m.batch * args.steps / (total_ms / 1e3)
+    if pipe is None:
+        seq_value = value
 
     # planning cost on the host (already inside the steps above, overlapped with the GPU)
     tp0 = time.perf_counter()
@@ -142,11 +191,15 @@ def main():
         "data": "synthetic (seeded N(0,1) inputs, random-init weights of the named architecture)",
         "config": {"workload": f"{m.name}: {m.dtype}, batch {m.batch}, {plan.n_slices} slices at "
                                f"{cuts}, RD k={max(plan.k)}, {args.codec} codec"
-                               + (f" R={m.codec_ratio}" if args.codec == "ae" else ""),
+                               + (f" R={ratios}" if args.codec == "ae" else ""),
                    "batch": m.batch, "slices": plan.n_slices, "k": plan.k, "codec": args.codec},
         "latency_ms": {"p50": round(statistics.median(per_step), 4),
                        "p95": round(float(np.percentile(per_step, 95)), 4)},
+        "mode": (f"slice pipeline: {args.replicas} instance(s) x {plan.n_slices} slices on "
+                 f"{len(set(id(s) for s in pipe.streams))} streams, {args.pipeline} code slots per (instance, cut); "
+                 f"latency_ms is one batch at a time") if pipe else "sequential: one batch at a time",
         "wall_s_timed_region": round(wall, 4),
+        "sequential_value": round(seq_value, 2),
         "host_plan_us": round(plan_us, 1),
     }
 
@@ -198,11 +251,12 @@ def main():
         for c, li in enumerate(cuts):
             shp = m.tensors[m.layer_output_tid(li)]["shape"]
             tb = numel(shp) * es
-            cbytes = tb // (m.codec_ratio if args.codec == "ae" else 1)
+            r = ratios[c] if args.codec == "ae" else 1
+            cbytes = tb // r
             wb = 0
             if args.codec == "ae":
                 ch = synth.boundary_channels(m, li)
-                wb = (2 * ch * (ch // m.codec_ratio) + ch + ch // m.codec_ratio) * es
+                wb = (2 * ch * (ch // r) + ch + ch // r) * es
             e_avg, d_avg = enc_ms[c] / n_t, dec_ms[c] / n_t
             codec.append({"cut_after": m.layers[li], "tensor_MB": round(tb / 1e6, 3),
                           "encode_us": round(e_avg * 1e3, 2), "decode_us": round(d_avg * 1e3, 2),

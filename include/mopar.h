@@ -261,6 +261,47 @@ int mopar_model_forward(mopar_model_t model, const mopar_plan* plan, const mopar
                         size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* Slice pipeline across requests                                           */
+/* ------------------------------------------------------------------------ */
+
+/* The paper deploys every slice as its own function and scales functions by
+ * running more instances, so consecutive requests occupy different slices
+ * and different instances at the same time (Sec. II-A, III-A, III-C).  On one
+ * GPU the pipeline keeps `replicas` instances of the sliced model; instance r
+ * runs slice s on streams[r * n_slices + s] (a caller may pass one stream for
+ * several slices of an instance) with its own workspace.  Batch i goes to
+ * instance i mod replicas and flows through its slices; slice s starts after
+ * slice s-1 of the same batch has encoded its boundary, which it decodes from
+ * a ring of `depth` code buffers per (instance, cut).  Every batch runs
+ * exactly the kernels of mopar_model_forward, so its output is bitwise
+ * identical to the sequential forward.
+ *
+ * streams:   replicas * n_slices caller-owned hipStream_t (default priority).
+ * ws:        mopar_pipeline_workspace_bytes(replicas) bytes, used by no one
+ *            else while the pipeline lives.
+ * code_bufs: replicas * depth * (n_slices - 1) device buffers; the buffer of
+ *            (instance r, ring slot q, cut c) is at
+ *            [(r * depth + q) * (n_slices - 1) + c], each of
+ *            mopar_boundary_code_bytes of that boundary.
+ * codecs:    n_slices - 1 codecs (copied).  The plan is copied.
+ * Per-op timing is not recorded by pipelined batches.
+ * Errors: as mopar_model_forward; MOPAR_E_HIP if an event cannot be made. */
+typedef struct mopar_pipeline_s* mopar_pipeline_t;
+
+int mopar_pipeline_workspace_bytes(mopar_model_t model, const mopar_plan* plan, int32_t replicas, size_t* bytes);
+int mopar_pipeline_create(mopar_model_t model, const mopar_plan* plan, const mopar_codec* codecs, int32_t replicas,
+                          int32_t depth, void* const* streams, void* ws, size_t ws_bytes, void* const* code_bufs,
+                          mopar_pipeline_t* out);
+
+/* Enqueue one batch: read `in_dev` (the model input), write `out_dev`.  Both
+ * must stay untouched by the caller until the last slice's stream has
+ * finished this batch (e.g. synchronise that stream).  Never blocks. */
+int mopar_pipeline_submit(mopar_pipeline_t pipe, const void* in_dev, void* out_dev);
+
+/* Destroy the pipeline's events; the caller must have synchronised its streams. */
+void mopar_pipeline_destroy(mopar_pipeline_t pipe);
+
+/* ------------------------------------------------------------------------ */
 /* Measurement                                                               */
 /* ------------------------------------------------------------------------ */
 

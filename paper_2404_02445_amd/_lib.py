@@ -81,6 +81,12 @@ SIGNATURES = {
     "mopar_boundary_decode": (c_i32, [ctypes.POINTER(Codec), ctypes.POINTER(TensorDesc), c_vp, c_vp, c_vp]),
     "mopar_model_forward": (c_i32, [c_vp, ctypes.POINTER(Plan), ctypes.POINTER(Codec), c_vp, c_vp,
                                     ctypes.POINTER(c_vp), c_vp, ctypes.c_size_t, c_vp]),
+    "mopar_pipeline_workspace_bytes": (c_i32, [c_vp, ctypes.POINTER(Plan), c_i32, ctypes.POINTER(ctypes.c_size_t)]),
+    "mopar_pipeline_create": (c_i32, [c_vp, ctypes.POINTER(Plan), ctypes.POINTER(Codec), c_i32, c_i32,
+                                      ctypes.POINTER(c_vp), c_vp, ctypes.c_size_t, ctypes.POINTER(c_vp),
+                                      ctypes.POINTER(c_vp)]),
+    "mopar_pipeline_submit": (c_i32, [c_vp, c_vp, c_vp]),
+    "mopar_pipeline_destroy": (None, [c_vp]),
     "mopar_model_set_timing": (c_i32, [c_vp, c_i32]),
     "mopar_model_timing_slots": (c_i32, [c_vp, ctypes.POINTER(c_i32)]),
     "mopar_model_op_times": (c_i32, [c_vp, ctypes.POINTER(c_f32), c_i32]),

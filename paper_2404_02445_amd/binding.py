@@ -347,6 +347,12 @@ class SlicedModel:
                                         _ptr(ws), 0 if ws is None else ws.numel(), _stream_ptr(stream)))
         return out
 
+    # -- cross-request slice pipeline ---------------------------------------------
+    def pipeline(self, plan, codec="ae", codec_weights=None, depth=2, replicas=1, stream_per_slice=True):
+        """A ``SlicePipeline``: ``replicas`` instances of the sliced model; each instance runs
+        its slices on one stream per slice, or on a single stream when ``stream_per_slice`` is False."""
+        return SlicePipeline(self, plan, codec, codec_weights, depth, replicas, stream_per_slice)
+
     # -- measurement -----------------------------------------------------------
     def set_timing(self, enable=True):
         check(lib().mopar_model_set_timing(self.handle, 1 if enable else 0))
@@ -366,3 +372,49 @@ class SlicedModel:
         check(lib().mopar_slice_forward(self.handle, ctypes.byref(plan.raw), s, _ptr(x), _ptr(out), _ptr(ws),
                                         ws.numel(), _stream_ptr(stream)))
         return out
+
+
+class SlicePipeline:
+    """Owns the streams, workspace, code-buffer ring and library handle of a slice pipeline."""
+
+    def __init__(self, sm, plan, codec, codec_weights, depth, replicas=1, stream_per_slice=True):
+        self.sm, self.plan = sm, plan
+        S = plan.n_slices
+        self.streams = []
+        for _ in range(replicas):
+            if stream_per_slice:
+                self.streams += [torch.cuda.Stream(device=sm.device) for _ in range(S)]
+            else:
+                st = torch.cuda.Stream(device=sm.device)
+                self.streams += [st] * S
+        self.codecs, self._keep = sm.codecs(plan, codec, codec_weights)
+        n = ctypes.c_size_t()
+        check(lib().mopar_pipeline_workspace_bytes(sm.handle, ctypes.byref(plan.raw), replicas, ctypes.byref(n)))
+        self.ws = torch.empty(max(n.value, 16), dtype=torch.uint8, device=sm.device)
+        self.codes = []
+        for _ in range(replicas * depth):
+            self.codes += sm.alloc_codes(plan, self.codecs)
+        sp = (ctypes.c_void_p * len(self.streams))(*[s.cuda_stream for s in self.streams])
+        cb = (ctypes.c_void_p * max(len(self.codes), 1))(*[b.data_ptr() for b in self.codes])
+        h = ctypes.c_void_p()
+        # the library keeps no pointer to these host arrays after create
+        check(lib().mopar_pipeline_create(sm.handle, ctypes.byref(plan.raw), self.codecs, replicas, depth, sp,
+                                          _ptr(self.ws), self.ws.numel(), cb, ctypes.byref(h)))
+        self.handle = h
+
+    def submit(self, x, out):
+        check(lib().mopar_pipeline_submit(self.handle, _ptr(x), _ptr(out)))
+        return out
+
+    def synchronize(self):
+        for s in self.streams:
+            s.synchronize()
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h is not None and h.value and L._lib is not None:
+            try:
+                self.synchronize()
+            finally:
+                L._lib.mopar_pipeline_destroy(h)
+                self.handle = None

@@ -20,6 +20,11 @@ int decode_impl(const mopar_codec*, const mopar_tensor_desc*, const void*, void*
 int model_forward_impl(const mopar_model_s*, const mopar_plan*, const mopar_codec*, const void*, void*, void* const*,
                        void*, size_t, void*);
 
+int pipeline_ws_bytes_impl(const mopar_model_s*, const mopar_plan*, int32_t, size_t*);
+int pipeline_create_impl(const mopar_model_s*, const mopar_plan*, const mopar_codec*, int32_t, int32_t, void* const*,
+                         void*, size_t, void* const*, mopar_pipeline_t*);
+int pipeline_submit_impl(mopar_pipeline_s*, const void*, void*);
+void pipeline_destroy_impl(mopar_pipeline_s*);
 int set_timing_impl(mopar_model_s*, int32_t);
 int timing_slots_impl(const mopar_model_s*, int32_t*);
 int op_times_impl(const mopar_model_s*, float*, int32_t);
@@ -103,6 +108,25 @@ int mopar_model_forward(mopar_model_t model, const mopar_plan* plan, const mopar
         return model_forward_impl(model, plan, codecs, in_dev, out_dev, code_bufs, ws, ws_bytes, stream);
     });
 }
+
+int mopar_pipeline_workspace_bytes(mopar_model_t model, const mopar_plan* plan, int32_t replicas, size_t* bytes) {
+    return guarded("mopar_pipeline_workspace_bytes",
+                   [&] { return pipeline_ws_bytes_impl(model, plan, replicas, bytes); });
+}
+
+int mopar_pipeline_create(mopar_model_t model, const mopar_plan* plan, const mopar_codec* codecs, int32_t replicas,
+                          int32_t depth, void* const* streams, void* ws, size_t ws_bytes, void* const* code_bufs,
+                          mopar_pipeline_t* out) {
+    return guarded("mopar_pipeline_create", [&] {
+        return pipeline_create_impl(model, plan, codecs, replicas, depth, streams, ws, ws_bytes, code_bufs, out);
+    });
+}
+
+int mopar_pipeline_submit(mopar_pipeline_t pipe, const void* in_dev, void* out_dev) {
+    return guarded("mopar_pipeline_submit", [&] { return pipeline_submit_impl(pipe, in_dev, out_dev); });
+}
+
+void mopar_pipeline_destroy(mopar_pipeline_t pipe) { pipeline_destroy_impl(pipe); }
 
 int mopar_model_set_timing(mopar_model_t model, int32_t enable) {
     return guarded("mopar_model_set_timing", [&] { return set_timing_impl(model, enable); });

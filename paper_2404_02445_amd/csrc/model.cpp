@@ -852,3 +852,159 @@ int model_forward_impl(const mopar_model_s* m, const mopar_plan* p, const mopar_
 }
 
 }  // namespace mopar
+
+// ---------------------------------------------------------------------------
+// Slice pipeline across requests
+// ---------------------------------------------------------------------------
+
+struct mopar_pipeline_s {
+    const mopar_model_s* m = nullptr;
+    std::vector<int32_t> slice_end, k;
+    mopar_plan plan{};
+    std::vector<mopar_codec> codecs;
+    int S = 0, depth = 0, replicas = 0;
+    std::vector<hipStream_t> streams;              // [replicas][S]
+    std::vector<unsigned char*> ws;                // [replicas][S], one model workspace each
+    std::vector<void*> codes;                      // [replicas][depth][S-1]
+    std::vector<hipEvent_t> enc_done, dec_done;    // [replicas][depth][S-1]
+    int64_t submitted = 0;
+    ~mopar_pipeline_s() {
+        for (auto e : enc_done) (void)hipEventDestroy(e);
+        for (auto e : dec_done) (void)hipEventDestroy(e);
+    }
+};
+
+namespace mopar {
+
+static size_t slice_ws_stride(const mopar_model_s* m) { return (m->ws_bytes + 255) / 256 * 256; }
+
+int pipeline_ws_bytes_impl(const mopar_model_s* m, const mopar_plan* p, int32_t replicas, size_t* bytes) {
+    if (!bytes) return set_error(MOPAR_E_ARG, "mopar_pipeline_workspace_bytes: null output");
+    if (replicas < 1 || replicas > 64) return set_error(MOPAR_E_ARG, "mopar_pipeline_workspace_bytes: replicas 1..64");
+    const int rc = check_plan(m, p, "mopar_pipeline_workspace_bytes");
+    if (rc) return rc;
+    *bytes = slice_ws_stride(m) * static_cast<size_t>(p->n_slices) * static_cast<size_t>(replicas);
+    return MOPAR_OK;
+}
+
+int pipeline_create_impl(const mopar_model_s* m, const mopar_plan* p, const mopar_codec* codecs, int32_t replicas,
+                         int32_t depth, void* const* streams, void* ws, size_t ws_bytes, void* const* code_bufs,
+                         mopar_pipeline_t* out) {
+    if (!out) return set_error(MOPAR_E_ARG, "mopar_pipeline_create: null output");
+    *out = nullptr;
+    int rc = check_plan(m, p, "mopar_pipeline_create");
+    if (rc) return rc;
+    const int S = p->n_slices;
+    if (depth < 1 || depth > 64) return set_error(MOPAR_E_ARG, "mopar_pipeline_create: depth must be 1..64");
+    if (replicas < 1 || replicas > 64) return set_error(MOPAR_E_ARG, "mopar_pipeline_create: replicas must be 1..64");
+    if (!streams) return set_error(MOPAR_E_ARG, "mopar_pipeline_create: null streams");
+    const size_t need = slice_ws_stride(m) * static_cast<size_t>(S) * static_cast<size_t>(replicas);
+    if (need && (!ws || ws_bytes < need))
+        return set_error(MOPAR_E_WORKSPACE, "mopar_pipeline_create: workspace smaller than mopar_pipeline_workspace_bytes");
+    if (S > 1 && (!codecs || !code_bufs)) return set_error(MOPAR_E_ARG, "mopar_pipeline_create: codecs / code buffers");
+    for (int c = 0; c + 1 < S; ++c) {
+        const auto& t = m->tensors[m->layer_out[p->slice_end[c]]];
+        int64_t pos;
+        int ch;
+        rc = codec_geometry(&codecs[c], &t, &pos, &ch, "mopar_pipeline_create");
+        if (rc) return rc;
+        for (int q = 0; q < replicas * depth; ++q)
+            if (!code_bufs[q * (S - 1) + c]) return set_error(MOPAR_E_ARG, "mopar_pipeline_create: null code buffer");
+    }
+    auto* pp = new mopar_pipeline_s();
+    pp->m = m;
+    pp->slice_end.assign(p->slice_end, p->slice_end + S);
+    pp->k.assign(p->k, p->k + m->n_layers);
+    pp->plan = *p;
+    pp->plan.slice_end = pp->slice_end.data();
+    pp->plan.k = pp->k.data();
+    if (S > 1) pp->codecs.assign(codecs, codecs + S - 1);
+    pp->S = S;
+    pp->depth = depth;
+    pp->replicas = replicas;
+    for (int i = 0; i < replicas * S; ++i) {
+        pp->streams.push_back(static_cast<hipStream_t>(streams[i]));
+        pp->ws.push_back(static_cast<unsigned char*>(ws) + slice_ws_stride(m) * static_cast<size_t>(i));
+    }
+    const int ncut = S - 1;
+    for (int i = 0; i < replicas * depth * ncut; ++i) {
+        pp->codes.push_back(code_bufs[i]);
+        hipEvent_t a, b;
+        rc = hip_check(hipEventCreateWithFlags(&a, hipEventDisableTiming), "hipEventCreateWithFlags");
+        if (rc) {
+            delete pp;
+            return rc;
+        }
+        rc = hip_check(hipEventCreateWithFlags(&b, hipEventDisableTiming), "hipEventCreateWithFlags");
+        if (rc) {
+            (void)hipEventDestroy(a);
+            delete pp;
+            return rc;
+        }
+        pp->enc_done.push_back(a);
+        pp->dec_done.push_back(b);
+    }
+    *out = pp;
+    return MOPAR_OK;
+}
+
+int pipeline_submit_impl(mopar_pipeline_s* pp, const void* in, void* out) {
+    if (!pp) return set_error(MOPAR_E_ARG, "mopar_pipeline_submit: null pipeline");
+    if (!in || !out) return set_error(MOPAR_E_ARG, "mopar_pipeline_submit: null input or output");
+    const mopar_model_s& m = *pp->m;
+    const int S = pp->S, ncut = S - 1;
+    const int rep = static_cast<int>(pp->submitted % pp->replicas);               // instance
+    const int r = static_cast<int>((pp->submitted / pp->replicas) % pp->depth) + rep * pp->depth;  // ring slot
+    int l0 = 0;
+    for (int s = 0; s < S; ++s) {
+        const int l1 = pp->slice_end[s];
+        const hipStream_t st = pp->streams[rep * S + s];
+        // slice s reads its input from the caller (s = 0) or from its own workspace (decoded)
+        Ptrs P{&m, pp->ws[rep * S + s], in, s == 0 ? m.input : -1, out, s == S - 1 ? m.output : -1};
+        int rc;
+        if (s > 0) {
+            const int c = s - 1, slot = r * ncut + c;
+            const int bt = m.layer_out[l0 - 1];
+            const auto& t = m.tensors[bt];
+            int64_t pos;
+            int ch;
+            codec_geometry(&pp->codecs[c], &t, &pos, &ch, "mopar_pipeline_submit");
+            rc = hip_check(hipStreamWaitEvent(st, pp->enc_done[slot], 0), "hipStreamWaitEvent");
+            if (rc) return rc;
+            rc = hip_check(codec_apply(pp->codecs[c], t.dtype, pos, ch, pp->codes[slot], P.get(bt), false, st),
+                           "boundary decode");
+            if (rc) return rc;
+            rc = hip_check(hipEventRecord(pp->dec_done[slot], st), "hipEventRecord");
+            if (rc) return rc;
+        }
+        for (int l = l0; l <= l1; ++l)
+            for (int i = m.layer_first[l]; i <= m.layer_last[l]; ++i) {
+                const int ksub = m.ops[i].rd ? pp->k[l] : 1;
+                rc = hip_check(run_op(m, i, P, ksub, st), "kernel launch");
+                if (rc) return rc;
+            }
+        if (s < S - 1) {
+            const int c = s, slot = r * ncut + c;
+            const int bt = m.layer_out[l1];
+            const auto& t = m.tensors[bt];
+            int64_t pos;
+            int ch;
+            codec_geometry(&pp->codecs[c], &t, &pos, &ch, "mopar_pipeline_submit");
+            // the slot is free once the previous batch using it has been decoded
+            rc = hip_check(hipStreamWaitEvent(st, pp->dec_done[slot], 0), "hipStreamWaitEvent");
+            if (rc) return rc;
+            rc = hip_check(codec_apply(pp->codecs[c], t.dtype, pos, ch, P.get(bt), pp->codes[slot], true, st),
+                           "boundary encode");
+            if (rc) return rc;
+            rc = hip_check(hipEventRecord(pp->enc_done[slot], st), "hipEventRecord");
+            if (rc) return rc;
+        }
+        l0 = l1 + 1;
+    }
+    ++pp->submitted;
+    return MOPAR_OK;
+}
+
+void pipeline_destroy_impl(mopar_pipeline_s* pp) { delete pp; }
+
+}  // namespace mopar

@@ -167,3 +167,25 @@ def test_codec_code_bytes_host_only():
     ae.c = 128
     with pytest.raises(P.MoparError):
         P.mopar_boundary_code_bytes(ae, (8, 256, 56, 56), "bf16")
+
+
+def test_pipeline_workspace_and_validation_host_only():
+    m = synth.build(2)
+    sm = P.SlicedModel(m, device="cpu")
+    pl = sm.plan()
+    n = ctypes.c_size_t()
+    assert P.lib().mopar_pipeline_workspace_bytes(sm.handle, ctypes.byref(pl.raw), 3, ctypes.byref(n)) == 0
+    per = (sm.workspace_bytes(pl) + 255) // 256 * 256
+    assert n.value == per * pl.n_slices * 3
+    h = ctypes.c_void_p()
+    streams = (ctypes.c_void_p * (3 * pl.n_slices))()
+    # depth 0, replicas 0 and a too-small workspace are rejected before any device call
+    st = P.lib().mopar_pipeline_create(sm.handle, ctypes.byref(pl.raw), None, 1, 0, streams, None, 0, None,
+                                       ctypes.byref(h))
+    assert st == L.MOPAR_E_ARG
+    st = P.lib().mopar_pipeline_create(sm.handle, ctypes.byref(pl.raw), None, 0, 2, streams, None, 0, None,
+                                       ctypes.byref(h))
+    assert st == L.MOPAR_E_ARG
+    st = P.lib().mopar_pipeline_create(sm.handle, ctypes.byref(pl.raw), None, 3, 2, streams, None, 0, None,
+                                       ctypes.byref(h))
+    assert st == L.MOPAR_E_WORKSPACE
