@@ -30,7 +30,8 @@
 // the store work on 4-wide vectors.
 //
 // Blocks are numbered so that the eight XCDs (which take blocks round-robin)
-// each receive a contiguous run of tiles sharing A rows, for L2 reuse.
+// each receive a contiguous run of tiles, grouped eight m-tiles at a time so
+// that the blocks an XCD runs together share A rows and B rows in its L2.
 #include <type_traits>
 
 #include "internal.h"
@@ -170,14 +171,20 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
     const int mt = static_cast<int>((p.M + BM - 1) / BM), nt = (width + BN - 1) / BN;
     const int total = mt * p.splits * p.ksub * nt;
     const int per_xcd = (total + 7) / 8;
-    int t = static_cast<int>(blockIdx.x % 8) * per_xcd + static_cast<int>(blockIdx.x / 8);
+    const int t = static_cast<int>(blockIdx.x % 8) * per_xcd + static_cast<int>(blockIdx.x / 8);
     if (t >= total) return;
-    const int nti = t % nt;
-    t /= nt;
-    const int j = t % p.ksub;
-    t /= p.ksub;
-    const int split = t % p.splits;
-    const int mti = t / p.splits;
+    // within an XCD's run, tiles go in groups of GM m-tiles x every column (split, sub-slice,
+    // n-tile), m fastest: the blocks resident together share both A rows and B rows in L2
+    constexpr int GM = 8;
+    const int cols = p.splits * p.ksub * nt;
+    const int group = t / (GM * cols), within = t - group * (GM * cols);
+    const int gm = min(GM, mt - group * GM);
+    const int mti = group * GM + within % gm;
+    int col = within / gm;
+    const int nti = col % nt;
+    col /= nt;
+    const int j = col % p.ksub;
+    const int split = col / p.ksub;
 
     const int q = p.N / p.ksub, rr = p.N % p.ksub;
     const int n_lo = j * q + min(j, rr), n_hi = (j + 1) * q + min(j + 1, rr);
@@ -211,13 +218,16 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
             rv[i] = m < p.M;
             const int64_t mc = rv[i] ? m : 0;
             if (CONV) {
-                const int64_t hw = static_cast<int64_t>(p.out_h) * p.out_w;
-                const int64_t img = mc / hw;
-                const int rem = static_cast<int>(mc - img * hw);
-                const int ho = rem / p.out_w, wo = rem - ho * p.out_w;
-                rowp[i] = Ap + img * p.img_h * p.img_w * static_cast<int64_t>(p.cs);
-                hb[i] = ho * p.stride - p.pad;
-                wb[i] = wo * p.stride - p.pad;
+                // M < 2^31, so the pixel decode runs in 32 bits with precomputed divisors;
+                // the row pointer already includes the window's top-left offset
+                const unsigned mu = static_cast<unsigned>(mc);
+                const unsigned img = p.div_hw.div(mu);
+                const unsigned rem = mu - img * static_cast<unsigned>(p.out_h * p.out_w);
+                const unsigned ho = p.div_w.div(rem), wo = rem - ho * static_cast<unsigned>(p.out_w);
+                hb[i] = static_cast<int>(ho) * p.stride - p.pad;
+                wb[i] = static_cast<int>(wo) * p.stride - p.pad;
+                rowp[i] = Ap + static_cast<int64_t>(img) * p.img_h * p.img_w * p.cs +
+                          static_cast<int64_t>(hb[i] * p.img_w + wb[i]) * p.cs;
             } else {
                 rowp[i] = Ap + mc * p.lda;
             }
@@ -264,6 +274,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
 
     // issue the loads of stage kt (coordinates must be those of stage kt) into LDS buffer buf
     auto issue = [&](int kt, int buf) {
+        int koff[2] = {0, 0};                   // conv: offset of the tap/channel within the window
+        if (CONV) {
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) koff[ks] = (tr[ks] * p.img_w + tcol[ks]) * p.cs + tci[ks];
+        }
 #pragma unroll
         for (int i = 0; i < LMAX; ++i) {
             const int blk = wave + 4 * i;
@@ -273,10 +288,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
             bool ok = rv[i] && k < p.K;
             const T* addr;
             if (CONV && blk < NBA) {
-                const int hi = hb[i] + tr[ks], wi = wb[i] + tcol[ks];
-                ok = ok && static_cast<unsigned>(hi) < static_cast<unsigned>(p.img_h) &&
-                     static_cast<unsigned>(wi) < static_cast<unsigned>(p.img_w);
-                addr = rowp[i] + static_cast<int64_t>((hi * p.img_w + wi) * p.cs + tci[ks]);
+                ok = ok && static_cast<unsigned>(hb[i] + tr[ks]) < static_cast<unsigned>(p.img_h) &&
+                     static_cast<unsigned>(wb[i] + tcol[ks]) < static_cast<unsigned>(p.img_w);
+                addr = rowp[i] + koff[ks];
             } else {
                 addr = rowp[i] + k;
             }
@@ -550,6 +564,10 @@ hipError_t launch_gemm(const GemmParams& params, int dtype, hipStream_t stream) 
     GemmParams p = params;
     if (p.splits < 1) p.splits = 1;
     if (p.ksub < 1) p.ksub = 1;
+    if (p.conv) {
+        p.div_hw = FastDiv(static_cast<unsigned>(p.out_h * p.out_w));
+        p.div_w = FastDiv(static_cast<unsigned>(p.out_w));
+    }
     if (p.M <= 0 || p.N <= 0) return hipSuccess;
     if (p.splits < 1 || (p.splits > 1 && (!p.partial || p.epi != EPI_STD))) return hipErrorInvalidValue;
     hipError_t e = dtype == MOPAR_BF16 ? dispatch<__bf16>(p, stream) : dispatch<float>(p, stream);

@@ -19,6 +19,23 @@ int hip_check(hipError_t e, const char* what);
 // Kernel launch parameters
 // ---------------------------------------------------------------------------
 
+// Unsigned division by a fixed divisor d >= 1 of numerators below 2^31:
+// q = (umulhi(n, mul) + n) >> shift, with shift = ceil(log2 d) and
+// mul = floor(2^32 * (2^shift - d) / d) + 1 (round-up multiplier method).
+struct FastDiv {
+    unsigned mul = 0, shift = 0;
+    FastDiv() = default;
+    explicit FastDiv(unsigned d) {
+        unsigned l = 0;
+        while ((1ull << l) < d) ++l;
+        shift = l;
+        mul = static_cast<unsigned>(((1ull << 32) * ((1ull << l) - d)) / d + 1);
+    }
+    __host__ __device__ unsigned div(unsigned n) const {
+        return static_cast<unsigned>(((static_cast<unsigned long long>(n) * mul >> 32) + n) >> shift);
+    }
+};
+
 // C[m, n] = act(sum_k A[m, k] * B[n, k] + bias[n] + res[m, n]) for the column
 // range of each sub-slice.  A is either a dense row-major matrix or the
 // implicit im2col view of an NHWC image (conv).  B is [N][K] row-major.
@@ -30,6 +47,7 @@ struct GemmParams {
     int img_h, img_w, cs;   // input H, W and channel storage stride
     int out_h, out_w;       // output H, W
     int kh, kw, stride, pad;
+    FastDiv div_hw, div_w;  // conv: divide by out_h * out_w and by out_w (set by launch_gemm)
     const void* B;          // [N][K]
     const void* bias;       // [N] or null
     const void* res;        // [M][ldc] or null

@@ -510,7 +510,9 @@ static hipError_t run_op(const mopar_model_s& m, int i, const Ptrs& P, int ksub,
             }
             GemmParams g{};
             g.A = src;
-            g.conv = 1;
+            // a 1x1, stride-1, unpadded conv over channels-last pixels is a plain GEMM
+            g.conv = (op.kh == 1 && op.kw == 1 && op.stride == 1 && op.pad == 0) ? 0 : 1;
+            g.lda = inf.cs;
             g.img_h = static_cast<int>(x.dims[2]);
             g.img_w = static_cast<int>(x.dims[3]);
             g.cs = inf.cs;
