@@ -18,10 +18,11 @@
 //
 // Data path.  Operands stream from HBM straight into LDS with
 // global_load_lds_dwordx4 (16 bytes per lane, no VGPR staging), NS stages deep.
-// LDS is fragment-major: for every 16-row block and 32-wide k step, the 64
-// lanes' MFMA fragments sit in one contiguous kilobyte, in lane order -- the
-// order the DMA writes them and the order ds_read_b128 reads them back, so
-// both sides are conflict-free.  Out-of-range chunks (image padding, M/N/K
+// A stage holds 64 bf16 (32 float) of k for every row: 128 bytes, one cache
+// line.  Each load instruction fetches 8 whole rows (the DMA writes lane l's
+// 16 bytes to slot l of a 1 KB LDS block); lanes take the chunks of a row in
+// XOR-swizzled order (chunk (l % 8) ^ row), so the ds_read_b128 of an MFMA
+// fragment -- 16 rows, one chunk each -- hits distinct banks.  Out-of-range chunks (image padding, M/N/K
 // tails) are loaded from a zero page, so every lane issues the same number of
 // loads and the wait counts are exact.  Four waves run v_mfma_f32_16x16x32_bf16
 // (bf16) or v_mfma_f32_16x16x4_f32 (fp32) on their wave tile, with the weight
@@ -104,6 +105,54 @@ __device__ __forceinline__ void store4(T* c, int64_t idx, const float* v, int nv
     for (int q = 0; q < nvalid; ++q) c[idx + q] = static_cast<T>(v[q]);
 }
 
+// eight consecutive elements as raw bits (one 16-byte load for bf16, two for float32)
+template <typename T> struct Raw8 { uint4 w[sizeof(T) / 2]; };
+
+__device__ __forceinline__ bool aligned16(const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; }
+
+template <typename T>
+__device__ __forceinline__ void unpack8(const Raw8<T>& r, float (&v)[8]) {
+    if constexpr (sizeof(T) == 2) {
+        const unsigned w[4] = {r.w[0].x, r.w[0].y, r.w[0].z, r.w[0].w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            v[2 * q] = __uint_as_float(w[q] << 16);
+            v[2 * q + 1] = __uint_as_float(w[q] & 0xffff0000u);
+        }
+    } else {
+        const unsigned w[8] = {r.w[0].x, r.w[0].y, r.w[0].z, r.w[0].w, r.w[1].x, r.w[1].y, r.w[1].z, r.w[1].w};
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] = __uint_as_float(w[q]);
+    }
+}
+
+// v[0..7] = p[i..i+7] for the first nvalid elements, 0 after them (and everywhere when p is null)
+template <typename T>
+__device__ __forceinline__ void load8(const T* p, int64_t i, int nvalid, float (&v)[8]) {
+    if (p && nvalid == 8 && aligned16(p + i)) {
+        unpack8<T>(*reinterpret_cast<const Raw8<T>*>(p + i), v);
+        return;
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q] = (p && q < nvalid) ? ld_f(p, i + q) : 0.0f;
+}
+
+template <typename T>
+__device__ __forceinline__ void store8(T* c, int64_t idx, const float (&v)[8], int nvalid) {
+    if (nvalid == 8 && aligned16(c + idx)) {
+        if constexpr (sizeof(T) == 2) {
+            const bf16x8 o = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3],
+                              (__bf16)v[4], (__bf16)v[5], (__bf16)v[6], (__bf16)v[7]};
+            *reinterpret_cast<bf16x8*>(c + idx) = o;
+        } else {
+            *reinterpret_cast<f32x4*>(c + idx) = f32x4{v[0], v[1], v[2], v[3]};
+            *reinterpret_cast<f32x4*>(c + idx + 4) = f32x4{v[4], v[5], v[6], v[7]};
+        }
+        return;
+    }
+    for (int q = 0; q < nvalid; ++q) c[idx + q] = static_cast<T>(v[q]);
+}
+
 // bias, second bias, residual, activation and the store of 4 consecutive columns
 template <typename T>
 __device__ __forceinline__ void epilogue4(const GemmParams& p, int64_t m, int n, int nvalid, float* v) {
@@ -144,7 +193,11 @@ __device__ __forceinline__ void wait_stages(int r) {
         case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
         case 1: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(L) : "memory"); break;
         case 2: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * L) : "memory"); break;
-        default: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * L) : "memory"); break;
+        case 3: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * L) : "memory"); break;
+        case 4: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(4 * L < 63 ? 4 * L : 63) : "memory"); break;
+        case 5: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(5 * L < 63 ? 5 * L : 63) : "memory"); break;
+        case 6: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(6 * L < 63 ? 6 * L : 63) : "memory"); break;
+        default: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(7 * L < 63 ? 7 * L : 63) : "memory"); break;
     }
 }
 
@@ -158,10 +211,12 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
     constexpr int NBLK = NBA + NBB;             // 1 KB fragment blocks per stage
     constexpr int LMAX = (NBLK + 3) / 4, LMIN = NBLK / 4;
     constexpr int STAGE = NBLK * 64;            // uint4 per stage
-    static_assert(WM * WN == 4 && FM >= 1 && FN >= 1 && NS >= 2 && NS <= 5 && LMIN >= 1, "tile");
+    static_assert(WM * WN == 4 && FM >= 1 && FN >= 1 && NS >= 2 && NS <= 9 && LMIN >= 1, "tile");
     static_assert((NS - 2) * LMIN <= 63, "vmcnt range");
 
-    __shared__ uint4 lds[NS * STAGE];
+    constexpr int LDT = BN + 4;                 // fp32 row stride of the staged output tile (padded)
+    constexpr int LDS_U4 = NS * STAGE > (BM * LDT + 3) / 4 ? NS * STAGE : (BM * LDT + 3) / 4;
+    __shared__ uint4 lds[LDS_U4];
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wm = wave / WN, wn = wave % WN;
@@ -201,7 +256,10 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
     const gptr_t zero = (gptr_t)(kZeroChunk);
 
     // --- this lane's rows in the blocks its wave loads ------------------------------------
-    const int chunk_lo = lane >> 4;             // chunk within the k step
+    // Load block blk of a stage covers 8 rows x 128 bytes (whole cache lines): lane l loads
+    // row 8 * blk + l / 8, k chunk cl = (l % 8) ^ (l / 8) -- the XOR swizzle that keeps the
+    // fragment reads conflict-free -- into LDS slot l of the block.
+    const int cl = (lane & 7) ^ (lane >> 3);    // this lane's chunk of every stage, 0..7
     const T* rowp[LMAX];
     int hb[LMAX], wb[LMAX];
     bool rv[LMAX];
@@ -213,7 +271,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
         hb[i] = wb[i] = 0;
         if (blk >= NBLK) continue;
         if (blk < NBA) {
-            const int row = (blk >> 1) * 16 + (lane & 15);
+            const int row = blk * 8 + (lane >> 3);
             const int64_t m = m0 + row;
             rv[i] = m < p.M;
             const int64_t mc = rv[i] ? m : 0;
@@ -232,65 +290,56 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
                 rowp[i] = Ap + mc * p.lda;
             }
         } else {
-            const int row = ((blk - NBA) >> 1) * 16 + (lane & 15);
+            const int row = (blk - NBA) * 8 + (lane >> 3);
             const int n = n0 + row;
             rv[i] = n < n_hi;
             rowp[i] = Bp + static_cast<int64_t>(rv[i] ? n : n0) * p.K;
         }
     }
 
-    // im2col coordinates (tap row, tap column, channel) of this lane's two chunk
-    // columns, advanced incrementally by one stage (BK = dq * cs + dc elements)
-    int tr[2] = {0, 0}, tcol[2] = {0, 0}, tci[2] = {0, 0};
+    // im2col coordinates (tap row, tap column, channel) of this lane's chunk, advanced
+    // incrementally by one stage (BK = dq * cs + dc elements)
+    int tr = 0, tcol = 0, tci = 0;
     int dq = 0, dc = 0;
     if (CONV) {
         dq = BK / p.cs;
         dc = BK - dq * p.cs;
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            const int k = kt0 * BK + (ks * 4 + chunk_lo) * EPC;
-            const int tap = k / p.cs;
-            tci[ks] = k - tap * p.cs;
-            tr[ks] = tap / p.kw;
-            tcol[ks] = tap - tr[ks] * p.kw;
-        }
+        const int k = kt0 * BK + cl * EPC;
+        const int tap = k / p.cs;
+        tci = k - tap * p.cs;
+        tr = tap / p.kw;
+        tcol = tap - tr * p.kw;
     }
     auto advance = [&]() {
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            tci[ks] += dc;
-            int dt = dq;
-            if (tci[ks] >= p.cs) {
-                tci[ks] -= p.cs;
-                ++dt;
-            }
-            tcol[ks] += dt;
-            while (tcol[ks] >= p.kw) {
-                tcol[ks] -= p.kw;
-                ++tr[ks];
-            }
+        tci += dc;
+        int dt = dq;
+        if (tci >= p.cs) {
+            tci -= p.cs;
+            ++dt;
+        }
+        tcol += dt;
+        while (tcol >= p.kw) {
+            tcol -= p.kw;
+            ++tr;
         }
     };
 
     // issue the loads of stage kt (coordinates must be those of stage kt) into LDS buffer buf
     auto issue = [&](int kt, int buf) {
-        int koff[2] = {0, 0};                   // conv: offset of the tap/channel within the window
-        if (CONV) {
-#pragma unroll
-            for (int ks = 0; ks < 2; ++ks) koff[ks] = (tr[ks] * p.img_w + tcol[ks]) * p.cs + tci[ks];
-        }
+        const int k = kt * BK + cl * EPC;
+        // conv: offset of the tap / channel within the window, and whether the tap row / column
+        // leaves the image is decided per row below
+        const int koff = CONV ? (tr * p.img_w + tcol) * p.cs + tci : 0;
 #pragma unroll
         for (int i = 0; i < LMAX; ++i) {
             const int blk = wave + 4 * i;
             if (blk >= NBLK) continue;          // wave-uniform
-            const int ks = blk & 1;
-            const int k = kt * BK + (ks * 4 + chunk_lo) * EPC;
             bool ok = rv[i] && k < p.K;
             const T* addr;
             if (CONV && blk < NBA) {
-                ok = ok && static_cast<unsigned>(hb[i] + tr[ks]) < static_cast<unsigned>(p.img_h) &&
-                     static_cast<unsigned>(wb[i] + tcol[ks]) < static_cast<unsigned>(p.img_w);
-                addr = rowp[i] + koff[ks];
+                ok = ok && static_cast<unsigned>(hb[i] + tr) < static_cast<unsigned>(p.img_h) &&
+                     static_cast<unsigned>(wb[i] + tcol) < static_cast<unsigned>(p.img_w);
+                addr = rowp[i] + koff;
             } else {
                 addr = rowp[i] + k;
             }
@@ -306,6 +355,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
         for (int b = 0; b < FN; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     // --- epilogue operands, fetched now so their latency hides under the main loop ---------
+    // MFMA layout (used by the LSTM cell): lane holds row mrow[a], columns ncol[b]..+3
     int64_t mrow[FM];
     int ncol[FN], nval[FN];
 #pragma unroll
@@ -315,20 +365,33 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
         ncol[b] = n0 + wn * TN + b * 16 + (lane >> 4) * 4;
         nval[b] = max(0, min(4, n_hi - ncol[b]));
     }
+    // chunk layout (everything else): thread owns 8 consecutive columns c0..c0+7 of tile
+    // rows cr, cr + RPP, ...; after the staging through LDS each chunk is one 16-byte store
+    constexpr int CPR = BN / 8, RPP = 256 / CPR, NCH = (BM + RPP - 1) / RPP;
+    const int cc = threadIdx.x % CPR, cr = threadIdx.x / CPR;
+    const int c0 = n0 + cc * 8;
+    const int cval = max(0, min(8, n_hi - c0));
+    float bias8[8];
+    load8<T>(static_cast<const T*>(p.bias), c0, cval, bias8);
+    if (p.bias2) {
+        float t8[8];
+        load8<T>(static_cast<const T*>(p.bias2), c0, cval, t8);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) bias8[e] += t8[e];
+    }
     const bool direct = p.splits == 1 && p.epi == EPI_STD;   // this block finishes its outputs
-    // residual kept packed (raw bits of 4 elements) so the prefetch costs few registers
-    typedef typename std::conditional<sizeof(T) == 2, uint2, uint4>::type Raw4;
-    Raw4 rraw[FM][FN];
-    const bool have_res = direct && p.res != nullptr;
+    // residual kept as raw bits so the prefetch costs few registers
+    Raw8<T> rraw[NCH];
+    bool rfast[NCH];
 #pragma unroll
-    for (int a = 0; a < FM; ++a)
-#pragma unroll
-        for (int b = 0; b < FN; ++b) {
-            const bool ok = have_res && mrow[a] < p.M && nval[b] == 4;
-            const int64_t idx = ok ? mrow[a] * p.ldc + ncol[b] : 0;
-            rraw[a][b] = Raw4{};
-            if (ok && (idx & 3) == 0) rraw[a][b] = *reinterpret_cast<const Raw4*>(static_cast<const T*>(p.res) + idx);
-        }
+    for (int i = 0; i < NCH; ++i) {
+        const int64_t m = m0 + cr + i * RPP;
+        const int64_t idx = m * p.ldc + c0;
+        rfast[i] = direct && p.res && cr + i * RPP < BM && m < p.M && cval == 8 &&
+                   aligned16(static_cast<const T*>(p.res) + idx);
+        rraw[i] = Raw8<T>{};
+        if (rfast[i]) rraw[i] = *reinterpret_cast<const Raw8<T>*>(static_cast<const T*>(p.res) + idx);
+    }
 
     // prologue: NS-1 stages in flight (coordinates then stand at stage kt0 + NS - 1)
 #pragma unroll
@@ -337,13 +400,18 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
         if (CONV) advance();
     }
 
-    // LDS byte address of this lane's slot in fragment block 0 of stage 0
-    const unsigned lds0 = static_cast<unsigned>(reinterpret_cast<size_t>((lds_ptr_t)(&lds[0]))) + lane * 16;
+    // LDS byte offsets of this lane's MFMA fragment (row l % 16 of a 16-row block, chunk
+    // 4 * ks + l / 16) for the two k steps of a stage, relative to the block's first 8 rows
+    const unsigned lds0 = static_cast<unsigned>(reinterpret_cast<size_t>((lds_ptr_t)(&lds[0])));
+    unsigned foff[2];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+        foff[ks] = lds0 + ((((lane >> 3) & 1) * 64 + (lane & 7) * 8 + ((ks * 4 + (lane >> 4)) ^ (lane & 7))) * 16);
     auto read_frags = [&](unsigned sbase, int ks, u32x4 (&af)[FM], u32x4 (&bf)[FN]) {
 #pragma unroll
-        for (int a = 0; a < FM; ++a) af[a] = lds_read16(sbase + ((((wm * TM + a * 16) >> 4) * 2 + ks) * 64) * 16);
+        for (int a = 0; a < FM; ++a) af[a] = lds_read16(sbase + foff[ks] + ((wm * TM + a * 16) >> 3) * 1024);
 #pragma unroll
-        for (int b = 0; b < FN; ++b) bf[b] = lds_read16(sbase + ((NBA + ((wn * TN + b * 16) >> 4) * 2 + ks) * 64) * 16);
+        for (int b = 0; b < FN; ++b) bf[b] = lds_read16(sbase + foff[ks] + (NBA + ((wn * TN + b * 16) >> 3)) * 1024);
     };
     auto mfmas = [&](u32x4 (&af)[FM], u32x4 (&bf)[FN]) {
 #pragma unroll
@@ -372,7 +440,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
             issue(kt + NS - 1, (kt - kt0 + NS - 1) % NS);
             if (CONV) advance();
         }
-        const unsigned sbase = lds0 + buf * STAGE * 16;
+        const unsigned sbase = buf * STAGE * 16;
         u32x4 a0[FM], b0[FN], a1[FM], b1[FN];
         read_frags(sbase, 0, a0, b0);
         lds_wait();
@@ -390,23 +458,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
         mfmas(a1, b1);
     }
 
-    // --- epilogue: lane holds row m, columns n..n+3 ----------------------------------------
-    // Every operand was loaded before the first store (stores could alias the loads, so
-    // interleaving them would serialise one memory round trip per tile).
-    if (p.splits > 1) {                       // raw partial sums; the reduce kernel finishes
-#pragma unroll
-        for (int a = 0; a < FM; ++a)
-#pragma unroll
-            for (int b = 0; b < FN; ++b) {
-                if (mrow[a] >= p.M || nval[b] == 0) continue;
-                float* dst = p.partial + (static_cast<int64_t>(split) * p.M + mrow[a]) * p.N + ncol[b];
-                if (nval[b] == 4 && ((reinterpret_cast<uintptr_t>(dst) & 15) == 0))
-                    *reinterpret_cast<f32x4*>(dst) = acc[a][b];
-                else
-                    for (int e = 0; e < nval[b]; ++e) dst[e] = acc[a][b][e];
-            }
-        return;
-    }
+    // --- epilogue --------------------------------------------------------------------------
     if (p.epi == EPI_LSTM) {
         // gates i, f, g, o of unit n / 4 (n is a multiple of 4 and the whole group is valid)
         f32x4 g4[FM][FN];
@@ -434,51 +486,65 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
             }
         return;
     }
-    float bias[FN][4];
-#pragma unroll
-    for (int b = 0; b < FN; ++b) {
-        for (int q = 0; q < 4; ++q) bias[b][q] = 0.0f;
-        if (nval[b] > 0) {
-            float t2[4];
-            if (p.bias) ld4(static_cast<const T*>(p.bias), ncol[b], nval[b], bias[b]);
-            if (p.bias2) {
-                ld4(static_cast<const T*>(p.bias2), ncol[b], nval[b], t2);
-                for (int q = 0; q < 4; ++q) bias[b][q] += t2[q];
-            }
-        }
-    }
+
+    // Stage the fp32 tile through LDS (row-major, padded rows) so that every thread then
+    // owns whole 8-column chunks: full-line stores, and bias / residual as vector loads.
+    __syncthreads();                          // every wave is done with the operand stages
+    float* tile = reinterpret_cast<float*>(lds);
 #pragma unroll
     for (int a = 0; a < FM; ++a)
 #pragma unroll
         for (int b = 0; b < FN; ++b) {
-            if (mrow[a] >= p.M || nval[b] == 0) continue;
-            float rsd[4] = {0.f, 0.f, 0.f, 0.f};
-            if (have_res) {
-                const int64_t idx = mrow[a] * p.ldc + ncol[b];
-                if (nval[b] == 4 && (idx & 3) == 0) {
-                    if constexpr (sizeof(T) == 2) {
-                        const uint2 r = rraw[a][b];
-                        rsd[0] = __uint_as_float(r.x << 16);
-                        rsd[1] = __uint_as_float(r.x & 0xffff0000u);
-                        rsd[2] = __uint_as_float(r.y << 16);
-                        rsd[3] = __uint_as_float(r.y & 0xffff0000u);
-                    } else {
-                        const uint4 r = rraw[a][b];
-                        rsd[0] = __uint_as_float(r.x), rsd[1] = __uint_as_float(r.y);
-                        rsd[2] = __uint_as_float(r.z), rsd[3] = __uint_as_float(r.w);
-                    }
-                } else {
-                    ld4(static_cast<const T*>(p.res), idx, nval[b], rsd);
-                }
-            }
-            float v[4];
-            for (int q = 0; q < 4; ++q) v[q] = act_f((acc[a][b][q] + bias[b][q]) + rsd[q], p.act);
-            const int64_t idx = mrow[a] * p.ldc + ncol[b];
-            if (p.out_f32)
-                store4<float>(static_cast<float*>(p.C), idx, v, nval[b]);
-            else
-                store4<T>(static_cast<T*>(p.C), idx, v, nval[b]);
+            const int row = wm * TM + a * 16 + (lane & 15), col = wn * TN + b * 16 + (lane >> 4) * 4;
+            *reinterpret_cast<f32x4*>(tile + row * LDT + col) = acc[a][b];
         }
+    __syncthreads();
+    auto tile8 = [&](int r, float (&v)[8]) {
+        const f32x4 lo = *reinterpret_cast<const f32x4*>(tile + r * LDT + cc * 8);
+        const f32x4 hi = *reinterpret_cast<const f32x4*>(tile + r * LDT + cc * 8 + 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = lo[e], v[4 + e] = hi[e];
+    };
+    // (v + bias) + residual, activation, store: the same operations, in the same order,
+    // whether the sums come from this block or from the split-K partials
+    auto finish = [&](int64_t m, float (&v)[8], const float (&rsd)[8]) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = act_f((v[e] + bias8[e]) + rsd[e], p.act);
+        const int64_t idx = m * p.ldc + c0;
+        if (p.out_f32)
+            store8<float>(static_cast<float*>(p.C), idx, v, cval);
+        else
+            store8<T>(static_cast<T*>(p.C), idx, v, cval);
+    };
+
+    if (direct) {
+#pragma unroll
+        for (int i = 0; i < NCH; ++i) {
+            const int r = cr + i * RPP;
+            const int64_t m = m0 + r;
+            if (r >= BM || m >= p.M || cval == 0) continue;
+            float v[8], rsd[8];
+            tile8(r, v);
+            if (rfast[i])
+                unpack8<T>(rraw[i], rsd);
+            else
+                load8<T>(static_cast<const T*>(p.res), m * p.ldc + c0, p.res ? cval : 0, rsd);
+            finish(m, v, rsd);
+        }
+        return;
+    }
+
+    // split-K: this block's partial sums; splitk_reduce_kernel adds them up in split order
+    float* part = p.partial + static_cast<int64_t>(split) * p.M * p.N;
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+        const int r = cr + i * RPP;
+        const int64_t m = m0 + r;
+        if (r >= BM || m >= p.M || cval == 0) continue;
+        float v[8];
+        tile8(r, v);
+        store8<float>(part, m * p.N + c0, v, cval);
+    }
 }
 
 // Split-K finish: sum the partials in split order, then the usual epilogue.
@@ -551,7 +617,11 @@ static hipError_t dispatch(const GemmParams& p, hipStream_t st) {
     auto blocks = [&](int64_t bm_tiles, int bn) { return bm_tiles * ((width + bn - 1) / bn) * p.ksub * p.splits; };
     if (width >= 128 && blocks(mt, 128) >= kCUs) return launch_cfg<T, 128, 128, 2, 2, 2>(p, width, st);
     if (width >= 64 && blocks(mt, 64) >= kCUs) return launch_cfg<T, 128, 64, 2, 2, 3>(p, width, st);
-    if (width >= 64) return launch_cfg<T, 64, 64, 2, 2, 4>(p, width, st);
+    if (width >= 64) {
+        // one block per CU or fewer: a deep pipeline keeps enough loads in flight
+        if (blocks((p.M + 63) / 64, 64) <= kCUs) return launch_cfg<T, 64, 64, 2, 2, 8>(p, width, st);
+        return launch_cfg<T, 64, 64, 2, 2, 4>(p, width, st);
+    }
     if (width >= 32) {
         if (blocks(mt, 32) >= kCUs) return launch_cfg<T, 128, 32, 4, 1, 3>(p, width, st);
         return launch_cfg<T, 64, 32, 2, 2, 4>(p, width, st);
