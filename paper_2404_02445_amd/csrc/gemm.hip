@@ -202,23 +202,25 @@ __device__ __forceinline__ void wait_stages(int r) {
 }
 
 template <typename T, int BM, int BN, int WM, int WN, int NS, bool CONV>
-__global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
+__global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const GemmParams p) {
     constexpr int EPC = Elt<T>::EPC;
     constexpr int BK = 8 * EPC;                 // K elements per stage: two 32-wide (bf16) k steps
     constexpr int TM = BM / WM, TN = BN / WN;   // wave tile
     constexpr int FM = TM / 16, FN = TN / 16;   // 16x16 MFMA tiles per wave
     constexpr int NBA = BM / 16 * 2, NBB = BN / 16 * 2;
     constexpr int NBLK = NBA + NBB;             // 1 KB fragment blocks per stage
-    constexpr int LMAX = (NBLK + 3) / 4, LMIN = NBLK / 4;
+    constexpr int NW = WM * WN, NT = NW * 64;   // waves and threads per block
+    constexpr int LMAX = (NBLK + NW - 1) / NW, LMIN = NBLK / NW;
     constexpr int STAGE = NBLK * 64;            // uint4 per stage
-    static_assert(WM * WN == 4 && FM >= 1 && FN >= 1 && NS >= 2 && NS <= 9 && LMIN >= 1, "tile");
+    static_assert((NW == 4 || NW == 8) && FM >= 1 && FN >= 1 && NS >= 2 && NS <= 9 && LMIN >= 1, "tile");
     static_assert((NS - 2) * LMIN <= 63, "vmcnt range");
 
     constexpr int LDT = BN + 4;                 // fp32 row stride of the staged output tile (padded)
     constexpr int LDS_U4 = NS * STAGE > (BM * LDT + 3) / 4 ? NS * STAGE : (BM * LDT + 3) / 4;
     __shared__ uint4 lds[LDS_U4];
 
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // scalar: load blocks are wave-uniform
     const int wm = wave / WN, wn = wave % WN;
 
     // --- block -> (m tile, split, sub-slice, n tile), XCD-grouped -------------------------
@@ -260,21 +262,23 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
     // row 8 * blk + l / 8, k chunk cl = (l % 8) ^ (l / 8) -- the XOR swizzle that keeps the
     // fragment reads conflict-free -- into LDS slot l of the block.
     const int cl = (lane & 7) ^ (lane >> 3);    // this lane's chunk of every stage, 0..7
+    // Rows past M (A) or past the sub-slice (B) load a real row (the last valid one) instead:
+    // the products they feed are never stored, and every load stays unconditional.
+    // Dense operands: a 32-bit byte offset per lane from a wave-uniform base that advances by
+    // one stage per step.  Conv A: a per-row pointer to the window plus its top-left corner.
+    unsigned voff[LMAX];
     const T* rowp[LMAX];
     int hb[LMAX], wb[LMAX];
-    bool rv[LMAX];
 #pragma unroll
     for (int i = 0; i < LMAX; ++i) {
-        const int blk = wave + 4 * i;
-        rv[i] = false;
+        const int blk = wave + NW * i;
+        voff[i] = 0;
         rowp[i] = Bp;
         hb[i] = wb[i] = 0;
         if (blk >= NBLK) continue;
         if (blk < NBA) {
-            const int row = blk * 8 + (lane >> 3);
-            const int64_t m = m0 + row;
-            rv[i] = m < p.M;
-            const int64_t mc = rv[i] ? m : 0;
+            const int64_t m = m0 + blk * 8 + (lane >> 3);
+            const int64_t mc = m < p.M ? m : p.M - 1;
             if (CONV) {
                 // M < 2^31, so the pixel decode runs in 32 bits with precomputed divisors;
                 // the row pointer already includes the window's top-left offset
@@ -287,13 +291,12 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
                 rowp[i] = Ap + static_cast<int64_t>(img) * p.img_h * p.img_w * p.cs +
                           static_cast<int64_t>(hb[i] * p.img_w + wb[i]) * p.cs;
             } else {
-                rowp[i] = Ap + mc * p.lda;
+                voff[i] = static_cast<unsigned>((mc * p.lda + cl * EPC) * static_cast<int64_t>(sizeof(T)));
             }
         } else {
-            const int row = (blk - NBA) * 8 + (lane >> 3);
-            const int n = n0 + row;
-            rv[i] = n < n_hi;
-            rowp[i] = Bp + static_cast<int64_t>(rv[i] ? n : n0) * p.K;
+            const int n = n0 + (blk - NBA) * 8 + (lane >> 3);
+            const int nc = n < n_hi ? n : n_hi - 1;
+            voff[i] = static_cast<unsigned>((static_cast<int64_t>(nc) * p.K + cl * EPC) * static_cast<int64_t>(sizeof(T)));
         }
     }
 
@@ -327,24 +330,34 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
     // issue the loads of stage kt (coordinates must be those of stage kt) into LDS buffer buf
     auto issue = [&](int kt, int buf) {
         const int k = kt * BK + cl * EPC;
-        // conv: offset of the tap / channel within the window, and whether the tap row / column
-        // leaves the image is decided per row below
+        const bool tail = (kt + 1) * BK > p.K;          // uniform: only the last stage may pass K
+        // conv: offset of the tap / channel within the window
         const int koff = CONV ? (tr * p.img_w + tcol) * p.cs + tci : 0;
+        const char* abase = reinterpret_cast<const char*>(Ap) + static_cast<int64_t>(kt) * BK * sizeof(T);
+        const char* bbase = reinterpret_cast<const char*>(Bp) + static_cast<int64_t>(kt) * BK * sizeof(T);
+        auto conv_src = [&](int i) -> gptr_t {
+            const bool ok = (!tail || k < p.K) &&
+                            static_cast<unsigned>(hb[i] + tr) < static_cast<unsigned>(p.img_h) &&
+                            static_cast<unsigned>(wb[i] + tcol) < static_cast<unsigned>(p.img_w);
+            return ok ? (gptr_t)(rowp[i] + koff) : zero;
+        };
+        if (!tail) {
 #pragma unroll
-        for (int i = 0; i < LMAX; ++i) {
-            const int blk = wave + 4 * i;
-            if (blk >= NBLK) continue;          // wave-uniform
-            bool ok = rv[i] && k < p.K;
-            const T* addr;
-            if (CONV && blk < NBA) {
-                ok = ok && static_cast<unsigned>(hb[i] + tr) < static_cast<unsigned>(p.img_h) &&
-                     static_cast<unsigned>(wb[i] + tcol) < static_cast<unsigned>(p.img_w);
-                addr = rowp[i] + koff;
-            } else {
-                addr = rowp[i] + k;
+            for (int i = 0; i < LMAX; ++i) {
+                const int blk = wave + NW * i;
+                if (blk >= NBLK) continue;      // wave-uniform
+                const gptr_t src = (CONV && blk < NBA) ? conv_src(i) : (gptr_t)((blk < NBA ? abase : bbase) + voff[i]);
+                __builtin_amdgcn_global_load_lds(src, (lds_ptr_t)(&lds[buf * STAGE + blk * 64]), 16, 0, 0);
             }
-            const gptr_t src = ok ? (gptr_t)(addr) : zero;
-            __builtin_amdgcn_global_load_lds(src, (lds_ptr_t)(&lds[buf * STAGE + blk * 64]), 16, 0, 0);
+        } else {                                // K tail: chunks past K read zeros on both operands
+#pragma unroll
+            for (int i = 0; i < LMAX; ++i) {
+                const int blk = wave + NW * i;
+                if (blk >= NBLK) continue;
+                gptr_t src = (CONV && blk < NBA) ? conv_src(i) : (gptr_t)((blk < NBA ? abase : bbase) + voff[i]);
+                if (k >= p.K) src = zero;
+                __builtin_amdgcn_global_load_lds(src, (lds_ptr_t)(&lds[buf * STAGE + blk * 64]), 16, 0, 0);
+            }
         }
     };
 
@@ -367,7 +380,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmParams p) {
     }
     // chunk layout (everything else): thread owns 8 consecutive columns c0..c0+7 of tile
     // rows cr, cr + RPP, ...; after the staging through LDS each chunk is one 16-byte store
-    constexpr int CPR = BN / 8, RPP = 256 / CPR, NCH = (BM + RPP - 1) / RPP;
+    constexpr int CPR = BN / 8, RPP = NT / CPR, NCH = (BM + RPP - 1) / RPP;
     const int cc = threadIdx.x % CPR, cr = threadIdx.x / CPR;
     const int c0 = n0 + cc * 8;
     const int cval = max(0, min(8, n_hi - c0));
@@ -596,12 +609,11 @@ template <typename T, int BM, int BN, int WM, int WN, int NS>
 static hipError_t launch_cfg(const GemmParams& p, int width, hipStream_t st) {
     const int64_t total = ((p.M + BM - 1) / BM) * ((width + BN - 1) / BN) * p.ksub * p.splits;
     const int64_t grid = (total + 7) / 8 * 8;
+    const dim3 block(WM * WN * 64);
     if (p.conv)
-        hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, NS, true>), dim3(static_cast<unsigned>(grid)), dim3(256), 0,
-                           st, p);
+        hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, NS, true>), dim3(static_cast<unsigned>(grid)), block, 0, st, p);
     else
-        hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, NS, false>), dim3(static_cast<unsigned>(grid)), dim3(256),
-                           0, st, p);
+        hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, NS, false>), dim3(static_cast<unsigned>(grid)), block, 0, st, p);
     return hipGetLastError();
 }
 
@@ -610,23 +622,19 @@ static hipError_t dispatch(const GemmParams& p, hipStream_t st) {
     const int width = (p.N + p.ksub - 1) / p.ksub;   // widest sub-slice
     if (p.M <= 16) return launch_cfg<T, 16, 64, 1, 4, 4>(p, width, st);
     if (p.M <= 64 || p.epi == EPI_LSTM) {
-        if (width >= 64 && p.epi != EPI_LSTM) return launch_cfg<T, 64, 64, 2, 2, 4>(p, width, st);
+        if (width >= 64 && p.epi != EPI_LSTM) return launch_cfg<T, 64, 64, 2, 4, 4>(p, width, st);
         return launch_cfg<T, 64, 16, 4, 1, 4>(p, width, st);
     }
     const int64_t mt = (p.M + 127) / 128;
     auto blocks = [&](int64_t bm_tiles, int bn) { return bm_tiles * ((width + bn - 1) / bn) * p.ksub * p.splits; };
-    if (width >= 128 && blocks(mt, 128) >= kCUs) return launch_cfg<T, 128, 128, 2, 2, 2>(p, width, st);
-    if (width >= 64 && blocks(mt, 64) >= kCUs) return launch_cfg<T, 128, 64, 2, 2, 3>(p, width, st);
-    if (width >= 64) {
-        // one block per CU or fewer: a deep pipeline keeps enough loads in flight
-        if (blocks((p.M + 63) / 64, 64) <= kCUs) return launch_cfg<T, 64, 64, 2, 2, 8>(p, width, st);
-        return launch_cfg<T, 64, 64, 2, 2, 4>(p, width, st);
-    }
+    if (width >= 128 && blocks(mt, 128) >= kCUs) return launch_cfg<T, 128, 128, 2, 4, 2>(p, width, st);
+    if (width >= 64 && blocks(mt, 64) >= kCUs) return launch_cfg<T, 128, 64, 4, 2, 3>(p, width, st);
+    if (width >= 64) return launch_cfg<T, 64, 64, 2, 4, 4>(p, width, st);
     if (width >= 32) {
-        if (blocks(mt, 32) >= kCUs) return launch_cfg<T, 128, 32, 4, 1, 3>(p, width, st);
-        return launch_cfg<T, 64, 32, 2, 2, 4>(p, width, st);
+        if (blocks(mt, 32) >= kCUs) return launch_cfg<T, 128, 32, 4, 2, 3>(p, width, st);
+        return launch_cfg<T, 64, 32, 4, 2, 4>(p, width, st);
     }
-    if (blocks(mt, 16) >= kCUs) return launch_cfg<T, 128, 16, 4, 1, 4>(p, width, st);
+    if (blocks(mt, 16) >= kCUs) return launch_cfg<T, 128, 16, 8, 1, 4>(p, width, st);
     return launch_cfg<T, 64, 16, 4, 1, 4>(p, width, st);
 }
 
@@ -639,6 +647,10 @@ hipError_t launch_gemm(const GemmParams& params, int dtype, hipStream_t stream) 
         p.div_w = FastDiv(static_cast<unsigned>(p.out_w));
     }
     if (p.M <= 0 || p.N <= 0) return hipSuccess;
+    // dense operands are addressed with 32-bit byte offsets
+    const int64_t esz = dtype == MOPAR_BF16 ? 2 : 4;
+    if ((!p.conv && p.M * p.lda * esz >= (int64_t(1) << 32)) || int64_t(p.N) * p.K * esz >= (int64_t(1) << 32))
+        return hipErrorInvalidValue;
     if (p.splits < 1 || (p.splits > 1 && (!p.partial || p.epi != EPI_STD))) return hipErrorInvalidValue;
     hipError_t e = dtype == MOPAR_BF16 ? dispatch<__bf16>(p, stream) : dispatch<float>(p, stream);
     if (e != hipSuccess || p.splits == 1) return e;
