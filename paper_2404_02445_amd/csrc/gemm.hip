@@ -600,6 +600,8 @@ int gemm_splits(int64_t M, int N, int K, int dtype, int epi) {
     const int bk = dtype == MOPAR_BF16 ? 64 : 32;
     const int64_t nk = (K + bk - 1) / bk;
     const int64_t tiles = ((M + 63) / 64) * ((N + 63) / 64);   // reference tiling, independent of k
+    // the reduce pass costs about as much as a dozen k stages: split only long K loops
+    if (nk < 24) return 1;
     int s = 1;
     while (s < 16 && tiles * s < kCUs && nk / (2 * s) >= 4) s *= 2;
     return s;

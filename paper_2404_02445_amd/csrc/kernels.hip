@@ -32,23 +32,31 @@ static inline unsigned blocks_for(int64_t n, int per_block) {
 // ---------------------------------------------------------------------------
 // NCHW float32 (model input) -> NHWC in the model dtype, channels padded to cs.
 // One thread per pixel: C strided reads (coalesced across neighbouring w),
-// one cs-wide contiguous write.
+// cs-wide contiguous 16-byte writes.  Sizes below 2^31 elements (host-checked).
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ void nchw_to_nhwc_kernel(const float* __restrict__ x, T* __restrict__ y, int n, int c, int h, int w,
                                     int cs) {
-    const int64_t pix = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    const int64_t hw = static_cast<int64_t>(h) * w;
-    if (pix >= static_cast<int64_t>(n) * hw) return;
-    const int64_t img = pix / hw, r = pix - img * hw;
-    const float* src = x + img * c * hw + r;
-    T* dst = y + pix * cs;
-    for (int ch = 0; ch < cs; ++ch) dst[ch] = from_f<T>(ch < c ? src[ch * hw] : 0.0f);
+    constexpr int V = Vec<T>::N;
+    const int pix = blockIdx.x * blockDim.x + threadIdx.x;
+    const int hw = h * w;
+    if (pix >= n * hw) return;
+    const int img = pix / hw, r = pix - img * hw;
+    const float* src = x + static_cast<int64_t>(img) * c * hw + r;
+    T* dst = y + static_cast<int64_t>(pix) * cs;
+    for (int c0 = 0; c0 < cs; c0 += V) {           // cs is a multiple of V
+        uint4 out;
+        T* o = reinterpret_cast<T*>(&out);
+#pragma unroll
+        for (int i = 0; i < V; ++i) o[i] = from_f<T>(c0 + i < c ? src[static_cast<int64_t>(c0 + i) * hw] : 0.0f);
+        *reinterpret_cast<uint4*>(dst + c0) = out;
+    }
 }
 
 hipError_t launch_nchw_to_nhwc(const float* x, void* y, int n, int c, int h, int w, int cs, int dtype,
                                hipStream_t s) {
     const int64_t pix = static_cast<int64_t>(n) * h * w;
+    if (pix * cs >= (int64_t(1) << 31) || cs % (dtype == MOPAR_BF16 ? 8 : 4) != 0) return hipErrorInvalidValue;
     if (dtype == MOPAR_BF16)
         hipLaunchKernelGGL(nchw_to_nhwc_kernel<__bf16>, dim3(blocks_for(pix, 256)), dim3(256), 0, s, x,
                            static_cast<__bf16*>(y), n, c, h, w, cs);
@@ -60,30 +68,30 @@ hipError_t launch_nchw_to_nhwc(const float* x, void* y, int n, int c, int h, int
 
 // ---------------------------------------------------------------------------
 // Max pool, NHWC: one thread per (output pixel, 16-byte channel group).
-// Window positions outside the image are skipped (they count as -inf).
+// Window positions outside the image are skipped (they count as -inf).  KW > 0
+// fixes the window size at compile time so all its loads issue together.
+// Sizes below 2^31 elements (host-checked): 32-bit index math.
 // ---------------------------------------------------------------------------
-template <typename T>
-__global__ void maxpool_kernel(const T* __restrict__ x, T* __restrict__ y, int n, int h, int w, int c, int k,
+template <typename T, int KW>
+__global__ void maxpool_kernel(const T* __restrict__ x, T* __restrict__ y, int n, int h, int w, int c, int kr,
                                int stride, int pad, int ho, int wo) {
     constexpr int V = Vec<T>::N;
+    const int k = KW > 0 ? KW : kr;
     const int groups = c / V;
-    const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    const int64_t total = static_cast<int64_t>(n) * ho * wo * groups;
-    if (t >= total) return;
-    const int g = static_cast<int>(t % groups);
-    const int64_t pix = t / groups;
-    const int ox = static_cast<int>(pix % wo);
-    const int oy = static_cast<int>((pix / wo) % ho);
-    const int64_t img = pix / (static_cast<int64_t>(wo) * ho);
+    const int t = blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= n * ho * wo * groups) return;
+    const int pix = t / groups, g = t - pix * groups;
+    const int img = pix / (ho * wo), rem = pix - img * (ho * wo);
+    const int oy = rem / wo, ox = rem - oy * wo;
     float m[V];
 #pragma unroll
     for (int i = 0; i < V; ++i) m[i] = -INFINITY;
-    for (int r = 0; r < k; ++r) {
+    for (int r = 0; r < k; ++r) {          // fully unrolled when KW > 0
         const int iy = oy * stride - pad + r;
-        if (iy < 0 || iy >= h) continue;
         for (int q = 0; q < k; ++q) {
             const int ix = ox * stride - pad + q;
-            if (ix < 0 || ix >= w) continue;
+            if (static_cast<unsigned>(iy) >= static_cast<unsigned>(h) || static_cast<unsigned>(ix) >= static_cast<unsigned>(w))
+                continue;
             const uint4 raw = *reinterpret_cast<const uint4*>(x + ((img * h + iy) * w + ix) * c + g * V);
             const T* e = reinterpret_cast<const T*>(&raw);
 #pragma unroll
@@ -97,26 +105,77 @@ __global__ void maxpool_kernel(const T* __restrict__ x, T* __restrict__ y, int n
     *reinterpret_cast<uint4*>(y + pix * c + g * V) = out;
 }
 
+template <typename T>
+static void maxpool_launch(const void* x, void* y, int n, int h, int w, int c, int k, int stride, int pad, int ho,
+                           int wo, hipStream_t s) {
+    const int64_t total = static_cast<int64_t>(n) * ho * wo * (c / Vec<T>::N);
+    const T* xp = static_cast<const T*>(x);
+    T* yp = static_cast<T*>(y);
+    if (k == 3)
+        hipLaunchKernelGGL((maxpool_kernel<T, 3>), dim3(blocks_for(total, 256)), dim3(256), 0, s, xp, yp, n, h, w, c, k,
+                           stride, pad, ho, wo);
+    else if (k == 2)
+        hipLaunchKernelGGL((maxpool_kernel<T, 2>), dim3(blocks_for(total, 256)), dim3(256), 0, s, xp, yp, n, h, w, c, k,
+                           stride, pad, ho, wo);
+    else
+        hipLaunchKernelGGL((maxpool_kernel<T, 0>), dim3(blocks_for(total, 256)), dim3(256), 0, s, xp, yp, n, h, w, c, k,
+                           stride, pad, ho, wo);
+}
+
 hipError_t launch_maxpool(const void* x, void* y, int n, int h, int w, int c, int k, int stride, int pad, int ho,
                           int wo, int dtype, hipStream_t s) {
-    if (dtype == MOPAR_BF16) {
-        const int64_t total = static_cast<int64_t>(n) * ho * wo * (c / 8);
-        hipLaunchKernelGGL(maxpool_kernel<__bf16>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
-                           static_cast<const __bf16*>(x), static_cast<__bf16*>(y), n, h, w, c, k, stride, pad, ho, wo);
-    } else {
-        const int64_t total = static_cast<int64_t>(n) * ho * wo * (c / 4);
-        hipLaunchKernelGGL(maxpool_kernel<float>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
-                           static_cast<const float*>(x), static_cast<float*>(y), n, h, w, c, k, stride, pad, ho, wo);
-    }
+    if (static_cast<int64_t>(n) * h * w * c >= (int64_t(1) << 31)) return hipErrorInvalidValue;
+    if (dtype == MOPAR_BF16)
+        maxpool_launch<__bf16>(x, y, n, h, w, c, k, stride, pad, ho, wo, s);
+    else
+        maxpool_launch<float>(x, y, n, h, w, c, k, stride, pad, ho, wo, s);
     return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
-// Global average pool, NHWC -> [N][C]: one thread per (n, c); reads are
-// coalesced across c.  fp32 sum in pixel order, then one division.
+// Global average pool, NHWC -> [N][C].  A block owns one image and 8 channel
+// chunks (16 bytes each); its 256 threads are 8 chunks x 32 pixel slices.
+// Slice s sums pixels s, s + 32, ... in order (fp32); the 32 slice sums are
+// then added in slice order and divided once: a fixed order, so the result
+// is reproducible.  Channel counts that are not a whole number of chunks use
+// one thread per channel, summing pixels in order.
 // ---------------------------------------------------------------------------
+constexpr int AP_SLICES = 32, AP_CHUNKS = 8;
+
 template <typename T>
-__global__ void avgpool_kernel(const T* __restrict__ x, T* __restrict__ y, int n, int hw, int c) {
+__global__ __launch_bounds__(256) void avgpool_kernel(const T* __restrict__ x, T* __restrict__ y, int hw, int c) {
+    constexpr int V = Vec<T>::N;
+    __shared__ float part[AP_SLICES][AP_CHUNKS * V];
+    const int img = blockIdx.y;
+    const int chunk = threadIdx.x % AP_CHUNKS, slice = threadIdx.x / AP_CHUNKS;
+    const int c0 = (blockIdx.x * AP_CHUNKS + chunk) * V;
+    float sum[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) sum[i] = 0.0f;
+    if (c0 < c) {
+        const T* p = x + static_cast<int64_t>(img) * hw * c + c0;
+        for (int px = slice; px < hw; px += AP_SLICES) {
+            const uint4 raw = *reinterpret_cast<const uint4*>(p + static_cast<int64_t>(px) * c);
+            const T* e = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+            for (int i = 0; i < V; ++i) sum[i] += to_f(e[i]);
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < V; ++i) part[slice][chunk * V + i] = sum[i];
+    __syncthreads();
+    if (threadIdx.x < AP_CHUNKS * V) {
+        const int ch = blockIdx.x * AP_CHUNKS * V + threadIdx.x;
+        if (ch < c) {
+            float s = 0.0f;
+            for (int sl = 0; sl < AP_SLICES; ++sl) s += part[sl][threadIdx.x];
+            y[static_cast<int64_t>(img) * c + ch] = from_f<T>(s / static_cast<float>(hw));
+        }
+    }
+}
+
+template <typename T>
+__global__ void avgpool_channel_kernel(const T* __restrict__ x, T* __restrict__ y, int n, int hw, int c) {
     const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     if (t >= static_cast<int64_t>(n) * c) return;
     const int64_t img = t / c;
@@ -127,14 +186,23 @@ __global__ void avgpool_kernel(const T* __restrict__ x, T* __restrict__ y, int n
     y[t] = from_f<T>(s / static_cast<float>(hw));
 }
 
+template <typename T>
+static void avgpool_launch(const void* x, void* y, int n, int hw, int c, hipStream_t s) {
+    constexpr int V = Vec<T>::N;
+    if (c % V == 0) {
+        const dim3 grid((c / V + AP_CHUNKS - 1) / AP_CHUNKS, n);
+        hipLaunchKernelGGL(avgpool_kernel<T>, grid, dim3(256), 0, s, static_cast<const T*>(x), static_cast<T*>(y), hw, c);
+    } else {
+        hipLaunchKernelGGL(avgpool_channel_kernel<T>, dim3(blocks_for(static_cast<int64_t>(n) * c, 256)), dim3(256), 0, s,
+                           static_cast<const T*>(x), static_cast<T*>(y), n, hw, c);
+    }
+}
+
 hipError_t launch_avgpool(const void* x, void* y, int n, int hw, int c, int dtype, hipStream_t s) {
-    const int64_t total = static_cast<int64_t>(n) * c;
     if (dtype == MOPAR_BF16)
-        hipLaunchKernelGGL(avgpool_kernel<__bf16>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
-                           static_cast<const __bf16*>(x), static_cast<__bf16*>(y), n, hw, c);
+        avgpool_launch<__bf16>(x, y, n, hw, c, s);
     else
-        hipLaunchKernelGGL(avgpool_kernel<float>, dim3(blocks_for(total, 256)), dim3(256), 0, s,
-                           static_cast<const float*>(x), static_cast<float*>(y), n, hw, c);
+        avgpool_launch<float>(x, y, n, hw, c, s);
     return hipGetLastError();
 }
 

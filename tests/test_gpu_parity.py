@@ -152,6 +152,26 @@ def test_maxpool_and_avgpool(dt, k, st, pad):
     assert rel_err(_np(out), env[m.output_tid]) <= TOL[dt]
 
 
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_avgpool_ragged_channels(dt):
+    # channel counts that are not a whole number of 16-byte chunks take the per-channel path
+    b = synth._Builder("pool", dt, 2, 9)
+    x = b.tensor((3, 16, 9, 9), "f32")
+    b.new_layer("L0")
+    x = b.conv(x, 20, 3, 1, 1, "relu", "c", bn_fold=True)
+    y = b.avgpool(x, "a")
+    m = b.finish(y, 1)
+    xx = synth.random_tensor((3, 16, 9, 9), "f32", seed=5)
+    _, env, _, _ = oracle.forward(m, xx, keep=True)
+    sm = P.SlicedModel(m)
+    plan = P.make_plan(1, [0], [1])
+    ws = sm.alloc_workspace(plan)
+    out = sm.alloc_output()
+    sm.forward(plan, torch.from_numpy(xx).cuda(), out, None, None, ws)
+    torch.cuda.synchronize()
+    assert rel_err(_np(out), env[m.output_tid]) <= TOL[dt]
+
+
 def test_layernorm_with_residual():
     bld, x = seq_input_model("bf16", 3, 33, 768)
     r = bld.linear(x, 768, "none", "r", "rand")
