@@ -59,6 +59,93 @@ def numel(shape):
     return n
 
 
+GEMM_SRC = os.path.join(ROOT, "paper_2404_02445_amd", "csrc", "gemm.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_kernel_resnet50_b8_traffic.md")
+
+
+def gemm_source_hash():
+    import hashlib
+    with open(GEMM_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def read_counters(path):
+    """rocprofv3 --pmc csv -> {dispatch id: (kernel name, value)} for its one counter."""
+    import csv
+    out = {}
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            out[int(r["Dispatch_Id"])] = (r["Kernel_Name"], float(r["Counter_Value"]))
+    return out
+
+
+def summarize_pmc(fetch_csv, write_csv, copy_mib):
+    """Markdown summary of per-dispatch HBM-side traffic of gemm_kernel, scaled by the
+    counters of a raw copy of known size (copy_mib MiB read and written)."""
+    fetch, write = read_counters(fetch_csv), read_counters(write_csv)
+    def avg(rows, key):
+        v = [val for name, val in rows.values() if key in name]
+        return (sum(v) / len(v), len(v)) if v else (0.0, 0)
+    # calibration: the largest copy_kernel dispatch is the known-size copy
+    cf = max((val for name, val in fetch.values() if "copy_kernel" in name), default=0.0)
+    cw = max((val for name, val in write.values() if "copy_kernel" in name), default=0.0)
+    kib = copy_mib * 1024.0
+    sf, sw = (kib / cf if cf else float("nan")), (kib / cw if cw else float("nan"))
+    gf, n_f = avg(fetch, "gemm_kernel")
+    gw, n_w = avg(write, "gemm_kernel")
+    rf, n_r = avg(fetch, "splitk_reduce_kernel")
+    rw, _ = avg(write, "splitk_reduce_kernel")
+    traffic = (gf * sf + gw * sw) * 1024.0
+    lines = [
+        "# gemm_kernel HBM-side traffic, ResNet-50 bf16 batch 8 (sequential sliced forward)",
+        "",
+        "Counters: rocprofv3 `FETCH_SIZE` and `WRITE_SIZE` (KiB per dispatch), one pass each,",
+        f"scaled by the same counters read for a raw copy of {copy_mib} MiB in the same run.",
+        "",
+        "| quantity | value |",
+        "|---|---|",
+        f"| copy calibration: FETCH_SIZE / WRITE_SIZE of the {copy_mib} MiB copy (KiB) | {cf:.1f} / {cw:.1f} |",
+        f"| scale factors (read, write) | {sf:.4f} / {sw:.4f} |",
+        f"| gemm_kernel dispatches (fetch pass / write pass) | {n_f} / {n_w} |",
+        f"| gemm_kernel mean FETCH_SIZE / WRITE_SIZE per dispatch (KiB) | {gf:.1f} / {gw:.1f} |",
+        f"| splitk_reduce_kernel dispatches, mean FETCH / WRITE (KiB) | {n_r}, {rf:.1f} / {rw:.1f} |",
+        f"| traffic per gemm_kernel launch (scaled read + write, bytes) | {traffic:.0f} |",
+        "",
+        "```",
+        f"gemm_hip_sha256: {gemm_source_hash()}",
+        f"traffic_bytes_per_launch: {traffic:.0f}",
+        "```",
+    ]
+    return "\n".join(lines)
+
+
+def committed_traffic():
+    """Traffic per gemm_kernel launch from the committed counter summary, or None when the
+    summary is missing or the kernel source has changed since it was taken."""
+    try:
+        txt = open(TRAFFIC_FILE).read()
+    except OSError:
+        return None
+    kv = dict(l.split(": ", 1) for l in txt.splitlines() if l.startswith(("gemm_hip_sha256:", "traffic_bytes_per_launch:")))
+    if kv.get("gemm_hip_sha256") != gemm_source_hash():
+        return None
+    try:
+        return float(kv["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def op_bytes(m, op, es):
+    """Algorithmic bytes of a contraction op: weights + bias + inputs (incl. residual) + output, once each."""
+    T = m.tensors
+    b = sum(numel(T[t]["shape"]) for t in op["inputs"]) + numel(T[op["out"]]["shape"])
+    if op["kind"] == "conv":
+        b += op["cout"] * T[op["inputs"][0]]["shape"][1] * op["kh"] * op["kw"] + op["cout"]
+    elif op["kind"] == "linear":
+        b += op["nout"] * op["nin"] + op["nout"]
+    return b * es
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -77,7 +164,13 @@ def main():
     ap.add_argument("--stream-per-slice", type=int, default=0, help="1: one stream per slice, 0: one per instance")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run a raw boundary copy of this many MiB per step (counter calibration)")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="print the traffic summary from two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) "
+                         "of this script with --calibrate-copy-mib, and exit")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        print(summarize_pmc(*args.summarize_pmc, args.calibrate_copy_mib or 64))
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -210,12 +303,22 @@ def main():
         gemm_ms = rd_ms = 0.0
         gemm_fl = rd_fl = 0
         gemm_launches = 0
+        gemm_bytes = 0
+        es = 2 if m.dtype == "bf16" else 4
         enc_ms = [0.0] * len(cuts)
         dec_ms = [0.0] * len(cuts)
         bw_ms = 0.0
         bw_bytes = 0
-        es = 2 if m.dtype == "bf16" else 4
         per_op = [0.0] * len(m.ops)
+        # AE codec GEMMs (encode and decode of every cut) are gemm_kernel launches too
+        codec_fl, codec_bytes = [], []
+        for c, li in enumerate(cuts):
+            shp = m.tensors[m.layer_output_tid(li)]["shape"]
+            ch = synth.boundary_channels(m, li)
+            pos = numel(shp) // ch
+            ce = ch // ratios[c] if args.codec == "ae" else ch
+            codec_fl.append(2 * pos * ch * ce)
+            codec_bytes.append((pos * ch + pos * ce + ch * ce + ce) * es)
         for _ in range(n_t):
             step()
             ops_ms, cut_ms = sm.op_times()
@@ -227,6 +330,7 @@ def main():
                     f = op_flops(m, op)
                     gemm_ms += t
                     gemm_fl += f
+                    gemm_bytes += op_bytes(m, op, es)
                     gemm_launches += 1
                     if op.get("rd"):
                         rd_ms += t
@@ -238,6 +342,11 @@ def main():
             for c, (e, d) in enumerate(cut_ms):
                 enc_ms[c] += e
                 dec_ms[c] += d
+                if args.codec == "ae":
+                    gemm_ms += e + d
+                    gemm_fl += 2 * codec_fl[c]
+                    gemm_bytes += 2 * codec_bytes[c]
+                    gemm_launches += 2
         sm.set_timing(False)
         if args.op_report:
             for i, op in enumerate(m.ops):
@@ -265,11 +374,17 @@ def main():
         gemm_avg_ms = gemm_ms / max(gemm_launches, 1)
         achieved = gemm_fl / (gemm_ms * 1e-3) / 1e12
         peak = PEAK_TFLOPS[m.dtype]
+        traffic = committed_traffic() if m.name.startswith("resnet50") else None
         res["roofline"] = {
-            "bound": "mfma", "kernel": "gemm_kernel (all conv / linear launches of a step)",
+            "bound": "mfma",
+            "kernel": "gemm_kernel: every conv / linear op and AE codec GEMM of a step (device time of "
+                      "each launch from its own HIP event pair; an op's time also holds the stem's layout "
+                      "conversion and the split-K reduce of split ops)",
             "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
-            "frac": round(achieved / peak, 4), "traffic": None,
+            "frac": round(achieved / peak, 4),
+            "traffic": round(traffic) if traffic is not None else None,
             "flop_per_launch": round(gemm_fl / max(gemm_launches, 1)),
+            "algorithmic_bytes_per_launch": round(gemm_bytes / max(gemm_launches, 1)),
             "avg_launch_us": round(gemm_avg_ms * 1e3, 2),
             "launches_per_step": gemm_launches // n_t,
         }

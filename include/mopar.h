@@ -305,12 +305,15 @@ void mopar_pipeline_destroy(mopar_pipeline_t pipe);
 /* Measurement                                                               */
 /* ------------------------------------------------------------------------ */
 
-/* Per-op timing.  While enabled, every op of mopar_slice_forward /
- * mopar_model_forward (an LSTM op counts as one, all its launches included)
- * and every boundary encode / decode of mopar_model_forward is bracketed by
- * two HIP events recorded on the launch stream.  Enabling creates the
- * events (no device memory); disabling destroys them.  Not thread-safe
- * with respect to concurrent forwards on the same model. */
+/* Per-op timing.  While enabled, every kernel that an op of
+ * mopar_slice_forward / mopar_model_forward launches (an LSTM op counts as
+ * one op, all its launches included), and every kernel of a boundary encode /
+ * decode of mopar_model_forward, is launched with its own pair of HIP events
+ * that the runtime stamps with that kernel's start and end on the device.  A
+ * slot's time is the sum of its kernels' durations: launch gaps between
+ * kernels are not counted.  Events are created on first use and reused (no
+ * device memory); disabling destroys them.  Not thread-safe with respect to
+ * concurrent forwards on the same model. */
 int mopar_model_set_timing(mopar_model_t model, int32_t enable);
 
 /* Number of timing slots: n_ops + 2 * (n_layers - 1).  Slot i < n_ops is op

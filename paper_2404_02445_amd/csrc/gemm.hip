@@ -613,9 +613,9 @@ static hipError_t launch_cfg(const GemmParams& p, int width, hipStream_t st) {
     const int64_t grid = (total + 7) / 8 * 8;
     const dim3 block(WM * WN * 64);
     if (p.conv)
-        hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, NS, true>), dim3(static_cast<unsigned>(grid)), block, 0, st, p);
+        launch_kernel((gemm_kernel<T, BM, BN, WM, WN, NS, true>), dim3(static_cast<unsigned>(grid)), block, 0, st, p);
     else
-        hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, NS, false>), dim3(static_cast<unsigned>(grid)), block, 0, st, p);
+        launch_kernel((gemm_kernel<T, BM, BN, WM, WN, NS, false>), dim3(static_cast<unsigned>(grid)), block, 0, st, p);
     return hipGetLastError();
 }
 
@@ -659,9 +659,9 @@ hipError_t launch_gemm(const GemmParams& params, int dtype, hipStream_t stream) 
     const int64_t n = p.M * ((p.N + 3) / 4);
     const unsigned blocks = static_cast<unsigned>((n + 255) / 256);
     if (dtype == MOPAR_BF16)
-        hipLaunchKernelGGL(splitk_reduce_kernel<__bf16>, dim3(blocks), dim3(256), 0, stream, p);
+        launch_kernel(splitk_reduce_kernel<__bf16>, dim3(blocks), dim3(256), 0, stream, p);
     else
-        hipLaunchKernelGGL(splitk_reduce_kernel<float>, dim3(blocks), dim3(256), 0, stream, p);
+        launch_kernel(splitk_reduce_kernel<float>, dim3(blocks), dim3(256), 0, stream, p);
     return hipGetLastError();
 }
 

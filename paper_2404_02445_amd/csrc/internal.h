@@ -3,8 +3,10 @@
 
 #include <cstdint>
 #include <string>
+#include <utility>
 #include <vector>
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "../../include/mopar.h"
@@ -14,6 +16,43 @@ namespace mopar {
 // Thread-local error text; set_error returns the status for `return set_error(...)`.
 int set_error(int status, const std::string& msg);
 int hip_check(hipError_t e, const char* what);
+
+// ---------------------------------------------------------------------------
+// Kernel launches.  While a model measures op times, the calling thread has a
+// LaunchTimer: every kernel is then launched with its own start / stop event
+// pair, stamped by the runtime with that kernel's begin and end, so an op's time
+// is the sum of its kernels' durations (launch gaps excluded).
+// ---------------------------------------------------------------------------
+struct LaunchTimer {
+    std::vector<std::pair<hipEvent_t, hipEvent_t>>* pool;   // grows on demand, owned by the model
+    size_t* next;                                           // next unused pair
+    hipError_t err;                                         // first event-creation failure
+};
+extern thread_local LaunchTimer* t_timer;
+
+template <typename F, typename... Args>
+inline void launch_kernel(F kernel, dim3 grid, dim3 block, unsigned shmem, hipStream_t s, Args... args) {
+    LaunchTimer* t = t_timer;
+    if (t && t->err == hipSuccess) {
+        auto& pool = *t->pool;
+        if (*t->next == pool.size()) {
+            hipEvent_t a = nullptr, b = nullptr;
+            hipError_t e = hipEventCreate(&a);
+            if (e == hipSuccess) e = hipEventCreate(&b);
+            if (e != hipSuccess) {
+                if (a) (void)hipEventDestroy(a);
+                t->err = e;
+                hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
+                return;
+            }
+            pool.emplace_back(a, b);
+        }
+        const auto ev = pool[(*t->next)++];
+        hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, ev.first, ev.second, 0u, args...);
+        return;
+    }
+    hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
+}
 
 // ---------------------------------------------------------------------------
 // Kernel launch parameters

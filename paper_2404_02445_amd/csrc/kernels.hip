@@ -58,10 +58,10 @@ hipError_t launch_nchw_to_nhwc(const float* x, void* y, int n, int c, int h, int
     const int64_t pix = static_cast<int64_t>(n) * h * w;
     if (pix * cs >= (int64_t(1) << 31) || cs % (dtype == MOPAR_BF16 ? 8 : 4) != 0) return hipErrorInvalidValue;
     if (dtype == MOPAR_BF16)
-        hipLaunchKernelGGL(nchw_to_nhwc_kernel<__bf16>, dim3(blocks_for(pix, 256)), dim3(256), 0, s, x,
+        launch_kernel(nchw_to_nhwc_kernel<__bf16>, dim3(blocks_for(pix, 256)), dim3(256), 0, s, x,
                            static_cast<__bf16*>(y), n, c, h, w, cs);
     else
-        hipLaunchKernelGGL(nchw_to_nhwc_kernel<float>, dim3(blocks_for(pix, 256)), dim3(256), 0, s, x,
+        launch_kernel(nchw_to_nhwc_kernel<float>, dim3(blocks_for(pix, 256)), dim3(256), 0, s, x,
                            static_cast<float*>(y), n, c, h, w, cs);
     return hipGetLastError();
 }
@@ -112,13 +112,13 @@ static void maxpool_launch(const void* x, void* y, int n, int h, int w, int c, i
     const T* xp = static_cast<const T*>(x);
     T* yp = static_cast<T*>(y);
     if (k == 3)
-        hipLaunchKernelGGL((maxpool_kernel<T, 3>), dim3(blocks_for(total, 256)), dim3(256), 0, s, xp, yp, n, h, w, c, k,
+        launch_kernel((maxpool_kernel<T, 3>), dim3(blocks_for(total, 256)), dim3(256), 0, s, xp, yp, n, h, w, c, k,
                            stride, pad, ho, wo);
     else if (k == 2)
-        hipLaunchKernelGGL((maxpool_kernel<T, 2>), dim3(blocks_for(total, 256)), dim3(256), 0, s, xp, yp, n, h, w, c, k,
+        launch_kernel((maxpool_kernel<T, 2>), dim3(blocks_for(total, 256)), dim3(256), 0, s, xp, yp, n, h, w, c, k,
                            stride, pad, ho, wo);
     else
-        hipLaunchKernelGGL((maxpool_kernel<T, 0>), dim3(blocks_for(total, 256)), dim3(256), 0, s, xp, yp, n, h, w, c, k,
+        launch_kernel((maxpool_kernel<T, 0>), dim3(blocks_for(total, 256)), dim3(256), 0, s, xp, yp, n, h, w, c, k,
                            stride, pad, ho, wo);
 }
 
@@ -191,9 +191,9 @@ static void avgpool_launch(const void* x, void* y, int n, int hw, int c, hipStre
     constexpr int V = Vec<T>::N;
     if (c % V == 0) {
         const dim3 grid((c / V + AP_CHUNKS - 1) / AP_CHUNKS, n);
-        hipLaunchKernelGGL(avgpool_kernel<T>, grid, dim3(256), 0, s, static_cast<const T*>(x), static_cast<T*>(y), hw, c);
+        launch_kernel(avgpool_kernel<T>, grid, dim3(256), 0, s, static_cast<const T*>(x), static_cast<T*>(y), hw, c);
     } else {
-        hipLaunchKernelGGL(avgpool_channel_kernel<T>, dim3(blocks_for(static_cast<int64_t>(n) * c, 256)), dim3(256), 0, s,
+        launch_kernel(avgpool_channel_kernel<T>, dim3(blocks_for(static_cast<int64_t>(n) * c, 256)), dim3(256), 0, s,
                            static_cast<const T*>(x), static_cast<T*>(y), n, hw, c);
     }
 }
@@ -256,12 +256,12 @@ __global__ void layernorm_kernel(const T* __restrict__ x, const T* __restrict__ 
 hipError_t launch_layernorm(const void* x, const void* res, const void* g, const void* b, void* y, int64_t rows,
                             int f, float eps, int dtype, hipStream_t s) {
     if (dtype == MOPAR_BF16)
-        hipLaunchKernelGGL(layernorm_kernel<__bf16>, dim3(blocks_for(rows, 4)), dim3(256), 0, s,
+        launch_kernel(layernorm_kernel<__bf16>, dim3(blocks_for(rows, 4)), dim3(256), 0, s,
                            static_cast<const __bf16*>(x), static_cast<const __bf16*>(res),
                            static_cast<const __bf16*>(g), static_cast<const __bf16*>(b), static_cast<__bf16*>(y),
                            rows, f, eps);
     else
-        hipLaunchKernelGGL(layernorm_kernel<float>, dim3(blocks_for(rows, 4)), dim3(256), 0, s,
+        launch_kernel(layernorm_kernel<float>, dim3(blocks_for(rows, 4)), dim3(256), 0, s,
                            static_cast<const float*>(x), static_cast<const float*>(res),
                            static_cast<const float*>(g), static_cast<const float*>(b), static_cast<float*>(y), rows,
                            f, eps);
@@ -297,12 +297,12 @@ hipError_t launch_embed_bert(const int32_t* ids, const void* tok, const void* po
                              hipStream_t s) {
     const int64_t rows = static_cast<int64_t>(batch) * seq;
     if (dtype == MOPAR_BF16)
-        hipLaunchKernelGGL(embed_bert_kernel<__bf16>, dim3(blocks_for(rows, 4)), dim3(256), 0, s, ids,
+        launch_kernel(embed_bert_kernel<__bf16>, dim3(blocks_for(rows, 4)), dim3(256), 0, s, ids,
                            static_cast<const __bf16*>(tok), static_cast<const __bf16*>(pos),
                            static_cast<const __bf16*>(type), static_cast<const __bf16*>(g),
                            static_cast<const __bf16*>(b), static_cast<__bf16*>(y), rows, seq, f, eps);
     else
-        hipLaunchKernelGGL(embed_bert_kernel<float>, dim3(blocks_for(rows, 4)), dim3(256), 0, s, ids,
+        launch_kernel(embed_bert_kernel<float>, dim3(blocks_for(rows, 4)), dim3(256), 0, s, ids,
                            static_cast<const float*>(tok), static_cast<const float*>(pos),
                            static_cast<const float*>(type), static_cast<const float*>(g),
                            static_cast<const float*>(b), static_cast<float*>(y), rows, seq, f, eps);
@@ -324,7 +324,7 @@ __global__ void embed_kernel(const int32_t* __restrict__ ids, const uint4* __res
 hipError_t launch_embed(const int32_t* ids, const void* table, void* y, int64_t n, int f, int dtype,
                         hipStream_t s) {
     const int chunks = static_cast<int>(f * dtype_size(dtype) / 16);
-    hipLaunchKernelGGL(embed_kernel, dim3(blocks_for(n * chunks, 256)), dim3(256), 0, s, ids,
+    launch_kernel(embed_kernel, dim3(blocks_for(n * chunks, 256)), dim3(256), 0, s, ids,
                        static_cast<const uint4*>(table), static_cast<uint4*>(y), n, chunks);
     return hipGetLastError();
 }
@@ -384,10 +384,10 @@ __global__ __launch_bounds__(ATT_MAXS) void attention_kernel(const T* __restrict
 hipError_t launch_attention(const void* qkv, void* y, int batch, int seq, int heads, float scale, int dtype,
                             hipStream_t s) {
     if (dtype == MOPAR_BF16)
-        hipLaunchKernelGGL(attention_kernel<__bf16>, dim3(batch * heads), dim3(ATT_MAXS), 0, s,
+        launch_kernel(attention_kernel<__bf16>, dim3(batch * heads), dim3(ATT_MAXS), 0, s,
                            static_cast<const __bf16*>(qkv), static_cast<__bf16*>(y), seq, heads, scale);
     else
-        hipLaunchKernelGGL(attention_kernel<float>, dim3(batch * heads), dim3(ATT_MAXS), 0, s,
+        launch_kernel(attention_kernel<float>, dim3(batch * heads), dim3(ATT_MAXS), 0, s,
                            static_cast<const float*>(qkv), static_cast<float*>(y), seq, heads, scale);
     return hipGetLastError();
 }
@@ -424,11 +424,11 @@ static unsigned stream_blocks(int64_t n16) {
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s) {
     const int64_t n16 = static_cast<int64_t>(bytes / 16);
     if (n16 > 0)
-        hipLaunchKernelGGL(copy_kernel, dim3(stream_blocks(n16)), dim3(256), 0, s, static_cast<const uint4*>(src),
+        launch_kernel(copy_kernel, dim3(stream_blocks(n16)), dim3(256), 0, s, static_cast<const uint4*>(src),
                            static_cast<uint4*>(dst), n16);
     const int64_t tail = static_cast<int64_t>(bytes % 16);
     if (tail)
-        hipLaunchKernelGGL(copy_tail_kernel, dim3(1), dim3(16), 0, s,
+        launch_kernel(copy_tail_kernel, dim3(1), dim3(16), 0, s,
                            static_cast<const unsigned char*>(src) + n16 * 16,
                            static_cast<unsigned char*>(dst) + n16 * 16, tail);
     return hipGetLastError();
@@ -437,10 +437,10 @@ hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s) 
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
     const int64_t n16 = static_cast<int64_t>(bytes / 16);
     if (n16 > 0)
-        hipLaunchKernelGGL(fill_zero_kernel, dim3(stream_blocks(n16)), dim3(256), 0, s, static_cast<uint4*>(p), n16);
+        launch_kernel(fill_zero_kernel, dim3(stream_blocks(n16)), dim3(256), 0, s, static_cast<uint4*>(p), n16);
     const int64_t tail = static_cast<int64_t>(bytes % 16);
     if (tail)
-        hipLaunchKernelGGL(fill_zero_tail_kernel, dim3(1), dim3(16), 0, s,
+        launch_kernel(fill_zero_tail_kernel, dim3(1), dim3(16), 0, s,
                            static_cast<unsigned char*>(p) + n16 * 16, tail);
     return hipGetLastError();
 }

@@ -58,16 +58,27 @@ struct mopar_model_s {
     std::vector<int> layer_out;                 // tensor leaving each node
     std::vector<size_t> offset;                 // workspace offset per tensor (SIZE_MAX: not in ws)
     size_t ws_bytes;
-    // measurement: event pairs per timing slot (ops, then encode/decode per cut)
-    std::vector<hipEvent_t> ev_start, ev_stop;
-    std::vector<char> ev_used;
-    ~mopar_model_s() {
-        for (auto e : ev_start) (void)hipEventDestroy(e);
-        for (auto e : ev_stop) (void)hipEventDestroy(e);
+    // measurement (timing slots: ops, then encode / decode per cut): each kernel launched
+    // inside a slot gets an event pair from kev; a slot owns the pairs [slot_lo, slot_hi)
+    bool timing = false;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> kev;
+    size_t kev_next = 0;
+    std::vector<size_t> slot_lo, slot_hi;
+    void free_events() {
+        for (auto& e : kev) {
+            (void)hipEventDestroy(e.first);
+            (void)hipEventDestroy(e.second);
+        }
+        kev.clear();
+        kev_next = 0;
     }
+    ~mopar_model_s() { free_events(); }
 };
 
 namespace mopar {
+
+thread_local LaunchTimer* t_timer = nullptr;
+
 namespace {
 
 
@@ -632,23 +643,22 @@ static hipError_t run_op(const mopar_model_s& m, int i, const Ptrs& P, int ksub,
 template <typename F>
 static hipError_t timed(const mopar_model_s& mc, int slot, hipStream_t s, F&& fn) {
     auto& m = const_cast<mopar_model_s&>(mc);
-    const bool on = !m.ev_start.empty() && slot >= 0 && slot < static_cast<int>(m.ev_start.size());
-    if (on) {
-        const hipError_t e = hipEventRecord(m.ev_start[slot], s);
-        if (e != hipSuccess) return e;
-    }
+    (void)s;
+    if (!m.timing || slot < 0 || slot >= static_cast<int>(m.slot_lo.size())) return fn();
+    LaunchTimer timer{&m.kev, &m.kev_next, hipSuccess};
+    m.slot_lo[slot] = m.kev_next;
+    t_timer = &timer;
     const hipError_t e = fn();
-    if (e != hipSuccess) return e;
-    if (on) {
-        m.ev_used[slot] = 1;
-        return hipEventRecord(m.ev_stop[slot], s);
-    }
-    return hipSuccess;
+    t_timer = nullptr;
+    m.slot_hi[slot] = m.kev_next;
+    return e != hipSuccess ? e : timer.err;
 }
 
 static void reset_timing(const mopar_model_s& mc) {
     auto& m = const_cast<mopar_model_s&>(mc);
-    std::fill(m.ev_used.begin(), m.ev_used.end(), 0);
+    m.kev_next = 0;
+    std::fill(m.slot_lo.begin(), m.slot_lo.end(), 0);
+    std::fill(m.slot_hi.begin(), m.slot_hi.end(), 0);
 }
 
 static int run_layers(const mopar_model_s& m, const mopar_plan& p, int l0, int l1, const Ptrs& P, hipStream_t s) {
@@ -663,26 +673,11 @@ static int run_layers(const mopar_model_s& m, const mopar_plan& p, int l0, int l
 
 int set_timing_impl(mopar_model_s* m, int32_t enable) {
     if (!m) return set_error(MOPAR_E_ARG, "mopar_model_set_timing: null model");
-    for (auto e : m->ev_start) (void)hipEventDestroy(e);
-    for (auto e : m->ev_stop) (void)hipEventDestroy(e);
-    m->ev_start.clear();
-    m->ev_stop.clear();
-    m->ev_used.clear();
-    if (!enable) return MOPAR_OK;
+    m->free_events();
     const size_t n = m->ops.size() + 2 * static_cast<size_t>(m->n_layers - 1);
-    for (size_t i = 0; i < n; ++i) {
-        hipEvent_t a, b;
-        int rc = hip_check(hipEventCreate(&a), "hipEventCreate");
-        if (rc) return rc;
-        rc = hip_check(hipEventCreate(&b), "hipEventCreate");
-        if (rc) {
-            (void)hipEventDestroy(a);
-            return rc;
-        }
-        m->ev_start.push_back(a);
-        m->ev_stop.push_back(b);
-    }
-    m->ev_used.assign(n, 0);
+    m->timing = enable != 0;
+    m->slot_lo.assign(enable ? n : 0, 0);
+    m->slot_hi.assign(enable ? n : 0, 0);
     return MOPAR_OK;
 }
 
@@ -694,14 +689,20 @@ int timing_slots_impl(const mopar_model_s* m, int32_t* n) {
 
 int op_times_impl(const mopar_model_s* m, float* ms, int32_t n) {
     if (!m || !ms) return set_error(MOPAR_E_ARG, "mopar_model_op_times: null argument");
-    if (m->ev_start.empty()) return set_error(MOPAR_E_ARG, "mopar_model_op_times: timing is not enabled");
+    if (!m->timing) return set_error(MOPAR_E_ARG, "mopar_model_op_times: timing is not enabled");
     for (int32_t i = 0; i < n; ++i) {
         ms[i] = -1.0f;
-        if (i >= static_cast<int32_t>(m->ev_start.size()) || !m->ev_used[i]) continue;
-        int rc = hip_check(hipEventSynchronize(m->ev_stop[i]), "hipEventSynchronize");
-        if (rc) return rc;
-        rc = hip_check(hipEventElapsedTime(&ms[i], m->ev_start[i], m->ev_stop[i]), "hipEventElapsedTime");
-        if (rc) return rc;
+        if (i >= static_cast<int32_t>(m->slot_lo.size()) || m->slot_hi[i] <= m->slot_lo[i]) continue;
+        float sum = 0.0f;
+        for (size_t k = m->slot_lo[i]; k < m->slot_hi[i]; ++k) {
+            int rc = hip_check(hipEventSynchronize(m->kev[k].second), "hipEventSynchronize");
+            if (rc) return rc;
+            float t = 0.0f;
+            rc = hip_check(hipEventElapsedTime(&t, m->kev[k].first, m->kev[k].second), "hipEventElapsedTime");
+            if (rc) return rc;
+            sum += t;
+        }
+        ms[i] = sum;
     }
     return MOPAR_OK;
 }
