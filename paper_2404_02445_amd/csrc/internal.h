@@ -95,7 +95,7 @@ struct GemmParams {
     int64_t M;
     int N, K;
     int act;
-    int ksub;               // number of sub-slices (gridDim.z)
+    int ksub;               // number of sub-slices (decoded from the block index)
     const void* bias2;      // optional second bias [N]
     int out_f32;            // store C as float32 instead of the model dtype
     int epi;                // EPI_STD or EPI_LSTM
