@@ -41,14 +41,14 @@ def op_flops(m, op):
 
 
 def codec_ratios(m, cuts):
-    """Compression ratio per cut: R = 8 where the code width stays a multiple of the 16-byte
-    granule (8 bf16 / 4 fp32 channels), else 4."""
+    """Compression ratio per cut: the largest R in 8, 4, 2, 1 that divides the boundary's
+    channel count C and leaves C / R a multiple of the 16-byte granule (8 bf16 / 4 fp32)."""
     import synth
     g = 8 if m.dtype == "bf16" else 4
     out = []
     for li in cuts:
         c = synth.boundary_channels(m, li)
-        out.append(8 if (c % 8 == 0 and (c // 8) % g == 0) else 4)
+        out.append(next((r for r in (8, 4, 2) if c % r == 0 and (c // r) % g == 0), 1))
     return out
 
 
@@ -164,6 +164,10 @@ def main():
     ap.add_argument("--stream-per-slice", type=int, default=0, help="1: one stream per slice, 0: one per instance")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run a raw boundary copy of this many MiB per step (counter calibration)")
+    ap.add_argument("--plan", choices=["config", "measured"], default="config",
+                    help="config: the workload's prescribed cuts and k; measured: Alg. 1 free mode with the "
+                         "parallelism search over t_p(l, k) measured on this GPU")
+    ap.add_argument("--k-max", type=int, default=4, help="largest sub-slice count of the measured search")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="print the traffic summary from two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) "
                          "of this script with --calibrate-copy-mib, and exit")
@@ -192,7 +196,19 @@ def main():
     s = m.slicing
     plan_kw = dict(n_slices=s["n_slices"], allowed_cut=s["allowed_cut"], elim_tau=s["elim_tau"],
                    k_override=s["k_override"])
-    plan = sm.plan()
+    x = torch.from_numpy(x_host).to(dev)
+    # measured-profile planning (Alg. 1 + Eq. 5 over t_p measured here), reported in every run
+    mplan, tp, mprof = sm.measured_plan(x, k_max=args.k_max, reps=3)
+    measured = {"k_max": args.k_max, "n_slices": mplan.n_slices, "slice_end": mplan.slice_end,
+                "k": mplan.k, "t_tau_ms": round(mplan.t_tau * 1e3, 4),
+                "tp_ms_by_k": [round(sum(r[e] for r in tp) * 1e3, 4) for e in range(args.k_max)]}
+    if args.plan == "measured":
+        plan = mplan
+        prof_fixed = mprof
+        plan_kw = dict(elim_tau=0.05, k_max=args.k_max, tp_table=tp, ta_table=[[0.0] * args.k_max for _ in tp])
+    else:
+        plan = sm.plan()
+        prof_fixed = None
     cuts = plan.slice_end[:-1]
     ratios = codec_ratios(m, cuts)
     cw = synth.make_codec_weights(m, cuts, ratio=ratios) if args.codec == "ae" else None
@@ -200,7 +216,6 @@ def main():
     codes = sm.alloc_codes(plan, codecs)
     ws = sm.alloc_workspace(plan)
     out = sm.alloc_output()
-    x = torch.from_numpy(x_host).to(dev)
     stream = torch.cuda.current_stream()
     calib = None
     if args.calibrate_copy_mib:
@@ -208,7 +223,7 @@ def main():
         calib = (torch.empty(nb, dtype=torch.uint8, device=dev), torch.empty(nb, dtype=torch.uint8, device=dev))
 
     def step():
-        prof = sm.profile()                                   # a1-a2: layer profiles (Eq. 1-4)
+        prof = prof_fixed or sm.profile()                     # a1-a2: layer profiles (Eq. 1-4)
         pl = P.mopar_plan_slices(prof, **plan_kw)             # a3-a4: HyPAD plan and sub-slice counts
         sm.forward(pl, x, out, codecs, codes, ws)             # a5-a10: sliced forward with codec hand-off
         return pl
@@ -236,7 +251,7 @@ def main():
                            stream_per_slice=bool(args.stream_per_slice))
 
         def pstep():
-            prof = sm.profile()
+            prof = prof_fixed or sm.profile()
             pl = P.mopar_plan_slices(prof, **plan_kw)
             pipe.submit(x, out)
             return pl
@@ -266,7 +281,7 @@ def main():
     # planning cost on the host (already inside the steps above, overlapped with the GPU)
     tp0 = time.perf_counter()
     for _ in range(20):
-        P.mopar_plan_slices(sm.profile(), **plan_kw)
+        P.mopar_plan_slices(prof_fixed or sm.profile(), **plan_kw)
     plan_us = (time.perf_counter() - tp0) / 20 * 1e6
 
     res = {
@@ -294,6 +309,8 @@ def main():
         "wall_s_timed_region": round(wall, 4),
         "sequential_value": round(seq_value, 2),
         "host_plan_us": round(plan_us, 1),
+        "plan": args.plan,
+        "measured_plan": measured,
     }
 
     # --- per-op timing pass (HIP events on the launch stream, same steps) ----------------

@@ -325,6 +325,23 @@ int mopar_model_timing_slots(mopar_model_t model, int32_t* n);
  * duration in milliseconds to ms[0..n-1] (-1 for slots that did not run). */
 int mopar_model_op_times(mopar_model_t model, float* ms, int32_t n);
 
+/* Measured layer profile for the parallelism search of Alg. 1 (the t_p(l, eta)
+ * of Eq. 5, Sec. III-C).  For eta = 1 .. k_max the whole model runs as one
+ * slice with min(eta, RD width) sub-slices on every node that has an RD op
+ * (1 elsewhere): one warm-up pass, then `reps` timed passes with per-kernel
+ * device timing (as mopar_model_set_timing).  tp_out[l * k_max + eta - 1]
+ * receives the median over the passes of node l's summed kernel time, in
+ * seconds.  Sub-slices write their own output columns of the shared tensor,
+ * so the matching aggregation table t_a is zero.  Feed tp_out (and
+ * tp_out[l * k_max] as each node's time_s) to mopar_plan_slices.
+ *   in_dev / out_dev: model input and output (device; out is overwritten);
+ *   ws: workspace of at least mopar_model_workspace_bytes bytes;
+ *   k_max 1..64, reps 1..1000.
+ * Runs on `stream` and returns once its events have completed (synchronous
+ * for the host).  Per-op timing is left as it was before the call. */
+int mopar_model_measure(mopar_model_t model, int32_t k_max, int32_t reps, const void* in_dev, void* out_dev,
+                        void* ws, size_t ws_bytes, void* stream, double* tp_out);
+
 /* Description of the last error on this thread ("" when none). */
 const char* mopar_last_error(void);
 

@@ -368,6 +368,28 @@ class SlicedModel:
         cuts = [(arr[nops + 2 * c], arr[nops + 2 * c + 1]) for c in range((n.value - nops) // 2)]
         return ops, [c for c in cuts if c[0] >= 0 or c[1] >= 0]
 
+    def measure(self, x, k_max=4, reps=3, ws=None, out=None, stream=None):
+        """mopar_model_measure: t_p(l, eta) in seconds, a list of n_layers rows of k_max values."""
+        n = self.n_layers
+        if ws is None:
+            ws = self.alloc_workspace(make_plan(n, [n - 1], [1] * n))
+        if out is None:
+            out = self.alloc_output()
+        tab = (L.c_f64 * (n * k_max))()
+        check(lib().mopar_model_measure(self.handle, k_max, reps, _ptr(x), _ptr(out), _ptr(ws), ws.numel(),
+                                        _stream_ptr(stream), tab))
+        return [list(tab[l * k_max:(l + 1) * k_max]) for l in range(n)]
+
+    def measured_plan(self, x, k_max=4, reps=3, **opts):
+        """Plan from the measured profile: each node's time t_l := t_p(l, 1) measured, the
+        parallelism search over t_p(l, eta) (t_a = 0).  Returns (plan, t_p table)."""
+        tp = self.measure(x, k_max=k_max, reps=reps)
+        prof = [(mem, tp[l][0], ob, rdw) for l, (mem, _, ob, rdw) in enumerate(self.profile())]
+        kw = dict(elim_tau=0.05)
+        kw.update(opts)
+        plan = mopar_plan_slices(prof, k_max=k_max, tp_table=tp, ta_table=[[0.0] * k_max for _ in tp], **kw)
+        return plan, tp, prof
+
     def slice_forward(self, plan, s, x, out, ws, stream=None):
         check(lib().mopar_slice_forward(self.handle, ctypes.byref(plan.raw), s, _ptr(x), _ptr(out), _ptr(ws),
                                         ws.numel(), _stream_ptr(stream)))

@@ -28,6 +28,7 @@ void pipeline_destroy_impl(mopar_pipeline_s*);
 int set_timing_impl(mopar_model_s*, int32_t);
 int timing_slots_impl(const mopar_model_s*, int32_t*);
 int op_times_impl(const mopar_model_s*, float*, int32_t);
+int measure_impl(mopar_model_s*, int32_t, int32_t, const void*, void*, void*, size_t, void*, double*);
 
 static thread_local std::string g_error;
 
@@ -138,6 +139,12 @@ int mopar_model_timing_slots(mopar_model_t model, int32_t* n) {
 
 int mopar_model_op_times(mopar_model_t model, float* ms, int32_t n) {
     return guarded("mopar_model_op_times", [&] { return op_times_impl(model, ms, n); });
+}
+
+int mopar_model_measure(mopar_model_t model, int32_t k_max, int32_t reps, const void* in_dev, void* out_dev,
+                        void* ws, size_t ws_bytes, void* stream, double* tp_out) {
+    return guarded("mopar_model_measure",
+                   [&] { return measure_impl(model, k_max, reps, in_dev, out_dev, ws, ws_bytes, stream, tp_out); });
 }
 
 const char* mopar_last_error(void) { return g_error.c_str(); }

@@ -722,6 +722,58 @@ int slice_forward_impl(const mopar_model_s* m, const mopar_plan* p, int32_t s, c
 }
 
 // ---------------------------------------------------------------------------
+// Measured layer profile: t_p(l, eta) for the parallelism search
+// ---------------------------------------------------------------------------
+
+int measure_impl(mopar_model_s* m, int32_t k_max, int32_t reps, const void* in, void* out, void* ws,
+                 size_t ws_bytes, void* stream, double* tp) {
+    if (!m || !in || !out || !tp) return set_error(MOPAR_E_ARG, "mopar_model_measure: null argument");
+    if (k_max < 1 || k_max > 64 || reps < 1 || reps > 1000)
+        return set_error(MOPAR_E_ARG, "mopar_model_measure: k_max must be 1..64 and reps 1..1000");
+    if (m->ws_bytes && (!ws || ws_bytes < m->ws_bytes))
+        return set_error(MOPAR_E_WORKSPACE, "mopar_model_measure: workspace smaller than mopar_model_workspace_bytes");
+    const int n = m->n_layers;
+    std::vector<int> minw(n, 0);                 // narrowest RD op of each node (0: none)
+    for (int l = 0; l < n; ++l)
+        for (int i = m->layer_first[l]; i <= m->layer_last[l]; ++i)
+            if (m->ops[i].rd) minw[l] = minw[l] == 0 ? m->ops[i].n_out : std::min(minw[l], m->ops[i].n_out);
+    const bool was_timing = m->timing;
+    int rc = set_timing_impl(m, 1);
+    if (rc) return rc;
+    std::vector<int32_t> end{n - 1}, k(n, 1);
+    mopar_plan plan{};
+    plan.n_layers = n;
+    plan.n_slices = 1;
+    plan.slice_end = end.data();
+    plan.k = k.data();
+    const size_t nslot = m->ops.size() + 2 * static_cast<size_t>(n - 1);
+    std::vector<float> ms(nslot);
+    std::vector<std::vector<double>> samples(n);
+    for (int eta = 1; eta <= k_max && !rc; ++eta) {
+        for (int l = 0; l < n; ++l) k[l] = minw[l] ? std::min(eta, minw[l]) : 1;
+        for (auto& v : samples) v.clear();
+        for (int r = -1; r < reps && !rc; ++r) {   // r = -1: warm-up
+            rc = slice_forward_impl(m, &plan, 0, in, out, ws, ws_bytes, stream);
+            if (!rc) rc = op_times_impl(m, ms.data(), static_cast<int32_t>(nslot));
+            if (rc || r < 0) continue;
+            for (int l = 0; l < n; ++l) {
+                double t = 0.0;
+                for (int i = m->layer_first[l]; i <= m->layer_last[l]; ++i) t += ms[i] > 0.0f ? ms[i] : 0.0f;
+                samples[l].push_back(t * 1e-3);
+            }
+        }
+        if (rc) break;
+        for (int l = 0; l < n; ++l) {
+            auto v = samples[l];
+            std::sort(v.begin(), v.end());
+            tp[static_cast<size_t>(l) * k_max + eta - 1] = v[v.size() / 2];   // median (upper)
+        }
+    }
+    const int rc2 = set_timing_impl(m, was_timing ? 1 : 0);
+    return rc ? rc : rc2;
+}
+
+// ---------------------------------------------------------------------------
 // Boundary codec
 // ---------------------------------------------------------------------------
 

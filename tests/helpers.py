@@ -28,10 +28,11 @@ TOL = {"f32": 1e-4, "bf16": 2e-2}
 
 
 def codec_ratios(model, cuts):
-    """Ratio 8 where the code width stays a multiple of the 16-byte granule, else 4."""
+    """Compression ratio per cut: the largest R in 8, 4, 2, 1 that divides the boundary's
+    channel count C and leaves C / R a multiple of the 16-byte granule (8 bf16 / 4 fp32)."""
     g = 8 if model.dtype == "bf16" else 4
     out = []
     for li in cuts:
         c = synth.boundary_channels(model, li)
-        out.append(8 if (c % 8 == 0 and (c // 8) % g == 0) else 4)
+        out.append(next((r for r in (8, 4, 2) if c % r == 0 and (c // r) % g == 0), 1))
     return out

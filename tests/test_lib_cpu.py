@@ -189,3 +189,16 @@ def test_pipeline_workspace_and_validation_host_only():
     st = P.lib().mopar_pipeline_create(sm.handle, ctypes.byref(pl.raw), None, 3, 2, streams, None, 0, None,
                                        ctypes.byref(h))
     assert st == L.MOPAR_E_WORKSPACE
+
+
+def test_measure_argument_checks_host_only():
+    m = synth.build(1)
+    sm = P.SlicedModel(m, device="cpu")
+    tab = (ctypes.c_double * (len(m.layers) * 4))()
+    dummy = ctypes.c_void_p(16)           # never dereferenced: the checks come first
+    for k_max, reps, src in [(0, 1, dummy), (65, 1, dummy), (4, 0, dummy), (4, 1, None)]:
+        st = P.lib().mopar_model_measure(sm.handle, k_max, reps, src, dummy, dummy, 1 << 30, None, tab)
+        assert st == L.MOPAR_E_ARG
+    st = P.lib().mopar_model_measure(sm.handle, 4, 1, dummy, dummy, None, 0, None, tab)
+    assert st == L.MOPAR_E_WORKSPACE or sm.workspace_bytes(P.make_plan(len(m.layers), [len(m.layers) - 1],
+                                                                        [1] * len(m.layers))) == 0
