@@ -268,6 +268,7 @@ def main():
         t0 = time.perf_counter()
         for _ in range(args.steps):
             pstep()
+        t_host = time.perf_counter() - t0
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
         total_ms = wall * 1e3
@@ -277,6 +278,7 @@ def main():
     value = m.batch * args.steps / (total_ms / 1e3)
     if pipe is None:
         seq_value = value
+        t_host = None
 
     # planning cost on the host (already inside the steps above, overlapped with the GPU)
     tp0 = time.perf_counter()
@@ -309,6 +311,7 @@ def main():
         "wall_s_timed_region": round(wall, 4),
         "sequential_value": round(seq_value, 2),
         "host_plan_us": round(plan_us, 1),
+        "host_submit_ms_per_step": round(t_host / args.steps * 1e3, 4) if t_host is not None else None,
         "plan": args.plan,
         "measured_plan": measured,
     }
@@ -409,9 +412,70 @@ def main():
                                "frac_of_peak": round(rd_fl / (rd_ms * 1e-3) / 1e12 / peak, 4) if rd_ms else None,
                                "rd_ms_per_step": round(rd_ms / n_t, 4)}
         res["codec"] = codec
+        # ideal step time: every op (and codec GEMM) at its own roofline, max(FLOP / P, bytes / B)
+        B = PEAK_HBM_GBS * 1e9
+        ideal_s = 0.0
+        rd_ideal_s = 0.0
+        for op in m.ops:
+            f = op_flops(m, op)
+            if op["kind"] in ("conv", "linear"):
+                by = op_bytes(m, op, es)
+            else:
+                by = (sum(numel(m.tensors[t]["shape"]) for t in op["inputs"]) + numel(m.tensors[op["out"]]["shape"])) * es
+            t_op = max(f / (peak * 1e12), by / B)
+            ideal_s += t_op
+            if op.get("rd"):
+                rd_ideal_s += f / min(peak * 1e12, f / by * B)
+        if args.codec == "ae":
+            for c in range(len(cuts)):
+                ideal_s += 2 * max(codec_fl[c] / (peak * 1e12), codec_bytes[c] / B)
+        res["ideal_step"] = {"ms": round(ideal_s * 1e3, 4),
+                             "frac_of_sequential_p50": round(ideal_s * 1e3 / res["latency_ms"]["p50"], 4)}
+        if rd_ms:
+            res["rd_mfma_util"]["attainable_frac"] = round(rd_ideal_s * 1e3 / (rd_ms / n_t), 4)
         res["bandwidth_ops"] = {"ms_per_step": round(bw_ms / n_t, 4),
                                 "GBs": round(bw_bytes / (bw_ms * 1e-3) / 1e9, 1) if bw_ms else None}
         res["gemm_ms_per_step"] = round(gemm_ms / n_t, 4)
+
+    # --- boundary codec in isolation, cold cache (a 512 MB write between runs evicts the
+    #     256 MB Infinity Cache), against a raw copy of the same tensor ------------------
+    if args.codec == "ae" and not args.no_op_timing:
+        scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+        raw = P.make_codec("raw")
+        iso = []
+        for c, li in enumerate(cuts):
+            shp = list(m.tensors[m.layer_output_tid(li)]["shape"])
+            gshape = [shp[0]] + shp[2:] + [shp[1]] if len(shp) == 4 else shp      # NHWC on the device
+            tdt = torch.bfloat16 if m.dtype == "bf16" else torch.float32
+            xt = torch.randn(gshape, device=dev).to(tdt)
+            yt = torch.empty_like(xt)
+            code = torch.empty(P.mopar_boundary_code_bytes(codecs[c], shp, m.dtype), dtype=torch.uint8, device=dev)
+            rawbuf = torch.empty_like(xt)
+
+            def cold(fn, reps=5):
+                ts = []
+                for _ in range(reps):
+                    scratch.fill_(1)
+                    a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    a0.record(stream)
+                    fn()
+                    a1.record(stream)
+                    torch.cuda.synchronize()
+                    ts.append(a0.elapsed_time(a1))
+                return statistics.median(ts)
+            t_enc = cold(lambda: P.mopar_boundary_encode(codecs[c], shp, m.dtype, xt, code))
+            t_dec = cold(lambda: P.mopar_boundary_decode(codecs[c], shp, m.dtype, code, yt))
+            t_raw = cold(lambda: P.mopar_boundary_encode(raw, shp, m.dtype, xt, rawbuf))
+            tb = numel(shp) * es
+            e_gbs = (tb + code.numel()) / (t_enc * 1e-3) / 1e9
+            d_gbs = (tb + code.numel()) / (t_dec * 1e-3) / 1e9
+            r_gbs = 2 * tb / (t_raw * 1e-3) / 1e9
+            iso.append({"cut_after": m.layers[li], "encode_GBs": round(e_gbs, 1), "decode_GBs": round(d_gbs, 1),
+                        "raw_copy_GBs": round(r_gbs, 1), "encode_frac_of_8TBs": round(e_gbs / PEAK_HBM_GBS, 3),
+                        "decode_frac_of_8TBs": round(d_gbs / PEAK_HBM_GBS, 3),
+                        "encode_frac_of_raw": round(e_gbs / r_gbs, 3), "decode_frac_of_raw": round(d_gbs / r_gbs, 3)})
+        res["codec_isolated_cold"] = iso
+        del scratch
 
     if calib is not None:   # known-size raw copies: the reference for HBM counter scaling
         raw = P.make_codec("raw")
@@ -434,7 +498,13 @@ def main():
             if time.perf_counter() - t0 >= args.cpu_seconds:
                 break
         el = time.perf_counter() - t0
+        cpu_model = ""
+        try:
+            cpu_model = next(l.split(":", 1)[1].strip() for l in open("/proc/cpuinfo") if l.startswith("model name"))
+        except (OSError, StopIteration):
+            pass
         res["cpu_baseline"] = {"value": round(done / el, 4), "unit": "inferences/s", "cores": cores,
+                               "nproc": len(os.sched_getaffinity(0)), "cpu_model": cpu_model,
                                "kind": "oracle",
                                "sample": f"{done} single-image forward(s) of the same sliced workload "
                                          f"(same plan, codecs and weights), {el:.1f} s"}
