@@ -95,6 +95,11 @@ typedef struct {
     const double* tp_table;     /* [n][k_max] measured t_p(l, eta); NULL: t_p = t_l               */
     const double* ta_table;     /* [n][k_max] measured t_a(l, eta); NULL: 0                       */
     const int32_t* k_override;  /* n entries; > 0 forces k for that node; NULL: none              */
+    int32_t uniform;            /* 1: the Uniform partitioning of the evaluation (Sec. IV): exactly
+                                   n_slices (> 0) slices with equal node counts (the first
+                                   n mod n_slices one node longer); allowed_cut and elimination do
+                                   not apply; the parallelism search, cost and latency as usual   */
+    int32_t reserved;
 } mopar_plan_opts;
 
 /* A plan.  slice_end and k are caller-allocated arrays of n entries. */
@@ -197,6 +202,14 @@ void mopar_model_destroy(mopar_model_t model);
  * (bf16) or 157.3e12 (f32) FLOP/s; FLOP counted for conv, linear, attention
  * and LSTM.  `out` has n_layers entries. */
 int mopar_model_profile(mopar_model_t model, mopar_layer_profile* out);
+
+/* The same profile built from each node's dominant operators only (Sec.
+ * III-B): the node's ops sorted by memory footprint, largest first (ties by
+ * position), and the shortest such prefix whose footprint reaches `frac`
+ * (the paper: 0.8) of the node's total, the total summed in op order and the
+ * prefix in sorted order.  Eq. 1-3 then aggregate the selected ops; out_bytes
+ * and rd_width are those of the whole node.  frac must be in (0, 1]. */
+int mopar_model_profile_dominant(mopar_model_t model, double frac, mopar_layer_profile* out);
 
 /* Bytes of device workspace mopar_slice_forward / mopar_model_forward need
  * under `plan` (activations inside slices, boundary tensors, scratch). */

@@ -93,7 +93,26 @@ class LayerProfile:
     rd_width: int
 
 
-def layer_profiles(model):
+def dominant_ops(mems, frac):
+    """Dominant operators of a layer (Sec. III-B): the ops sorted by memory footprint,
+    largest first (reading of 'ascending ... top n': the top n by size), ties by
+    position, and the shortest such prefix whose footprint reaches frac of the
+    layer's total (the total summed in op order, the prefix in sorted order).
+    Returns the selected indices in op order."""
+    total = 0.0
+    for m in mems:
+        total = total + m
+    order = sorted(range(len(mems)), key=lambda i: (-mems[i], i))
+    acc, chosen = 0.0, []
+    for i in order:
+        acc = acc + mems[i]
+        chosen.append(i)
+        if acc >= frac * total:
+            break
+    return sorted(chosen)
+
+
+def layer_profiles(model, dominant=None):
     """Layer profiles M_l, t_l (Eq. 1-3) and the service profile vectors (Eq. 4).
 
     Ops with branch 0 form the sequential chain (Eq. 1): M_c = max m_i,
@@ -103,10 +122,16 @@ def layer_profiles(model):
     Sums run in op order (chain), branch order (per position) and position
     order (over positions).  rd_width is the smallest output width among the
     layer's resource-dominant ops (0 when it has none).
+    With ``dominant`` = f (0.8 in the paper), only the layer's dominant operators
+    (dominant_ops) enter the aggregation; rd_width and out_bytes are unchanged.
     """
     out = []
     for li in range(len(model.layers)):
-        ops = [o for o in model.ops if o["layer"] == li]
+        all_ops = [o for o in model.ops if o["layer"] == li]
+        ops = all_ops
+        if dominant is not None:
+            keep = dominant_ops([op_profile(model, o)[0] for o in all_ops], dominant)
+            ops = [all_ops[i] for i in keep]
         mc, tc = 0.0, 0.0
         pos_m, pos_t = {}, {}
         for o in ops:
@@ -126,9 +151,9 @@ def layer_profiles(model):
         tb = 0.0
         for p in sorted(pos_t):
             tb = tb + pos_t[p]
-        T = model.tensors[ops[-1]["out"]]
+        T = model.tensors[all_ops[-1]["out"]]
         ob = float(_numel(T["shape"]) * DTYPE_BYTES[T["dtype"]])
-        widths = [o["cout"] if o["kind"] == "conv" else o["nout"] for o in ops if o.get("rd")]
+        widths = [o["cout"] if o["kind"] == "conv" else o["nout"] for o in all_ops if o.get("rd")]
         out.append(LayerProfile(max(mc, mb), tc + tb, ob, min(widths) if widths else 0))
     return out
 
@@ -151,6 +176,7 @@ class PlanOpts:
     tp_table: list | None = None        # [n][k_max] measured t_p(l, eta); None: analytic
     ta_table: list | None = None        # [n][k_max] measured t_a(l, eta); None: 0
     k_override: list | None = None      # per node, > 0 forces k
+    uniform: bool = False               # the Uniform variant: n_slices slices of equal node counts
 
 
 @dataclass
@@ -241,7 +267,21 @@ def plan_slices(prof, opts: PlanOpts) -> Plan:
     K = opts.n_slices
     if K < 0 or K > n:
         raise Infeasible("n_slices out of range")
-    if K == 0:
+    if opts.uniform:
+        # the Uniform partitioning of the evaluation (Sec. IV): the same number of
+        # slices, each with the same number of nodes -- node counts as array_split
+        # gives them (the first n mod K slices one node longer); no elimination
+        if K == 0:
+            raise ValueError("the uniform variant needs n_slices > 0")
+        q, r = divmod(n, K)
+        ends, e = [], -1
+        for s_ in range(K):
+            e += q + (1 if s_ < r else 0)
+            ends.append(e)
+        cost = plan_cost(prof, opts, ends)
+        allowed = [1] * (n - 1)
+        ends.reverse()
+    elif K == 0:
         dp = [INF] * (n + 1)
         arg = [0] * (n + 1)
         dp[0] = 0.0

@@ -34,7 +34,8 @@ class PlanOpts(ctypes.Structure):
     _fields_ = [("n_slices", c_i32), ("k_max", c_i32), ("allowed_cut", ctypes.POINTER(ctypes.c_uint8)),
                 ("elim_tau", c_f64), ("c_m", c_f64), ("c_n", c_f64), ("bw_Bps", c_f64),
                 ("ratio", ctypes.POINTER(c_f64)), ("lambda_bytes", c_f64), ("tp_table", ctypes.POINTER(c_f64)),
-                ("ta_table", ctypes.POINTER(c_f64)), ("k_override", ctypes.POINTER(c_i32))]
+                ("ta_table", ctypes.POINTER(c_f64)), ("k_override", ctypes.POINTER(c_i32)),
+                ("uniform", c_i32), ("reserved", c_i32)]
 
 
 class Plan(ctypes.Structure):
@@ -90,6 +91,7 @@ SIGNATURES = {
     "mopar_model_set_timing": (c_i32, [c_vp, c_i32]),
     "mopar_model_timing_slots": (c_i32, [c_vp, ctypes.POINTER(c_i32)]),
     "mopar_model_op_times": (c_i32, [c_vp, ctypes.POINTER(c_f32), c_i32]),
+    "mopar_model_profile_dominant": (c_i32, [c_vp, c_f64, ctypes.POINTER(LayerProfile)]),
     "mopar_model_measure": (c_i32, [c_vp, c_i32, c_i32, c_vp, c_vp, c_vp, ctypes.c_size_t, c_vp,
                                     ctypes.POINTER(c_f64)]),
     "mopar_last_error": (ctypes.c_char_p, []),

@@ -70,13 +70,15 @@ def _profiles_array(profiles):
 
 
 def mopar_plan_slices(profiles, n_slices=0, allowed_cut=None, elim_tau=0.05, c_m=1.0, c_n=1.0, bw=8.0e12,
-                      ratio=None, k_max=1, lambda_bytes=0.0, tp_table=None, ta_table=None, k_override=None):
+                      ratio=None, k_max=1, lambda_bytes=0.0, tp_table=None, ta_table=None, k_override=None,
+                      uniform=False):
     """HyPAD partitioning in the library.  ``profiles``: sequence of (mem, time, out_bytes, rd_width)."""
     n = len(profiles)
     prof = _profiles_array(profiles)
     o = L.PlanOpts()
     o.n_slices, o.k_max, o.elim_tau, o.c_m, o.c_n, o.bw_Bps = n_slices, k_max, elim_tau, c_m, c_n, bw
     o.lambda_bytes = lambda_bytes
+    o.uniform = 1 if uniform else 0
     keep = []
     if allowed_cut is not None:
         a = (ctypes.c_uint8 * max(1, n - 1))(*[1 if v else 0 for v in allowed_cut])
@@ -285,9 +287,14 @@ class SlicedModel:
             self.handle = None
 
     # -- planning -----------------------------------------------------------
-    def profile(self):
+    def profile(self, dominant=None):
+        """Layer profiles (Eq. 1-4); ``dominant`` = f builds them from each node's dominant
+        operators (mopar_model_profile_dominant), None from every op."""
         arr = (L.LayerProfile * self.n_layers)()
-        check(lib().mopar_model_profile(self.handle, arr))
+        if dominant is None:
+            check(lib().mopar_model_profile(self.handle, arr))
+        else:
+            check(lib().mopar_model_profile_dominant(self.handle, float(dominant), arr))
         return [(p.mem_bytes, p.time_s, p.out_bytes, p.rd_width) for p in arr]
 
     def plan(self, **opts):

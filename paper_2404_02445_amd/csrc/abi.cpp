@@ -11,7 +11,7 @@ int plan_slices_impl(const mopar_layer_profile*, int32_t, const mopar_plan_opts*
 int subslice_range_impl(int32_t, int32_t, int32_t, int32_t*, int32_t*);
 int model_create_impl(const mopar_model_desc*, const void*, size_t, mopar_model_t*);
 void model_destroy_impl(mopar_model_t);
-int model_profile_impl(const mopar_model_s*, mopar_layer_profile*);
+int model_profile_impl(const mopar_model_s*, mopar_layer_profile*, double);
 int workspace_bytes_impl(const mopar_model_s*, const mopar_plan*, size_t*);
 int slice_forward_impl(const mopar_model_s*, const mopar_plan*, int32_t, const void*, void*, void*, size_t, void*);
 int code_bytes_impl(const mopar_codec*, const mopar_tensor_desc*, size_t*);
@@ -76,7 +76,11 @@ int mopar_model_create(const mopar_model_desc* desc, const void* weights_dev, si
 void mopar_model_destroy(mopar_model_t model) { model_destroy_impl(model); }
 
 int mopar_model_profile(mopar_model_t model, mopar_layer_profile* out) {
-    return guarded("mopar_model_profile", [&] { return model_profile_impl(model, out); });
+    return guarded("mopar_model_profile", [&] { return model_profile_impl(model, out, 1.0); });
+}
+
+int mopar_model_profile_dominant(mopar_model_t model, double frac, mopar_layer_profile* out) {
+    return guarded("mopar_model_profile_dominant", [&] { return model_profile_impl(model, out, frac); });
 }
 
 int mopar_model_workspace_bytes(mopar_model_t model, const mopar_plan* plan, size_t* bytes) {

@@ -145,15 +145,38 @@ static void op_profile(const mopar_model_s& m, const mopar_op& op, double* mem, 
     *time = std::fmax(static_cast<double>(flop) / peak, *mem / kPeakBytes);
 }
 
-int model_profile_impl(const mopar_model_s* m, mopar_layer_profile* out) {
+int model_profile_impl(const mopar_model_s* m, mopar_layer_profile* out, double frac) {
     if (!m || !out) return set_error(MOPAR_E_ARG, "mopar_model_profile: null argument");
+    if (!(frac > 0.0 && frac <= 1.0)) return set_error(MOPAR_E_ARG, "mopar_model_profile_dominant: frac must be in (0, 1]");
     for (int l = 0; l < m->n_layers; ++l) {
         double mc = 0.0, tc = 0.0;
         std::map<int, std::vector<std::pair<int, int>>> at_pos;   // pos -> (branch, op)
         int rdw = 0;
+        // dominant operators: largest footprints first, the shortest prefix reaching frac
+        const int f0 = m->layer_first[l], nl = m->layer_last[l] - f0 + 1;
+        std::vector<double> mem(nl);
+        double total = 0.0;
+        for (int q = 0; q < nl; ++q) {
+            double tt;
+            op_profile(*m, m->ops[f0 + q], &mem[q], &tt);
+            total = total + mem[q];
+        }
+        std::vector<int> order(nl);
+        for (int q = 0; q < nl; ++q) order[q] = q;
+        std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return mem[a] > mem[b]; });
+        std::vector<char> keep(nl, frac >= 1.0 ? 1 : 0);
+        if (frac < 1.0) {
+            double acc = 0.0;
+            for (int q : order) {
+                acc = acc + mem[q];
+                keep[q] = 1;
+                if (acc >= frac * total) break;
+            }
+        }
         for (int i = m->layer_first[l]; i <= m->layer_last[l]; ++i) {
             const auto& op = m->ops[i];
             if (op.rd) rdw = rdw == 0 ? op.n_out : std::min(rdw, op.n_out);
+            if (!keep[i - f0]) continue;
             if (op.branch == 0) {
                 double mm, tt;
                 op_profile(*m, op, &mm, &tt);

@@ -16,7 +16,9 @@
 //   * parallelism: per slice, eta in 1..eta_max (k_max, and floor(M_g/lambda)
 //     when lambda > 0) minimising sum (t_p + t_a) of Eq. 5 (ties: smallest eta),
 //     assigned to the slice's RD nodes;
-//   * the latency constraint of Eq. 6 is evaluated and reported, not enforced.
+//   * the latency constraint of Eq. 6 is evaluated and reported, not enforced;
+//   * the Uniform variant of the evaluation keeps the slice count and gives every
+//     slice the same number of nodes (array_split sizes).
 // Sums run in ascending node order so the doubles are reproducible.
 #include <cmath>
 #include <limits>
@@ -91,7 +93,23 @@ int plan_slices_impl(const mopar_layer_profile* L, int32_t n, const mopar_plan_o
     if (K < 0 || K > n) return set_error(MOPAR_E_INFEASIBLE, "mopar_plan_slices: n_slices out of range");
     std::vector<int> ends;
     double cost;
-    if (K == 0) {
+    if (o->uniform) {
+        // Uniform: K slices of equal node counts (the first n mod K one longer)
+        if (K == 0) return set_error(MOPAR_E_ARG, "mopar_plan_slices: the uniform variant needs n_slices > 0");
+        const int q = n / K, r = n % K;
+        std::vector<int> fwd;
+        for (int s = 0, e = -1; s < K; ++s) {
+            e += q + (s < r ? 1 : 0);
+            fwd.push_back(e);
+        }
+        cost = 0.0;
+        for (int s = 0, i = 1; s < K; ++s) {
+            const int j = fwd[s] + 1;
+            cost = cost + (cost_cal(c, i, j) + cost_com(c, j));
+            i = j + 1;
+        }
+        ends.assign(fwd.rbegin(), fwd.rend());
+    } else if (K == 0) {
         std::vector<double> dp(n + 1, kInf);
         std::vector<int> arg(n + 1, 0);
         dp[0] = 0.0;

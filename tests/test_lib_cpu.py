@@ -202,3 +202,31 @@ def test_measure_argument_checks_host_only():
     st = P.lib().mopar_model_measure(sm.handle, 4, 1, dummy, dummy, None, 0, None, tab)
     assert st == L.MOPAR_E_WORKSPACE or sm.workspace_bytes(P.make_plan(len(m.layers), [len(m.layers) - 1],
                                                                         [1] * len(m.layers))) == 0
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_dominant_profile_equals_oracle(cfg):
+    kw = {} if cfg != 3 else dict(batch=2, hw=64)
+    m = synth.build(cfg, **kw)
+    sm = P.SlicedModel(m, device="cpu")
+    for frac in (0.8, 0.5):
+        got = sm.profile(dominant=frac)
+        want = OP.layer_profiles(m, dominant=frac)
+        assert [tuple(g) for g in got] == [(w.mem_bytes, w.time_s, w.out_bytes, w.rd_width) for w in want]
+    with pytest.raises(P.MoparError):
+        sm.profile(dominant=0.0)
+
+
+def test_uniform_plan_bitwise_equal_to_oracle():
+    rng = np.random.default_rng(7)
+    for trial in range(60):
+        n = int(rng.integers(1, 16))
+        prof = _rand_prof(rng, n)
+        K = int(rng.integers(1, n + 1))
+        kmax = int(rng.integers(1, 4))
+        kw = dict(n_slices=K, uniform=True, k_max=kmax, ratio=[float(rng.choice([1, 8])) for _ in range(n - 1)])
+        want = OP.plan_slices([OP.LayerProfile(*p) for p in prof], OP.PlanOpts(**kw))
+        got = P.mopar_plan_slices(prof, **kw)
+        assert (got.slice_end, got.k, got.cost, got.t_tau) == (want.slice_end, want.k, want.cost, want.t_tau)
+    with pytest.raises(P.MoparError):
+        P.mopar_plan_slices([(1.0, 1.0, 1.0, 0)], n_slices=0, uniform=True)

@@ -211,3 +211,62 @@ def test_cfg1_plan_three_slices_and_rd_split():
     assert pl.n_slices == 3
     assert pl.k[m.layers.index("conv6")] == 2
     assert sum(pl.k) == len(m.layers) + 1
+
+
+# --- dominant operators (Sec. III-B) and the Uniform variant (Sec. IV) -------------
+
+def test_dominant_ops_is_smallest_set_reaching_the_share():
+    # brute force: the selected set has the fewest ops of any subset whose footprint
+    # reaches 80 % of the total, and it consists of the largest ops (ties by position)
+    import itertools
+    rng = np.random.default_rng(11)
+    for trial in range(300):
+        n = int(rng.integers(1, 8))
+        mems = [float(v) for v in rng.integers(1, 6, n) * (10.0 ** rng.integers(0, 3, n))]
+        frac = [0.8, 0.5, 1.0, 0.95][trial % 4]
+        got = P.dominant_ops(mems, frac)
+        total = sum(mems)
+        need = min(len(c) for r in range(1, n + 1) for c in itertools.combinations(range(n), r)
+                   if sum(mems[i] for i in c) >= frac * total - 1e-9 * total)
+        assert len(got) == need
+        cut = sorted(mems, reverse=True)[need - 1]
+        assert all(mems[i] >= cut for i in got)
+        assert got == sorted(got)
+
+
+def test_dominant_ops_hand_cases():
+    assert P.dominant_ops([50, 30, 15, 5], 0.8) == [0, 1]
+    assert P.dominant_ops([5, 15, 30, 50], 0.8) == [2, 3]
+    assert P.dominant_ops([10, 10, 10, 10], 0.8) == [0, 1, 2, 3]
+    assert P.dominant_ops([10, 10, 10, 10], 0.5) == [0, 1]          # ties: earlier positions first
+    assert P.dominant_ops([7], 0.8) == [0]
+
+
+def test_layer_profile_from_dominant_ops(fake_profiles):
+    # chain of four ops with memories 50, 30, 15, 5 and times 1, 2, 4, 8:
+    # dominant (80 %) = first two -> M = 50, t = 3; all ops -> M = 50, t = 15
+    m = _mini_model([(0, 1, 50, 1.0), (0, 2, 30, 2.0), (0, 3, 15, 4.0), (0, 4, 5, 8.0)])
+    p = P.layer_profiles(m, dominant=0.8)[0]
+    assert (p.mem_bytes, p.time_s) == (50.0, 3.0)
+    q = P.layer_profiles(m)[0]
+    assert (q.mem_bytes, q.time_s) == (50.0, 15.0)
+    # branches: dominant ops are 9 (b1, pos 2) and 7 (b2, pos 1) and 5 (b1 pos 1): total 25, 80 % = 20
+    m = _mini_model([(1, 1, 5, 2.0), (2, 1, 7, 5.0), (1, 2, 9, 1.0), (1, 3, 4, 3.0)])
+    p = P.layer_profiles(m, dominant=0.8)[0]
+    # kept: 9, 7, 5 (21 >= 20); positions: 1 -> 5 + 7 = 12 (t max 5), 2 -> 9 (t 1)
+    assert (p.mem_bytes, p.time_s) == (12.0, 6.0)
+
+
+@pytest.mark.parametrize("n,K", [(7, 3), (10, 4), (5, 5), (6, 1), (13, 4)])
+def test_uniform_variant_sizes_and_cost(n, K):
+    rng = np.random.default_rng(n * 10 + K)
+    prof = _rand_prof(rng, n)
+    u = P.plan_slices(prof, P.PlanOpts(n_slices=K, uniform=True))
+    sizes = [len(c) for c in np.array_split(np.arange(n), K)]          # numpy's equal split
+    assert np.diff([-1] + u.slice_end).tolist() == sizes
+    # the DP's optimum over the same slice count can only be cheaper
+    best, _ = P.brute_force_plan(prof, P.PlanOpts(n_slices=K, elim_tau=-1.0))
+    assert best <= u.cost
+    assert u.cost == P.plan_cost(prof, P.PlanOpts(), u.slice_end)
+    with pytest.raises(ValueError):
+        P.plan_slices(prof, P.PlanOpts(n_slices=0, uniform=True))
