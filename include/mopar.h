@@ -171,7 +171,12 @@ typedef struct {
     int32_t kh, kw, stride, pad;
     int32_t heads;
     int32_t n_out;              /* conv C_out, linear N, LSTM hidden size */
-    int32_t reserved;
+    int32_t out_off;            /* conv: first channel of `out` this op writes.  When out has more
+                                   channels than n_out, the op fills channels [out_off,
+                                   out_off + n_out) -- the branches of a parallel node concatenated
+                                   in place (Sec. III-B, parallel topology); the writers of one
+                                   tensor sit in one node, tile its channels exactly, take no
+                                   residual, and precede every reader.  0 otherwise. */
     float eps;
     float scale;
     int64_t rows[3];            /* table rows: EMBED_BERT vocab, positions, token types; EMBED vocab */

@@ -306,9 +306,18 @@ def forward(model, x, k=None, cuts=(), codecs=None, sample=None, keep=False):
         for op in [o for o in model.ops if o["layer"] == li]:
             kk = 1 if k is None else int(k[li])
             if op.get("rd") and kk > 1:
-                env[op["out"]] = run_op_sliced(model, op, env, kk)
+                res = run_op_sliced(model, op, env, kk)
             else:
-                env[op["out"]] = run_op(model, op, env)
+                res = run_op(model, op, env)
+            if "out_off" in op:
+                # a branch of a parallel node: its channels of the concatenated node output
+                full = env.get(op["out"])
+                if full is None:
+                    full = np.zeros((res.shape[0],) + tuple(model.tensors[op["out"]]["shape"][1:]), dtype=res.dtype)
+                    env[op["out"]] = full
+                full[:, op["out_off"]:op["out_off"] + res.shape[1]] = res
+            else:
+                env[op["out"]] = res
         if li in cuts:
             ci = cuts.index(li)
             tid = model.layer_output_tid(li)

@@ -64,9 +64,11 @@ def op_profile(model, op):
         if key in op:
             pb += _numel(model.weights[op[key]].shape) * DTYPE_BYTES[dt]
     ib = sum(_numel(T[t]["shape"]) * DTYPE_BYTES[T[t]["dtype"]] for t in op["inputs"])
-    ob = _numel(T[op["out"]]["shape"]) * DTYPE_BYTES[T[op["out"]]["dtype"]]
     k = op["kind"]
     out_shape = T[op["out"]]["shape"]
+    if k == "conv":             # a branch writing part of a concatenated tensor counts its own channels
+        out_shape = (out_shape[0], op["cout"], out_shape[2], out_shape[3])
+    ob = _numel(out_shape) * DTYPE_BYTES[T[op["out"]]["dtype"]]
     in_shape = T[op["inputs"][0]]["shape"]
     if k == "conv":
         flop = 2 * _numel(out_shape) * in_shape[1] * op["kh"] * op["kw"]

@@ -51,7 +51,7 @@ class TensorDesc(ctypes.Structure):
 class Op(ctypes.Structure):
     _fields_ = [("kind", c_i32), ("act", c_i32), ("layer", c_i32), ("branch", c_i32), ("pos", c_i32),
                 ("rd", c_i32), ("in0", c_i32), ("in1", c_i32), ("out", c_i32), ("kh", c_i32), ("kw", c_i32),
-                ("stride", c_i32), ("pad", c_i32), ("heads", c_i32), ("n_out", c_i32), ("reserved", c_i32),
+                ("stride", c_i32), ("pad", c_i32), ("heads", c_i32), ("n_out", c_i32), ("out_off", c_i32),
                 ("eps", c_f32), ("scale", c_f32), ("rows", c_i64 * 3), ("w", c_i64), ("b", c_i64),
                 ("w2", c_i64), ("w3", c_i64), ("w4", c_i64), ("w5", c_i64)]
 

@@ -207,6 +207,7 @@ def _pack(model):
         if k == "conv":
             o.kind, o.act = L.OP_CONV, L.ACT[op["act"]]
             o.kh, o.kw, o.stride, o.pad, o.n_out = op["kh"], op["kw"], op["stride"], op["pad"], op["cout"]
+            o.out_off = op.get("out_off", 0)
             w = W[op["w"]]
             c = w.shape[1]
             cs = c if c % epc == 0 else (c + epc - 1) // epc * epc

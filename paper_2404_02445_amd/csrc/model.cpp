@@ -126,11 +126,13 @@ static void op_profile(const mopar_model_s& m, const mopar_op& op, double* mem, 
     int64_t ib = numel(m.tensors[op.in0]) * static_cast<int64_t>(elt_bytes(m.tensors[op.in0].dtype));
     if (op.in1 >= 0) ib += numel(m.tensors[op.in1]) * static_cast<int64_t>(elt_bytes(m.tensors[op.in1].dtype));
     const auto& o = m.tensors[op.out];
-    const int64_t ob = numel(o) * static_cast<int64_t>(elt_bytes(o.dtype));
+    // a conv that fills part of a concatenated tensor counts its own channels only
+    const int64_t on = op.kind == MOPAR_OP_CONV ? numel(o) / o.dims[1] * op.n_out : numel(o);
+    const int64_t ob = on * static_cast<int64_t>(elt_bytes(o.dtype));
     const auto& in = m.tensors[op.in0];
     int64_t flop = 0;
     switch (op.kind) {
-        case MOPAR_OP_CONV: flop = 2 * numel(o) * in.dims[1] * op.kh * op.kw; break;
+        case MOPAR_OP_CONV: flop = 2 * on * in.dims[1] * op.kh * op.kw; break;
         case MOPAR_OP_LINEAR: {
             const int64_t K = in.rank == 4 ? in.dims[1] * in.dims[2] * in.dims[3] : in.dims[in.rank - 1];
             flop = 2 * numel(o) * K;
@@ -230,6 +232,8 @@ static int validate_and_build(mopar_model_s& m) {
             return set_error(MOPAR_E_DTYPE, "tensor " + std::to_string(t) + ": dtype must be the model dtype");
     }
     std::vector<int> producer(nt, -1);
+    std::vector<int64_t> filled(nt, 0);          // channels written so far by partial (concat) writers
+    std::vector<int> last_writer(nt, -1);
     int prev_layer = -1;
     m.layer_first.assign(m.n_layers, -1);
     m.layer_last.assign(m.n_layers, -1);
@@ -255,12 +259,27 @@ static int validate_and_build(mopar_model_s& m) {
         if (op.branch < 0 || (op.branch > 0 && op.pos < 1)) return set_error(MOPAR_E_ARG, nm + ": branch/pos");
         if (!tid_ok(op.in0) || !tid_ok(op.out) || (op.in1 != -1 && !tid_ok(op.in1)))
             return set_error(MOPAR_E_ARG, nm + ": tensor id out of range");
-        if (producer[op.out] != -1 || op.out == m.input)
-            return set_error(MOPAR_E_ARG, nm + ": output tensor written twice");
+        // a conv whose output tensor is wider than n_out fills channels [out_off, out_off + n_out)
+        const bool partial = op.kind == MOPAR_OP_CONV && m.tensors[op.out].rank == 4 &&
+                             m.tensors[op.out].dims[1] > op.n_out;
+        if (op.out == m.input) return set_error(MOPAR_E_ARG, nm + ": writes the model input");
+        if (partial) {
+            const auto& y = m.tensors[op.out];
+            if (op.out_off != filled[op.out] || op.out_off + op.n_out > y.dims[1] || op.in1 >= 0)
+                return set_error(MOPAR_E_ARG, nm + ": concatenating writers must fill the channels in order, "
+                                                   "without overlap or residual");
+            if (producer[op.out] != -1 && m.ops[producer[op.out]].layer != op.layer)
+                return set_error(MOPAR_E_ARG, nm + ": concatenating writers of a tensor must share a node");
+        } else {
+            if (op.out_off != 0) return set_error(MOPAR_E_ARG, nm + ": out_off without a wider output tensor");
+            if (producer[op.out] != -1) return set_error(MOPAR_E_ARG, nm + ": output tensor written twice");
+        }
         for (int t : {op.in0, op.in1}) {
             if (t < 0) continue;
             if (t != m.input && producer[t] < 0)
                 return set_error(MOPAR_E_ARG, nm + ": reads a tensor before it is produced");
+            if (t != m.input && last_writer[t] >= 0 && filled[t] != m.tensors[t].dims[1])
+                return set_error(MOPAR_E_ARG, nm + ": reads a concatenated tensor before all its channels are written");
             // single-input planning nodes: every op reads tensors of its own node, or the
             // tensor leaving the previous node (or the model input for node 0)
             if (t == m.input) {
@@ -289,7 +308,7 @@ static int validate_and_build(mopar_model_s& m) {
                     return set_error(MOPAR_E_SHAPE, nm + ": conv geometry");
                 const int64_t ho = (x.dims[2] + 2 * op.pad - op.kh) / op.stride + 1;
                 const int64_t wo = (x.dims[3] + 2 * op.pad - op.kw) / op.stride + 1;
-                if (ho < 1 || wo < 1 || !shape_eq(y, {x.dims[0], op.n_out, ho, wo}))
+                if (ho < 1 || wo < 1 || !shape_eq(y, {x.dims[0], partial ? y.dims[1] : op.n_out, ho, wo}))
                     return set_error(MOPAR_E_SHAPE, nm + ": conv output shape");
                 if (op.in1 >= 0 && !shape_eq(m.tensors[op.in1], {x.dims[0], op.n_out, ho, wo}))
                     return set_error(MOPAR_E_SHAPE, nm + ": residual shape");
@@ -399,8 +418,15 @@ static int validate_and_build(mopar_model_s& m) {
             }
             default: return set_error(MOPAR_E_ARG, nm + ": unknown op kind");
         }
-        producer[op.out] = i;
+        if (producer[op.out] == -1) producer[op.out] = i;
+        if (partial) {
+            filled[op.out] += op.n_out;
+            last_writer[op.out] = i;
+        }
     }
+    for (int t = 0; t < nt; ++t)
+        if (last_writer[t] >= 0 && filled[t] != m.tensors[t].dims[1])
+            return set_error(MOPAR_E_ARG, "tensor " + std::to_string(t) + ": concatenating writers leave channels unwritten");
     if (prev_layer != m.n_layers - 1) return set_error(MOPAR_E_ARG, "model: a planning node has no ops");
     if (producer[m.output] != static_cast<int>(m.ops.size()) - 1)
         return set_error(MOPAR_E_ARG, "model: the output must be produced by the last op");
@@ -435,7 +461,7 @@ static int validate_and_build(mopar_model_s& m) {
         inf.temp_off.clear();
         for (size_t tb : inf.temps) inf.temp_off.push_back(alloc(tb, i));
         const int t = m.ops[i].out;
-        if (t != m.output) {
+        if (t != m.output && m.offset[t] == SIZE_MAX) {   // first writer allocates (concatenations)
             const size_t bytes = static_cast<size_t>(numel(m.tensors[t])) * es;
             m.offset[t] = alloc(bytes, std::max(last_use[t], i));
         }
@@ -559,8 +585,8 @@ static hipError_t run_op(const mopar_model_s& m, int i, const Ptrs& P, int ksub,
             g.B = W(m, op.w);
             g.bias = W(m, op.b);
             g.res = op.in1 >= 0 ? P.get(op.in1) : nullptr;
-            g.C = P.get(op.out);
-            g.ldc = op.n_out;
+            g.ldc = y.dims[1];                     // > n_out when the op fills part of a concatenation
+            g.C = static_cast<unsigned char*>(P.get(op.out)) + static_cast<size_t>(op.out_off) * elt_bytes(m.dtype);
             g.M = inf.M;
             g.N = op.n_out;
             g.K = static_cast<int>(inf.K);

@@ -126,10 +126,31 @@ class _Builder:
             bias = np.zeros(cout)
         self.store(name + ".w", wt)
         self.store(name + ".b", bias)
-        out = self.tensor((n, cout, ho, wo))
+        into = kw.pop("into", None)          # (tensor, channel offset): fill part of a concatenation
+        if into is None:
+            out = self.tensor((n, cout, ho, wo))
+        else:
+            out, off = into
+            on, oc, oh, ow = self.shape(out)
+            assert (on, oh, ow) == (n, ho, wo) and off + cout <= oc
+            kw["out_off"] = off
         ins = [x] + ([res] if res is not None else [])
         return self.op(kind="conv", name=name, inputs=ins, out=out, cout=cout, kh=k, kw=k,
                        stride=stride, pad=pad, act=act, w=name + ".w", b=name + ".b", **kw)
+
+    def inception(self, x, c1, c3r, c3, c5r, c5, cp, name, rd=False):
+        """Four parallel branches over x -- 1x1; 1x1 -> 3x3; 1x1 -> 5x5; 3x3 max pool ->
+        1x1 -- written side by side into one concatenated tensor (Eq. 2 topology)."""
+        n, _, h, w = self.shape(x)
+        out = self.tensor((n, c1 + c3 + c5 + cp, h, w))
+        self.conv(x, c1, 1, 1, 0, "relu", name + ".b1", bn_fold=True, branch=1, pos=1, into=(out, 0))
+        t = self.conv(x, c3r, 1, 1, 0, "relu", name + ".b2r", bn_fold=True, branch=2, pos=1)
+        self.conv(t, c3, 3, 1, 1, "relu", name + ".b2", bn_fold=True, branch=2, pos=2, rd=rd, into=(out, c1))
+        t = self.conv(x, c5r, 1, 1, 0, "relu", name + ".b3r", bn_fold=True, branch=3, pos=1)
+        self.conv(t, c5, 5, 1, 2, "relu", name + ".b3", bn_fold=True, branch=3, pos=2, into=(out, c1 + c3))
+        t = self.maxpool(x, 3, 1, 1, name + ".b4p", branch=4, pos=1)
+        return self.conv(t, cp, 1, 1, 0, "relu", name + ".b4", bn_fold=True, branch=4, pos=2,
+                         into=(out, c1 + c3 + c5))
 
     def maxpool(self, x, k, stride, pad, name, **kw):
         n, c, h, w = self.shape(x)
@@ -363,8 +384,36 @@ def lstm_lm(batch=64, seq=128, hidden=1024, emb=1024, vocab=32000, n_layers=2, k
     return bld.finish(y, n_slices=len(cuts) + 1, cuts_after=cuts, k_by_layer={bld.layer: k_rd})
 
 
-BUILDERS = {1: tiny_vgg, 2: resnet50, 3: vgg16, 4: bert_base, 5: lstm_lm}
-NAMES = {1: "tiny_vgg", 2: "resnet50", 3: "vgg16", 4: "bert_base", 5: "lstm_lm"}
+
+
+def inception_mini(batch=2, hw=32, k_rd=2, seed=1006, dtype=BF16):
+    """Small Inception-style CNN (the branching family of the paper's CNN benchmarks): a
+    stem conv and max pool, three four-branch nodes whose branch outputs are concatenated
+    in place (some at channel offsets that are not a whole 16-byte chunk), a second pool,
+    global average pool and a classifier.  Each node's 3x3 branch conv is the RD op."""
+    bld = _Builder("inception_mini", dtype, batch, seed, cfg=6)
+    x = bld.tensor((batch, 3, hw, hw), F32)
+    bld.new_layer("stem")
+    x = bld.conv(x, 32, 3, 2, 1, "relu", "stem.conv", bn_fold=True)
+    bld.new_layer("pool1")
+    x = bld.maxpool(x, 3, 2, 1, "pool1")
+    k_by_layer = {}
+    for nm, ch in (("inc3a", (16, 16, 24, 8, 12, 12)), ("inc3b", (24, 24, 32, 8, 20, 20)),
+                   ("pool2", None), ("inc4a", (32, 32, 48, 8, 16, 16))):
+        bld.new_layer(nm)
+        if ch is None:
+            x = bld.maxpool(x, 3, 2, 1, nm)
+            continue
+        x = bld.inception(x, *ch, nm, rd=True)
+        k_by_layer[bld.layer] = k_rd
+    bld.new_layer("head")
+    x = bld.avgpool(x, "gap")
+    y = bld.linear(x, 10, "none", "fc", "he")
+    return bld.finish(y, n_slices=3, k_by_layer=k_by_layer)
+
+
+BUILDERS = {1: tiny_vgg, 2: resnet50, 3: vgg16, 4: bert_base, 5: lstm_lm, 6: inception_mini}
+NAMES = {1: "tiny_vgg", 2: "resnet50", 3: "vgg16", 4: "bert_base", 5: "lstm_lm", 6: "inception_mini"}
 
 
 def build(cfg: int, **kw) -> Model:

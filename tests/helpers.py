@@ -13,6 +13,7 @@ SMALL = {
             cut_after_pools=(3, 5)),
     4: dict(batch=2, seq=40, layers=3, hidden=128, heads=2, ffn=256, vocab=300, max_pos=64, slice_every=1),
     5: dict(batch=3, seq=9, hidden=64, emb=64, vocab=301),
+    6: dict(batch=3, hw=32),
 }
 
 

@@ -20,7 +20,7 @@ def _np(t):
     return a.transpose(0, 3, 1, 2) if a.ndim == 4 else a
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 4])
+@pytest.mark.parametrize("cfg", [1, 2, 4, 6])
 def test_measured_plan_matches_oracle_planner_and_runs(cfg):
     m = synth.build(cfg, **SMALL[cfg])
     x_host = synth.make_input(m)
@@ -82,3 +82,29 @@ def test_measure_restores_timing_state_and_rejects_bad_arguments():
         sm.measure(x, k_max=0)
     with pytest.raises(P.MoparError):
         sm.measure(x, k_max=2, reps=0)
+
+
+def test_uniform_and_dominant_plans_run_on_the_branching_model():
+    # Uniform variant (same slice count as the DP, equal node counts) on the Inception-style
+    # model, from the dominant-operator profile; every cut carries one tensor
+    m = synth.build(6, **SMALL[6])
+    x_host = synth.make_input(m)
+    sm = P.SlicedModel(m)
+    prof = sm.profile(dominant=0.8)
+    mopar = P.mopar_plan_slices(prof, n_slices=0, k_max=2)
+    uni = P.mopar_plan_slices(prof, n_slices=mopar.n_slices, uniform=True, k_max=2)
+    want = OP.plan_slices([OP.LayerProfile(*p) for p in prof],
+                          OP.PlanOpts(n_slices=mopar.n_slices, uniform=True, k_max=2))
+    assert (uni.slice_end, uni.k, uni.cost) == (want.slice_end, want.k, want.cost)
+    assert mopar.cost <= uni.cost
+    for plan in (mopar, uni):
+        cuts = plan.slice_end[:-1]
+        cw = synth.make_codec_weights(m, cuts, ratio=codec_ratios(m, cuts)) if cuts else None
+        codecs, keep = sm.codecs(plan, "ae", cw)
+        codes = sm.alloc_codes(plan, codecs)
+        ws = sm.alloc_workspace(plan)
+        out = sm.alloc_output()
+        sm.forward(plan, torch.from_numpy(x_host).cuda(), out, codecs, codes, ws)
+        torch.cuda.synchronize()
+        ref = oracle.forward(m, x_host, k=plan.k, cuts=cuts, codecs=cw)
+        assert rel_err(_np(out), ref) <= TOL[m.dtype]

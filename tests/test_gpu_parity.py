@@ -287,7 +287,7 @@ def test_codec_errors_enqueue_nothing():
 # whole models (shrunken workloads)
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
 def test_small_model_sliced_ae_parity(cfg):
     m = synth.build(cfg, **SMALL[cfg])
     x = synth.make_input(m)
@@ -304,7 +304,7 @@ def test_small_model_sliced_ae_parity(cfg):
     assert rel_err(_np(y), ref) <= TOL[m.dtype]
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
 def test_small_model_raw_slicing_and_subslicing_bitwise(cfg):
     m = synth.build(cfg, **SMALL[cfg])
     x = synth.make_input(m)

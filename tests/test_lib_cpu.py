@@ -11,6 +11,9 @@ import pytest
 import oracle
 import synth
 from oracle import plan as OP
+from helpers import SMALL
+
+SMALL6 = SMALL[6]
 
 P = pytest.importorskip("paper_2404_02445_amd")
 from paper_2404_02445_amd import _lib as L  # noqa: E402
@@ -93,7 +96,7 @@ def test_planner_error_paths():
     assert P.mopar_plan_slices(prof, n_slices=2).slice_end == [0, 1]
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
 def test_model_profile_and_plan_equal_oracle(cfg):
     kw = {} if cfg != 3 else dict(batch=2, hw=64)
     m = synth.build(cfg, **kw)
@@ -204,7 +207,7 @@ def test_measure_argument_checks_host_only():
                                                                         [1] * len(m.layers))) == 0
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
 def test_dominant_profile_equals_oracle(cfg):
     kw = {} if cfg != 3 else dict(batch=2, hw=64)
     m = synth.build(cfg, **kw)
@@ -230,3 +233,33 @@ def test_uniform_plan_bitwise_equal_to_oracle():
         assert (got.slice_end, got.k, got.cost, got.t_tau) == (want.slice_end, want.k, want.cost, want.t_tau)
     with pytest.raises(P.MoparError):
         P.mopar_plan_slices([(1.0, 1.0, 1.0, 0)], n_slices=0, uniform=True)
+
+
+def test_concatenating_writers_validated():
+    m = synth.build(6, **SMALL6)
+    tens, ops, blob = P.binding._pack(m)
+    host = np.zeros(blob.size, dtype=np.uint8)
+
+    def create(ops_arr):
+        d = L.ModelDesc()
+        d.dtype = L.MOPAR_BF16
+        d.n_tensors, d.tensors = len(m.tensors), ctypes.cast(tens, ctypes.POINTER(L.TensorDesc))
+        d.n_ops, d.ops = len(m.ops), ctypes.cast(ops_arr, ctypes.POINTER(L.Op))
+        d.n_layers, d.input, d.output = len(m.layers), m.input_tid, m.output_tid
+        h = ctypes.c_void_p()
+        st = P.lib().mopar_model_create(ctypes.byref(d), host.ctypes.data_as(ctypes.c_void_p), blob.size,
+                                        ctypes.byref(h))
+        if st == 0:
+            P.lib().mopar_model_destroy(h)
+        return st
+
+    assert create(ops) == 0
+    writers = [i for i, o in enumerate(m.ops) if "out_off" in o]
+    first, second = writers[0], writers[1]
+    bad = (L.Op * len(m.ops))(*ops)
+    bad[second].out_off += 1                      # a gap / overlap between branches
+    assert create(bad) == L.MOPAR_E_ARG
+    bad = (L.Op * len(m.ops))(*ops)
+    bad[first].out_off = 0
+    bad[first].n_out += 8                         # writes past the next branch's channels
+    assert create(bad) != 0

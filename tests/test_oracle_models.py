@@ -33,6 +33,7 @@ def torch_forward(m, x):
         env = {m.input_tid: torch.from_numpy(x.astype(np.int64))}
     else:
         env = {m.input_tid: _round(torch.from_numpy(x.astype(np.float64)), dt)}
+    parts = {}
     for op in m.ops:
         ins = [env[t] for t in op["inputs"]]
         k = op["kind"]
@@ -88,6 +89,9 @@ def torch_forward(m, x):
             y = torch.stack(outs, 1)
         else:
             raise ValueError(k)
+        if "out_off" in op:                 # branch of a parallel node: channel concatenation
+            parts.setdefault(op["out"], []).append((op["out_off"], y))
+            y = torch.cat([p for _, p in sorted(parts[op["out"]], key=lambda q: q[0])], dim=1)
         env[op["out"]] = y
     return env[m.output_tid].numpy()
 
@@ -99,10 +103,11 @@ SMALL = {
             cut_after_pools=(2, 4)),
     4: dict(batch=2, seq=16, layers=2, hidden=64, heads=2, ffn=128, vocab=100, max_pos=32, slice_every=1),
     5: dict(batch=2, seq=6, hidden=32, emb=24, vocab=50),
+    6: dict(batch=2, hw=16),
 }
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
 def test_oracle_model_matches_torch_library_forward(cfg):
     m = synth.build(cfg, **SMALL[cfg])
     x = synth.make_input(m)
