@@ -205,7 +205,9 @@ void mopar_model_destroy(mopar_model_t model);
 /* Layer profiles (Eq. 1-4) of the model: op memory = bytes of parameters +
  * inputs + output; op time = max(FLOP / peak, bytes / 8e12), peak 2.5e15
  * (bf16) or 157.3e12 (f32) FLOP/s; FLOP counted for conv, linear, attention
- * and LSTM.  `out` has n_layers entries. */
+ * and LSTM.  out_bytes of node j < n_layers - 1 is the size of every tensor
+ * crossing the cut after it (mopar_model_cut_tensors), of the last node its
+ * output.  `out` has n_layers entries. */
 int mopar_model_profile(mopar_model_t model, mopar_layer_profile* out);
 
 /* The same profile built from each node's dominant operators only (Sec.
@@ -222,9 +224,11 @@ int mopar_model_workspace_bytes(mopar_model_t model, const mopar_plan* plan, siz
 
 /* Run slice s of `plan`: the layers after the previous cut up to
  * slice_end[s].  `in_dev` holds the slice input (the model input for s = 0,
- * otherwise the boundary tensor leaving slice s-1, in its physical layout);
- * `out_dev` receives the tensor leaving slice s.  RD ops of node l run as
- * k[l] sub-slices of one launch. */
+ * otherwise the output of node slice_end[s-1], in its physical layout);
+ * `out_dev` receives the output of node slice_end[s].  Any other tensor
+ * crossing the cut before slice s (a skip edge, see mopar_model_cut_tensors)
+ * is read from its slot in `ws`, where the earlier slices, run with the same
+ * workspace, left it.  RD ops of node l run as k[l] sub-slices of one launch. */
 int mopar_slice_forward(mopar_model_t model, const mopar_plan* plan, int32_t s, const void* in_dev,
                         void* out_dev, void* ws, size_t ws_bytes, void* stream);
 
@@ -267,16 +271,26 @@ int mopar_boundary_decode(const mopar_codec* codec, const mopar_tensor_desc* y, 
 /* Whole model                                                               */
 /* ------------------------------------------------------------------------ */
 
-/* Sliced forward pass: for each slice s, decode code_bufs[s-1] into the
- * slice input (s > 0), run the slice, and encode its output into
- * code_bufs[s] (s < S-1), all on `stream` with no host round-trip (the
- * device buffer and stream order stand for the share-memory directory and
- * message channel of Sec. III-D).  `codecs` and `code_bufs` have S-1
- * entries (may be NULL when S = 1); code_bufs[s] must hold
- * mopar_boundary_code_bytes of that boundary. */
+/* Sliced forward pass: for each slice s, decode the tensors crossing the cut
+ * before it (s > 0), run the slice, and encode the tensors crossing the cut
+ * after it (s < S-1), all on `stream` with no host round-trip (the device
+ * buffers and stream order stand for the share-memory directory and message
+ * channel of Sec. III-D).  A cut after node j carries the tensors of
+ * mopar_model_cut_tensors(j): one for a chain of single-input nodes, more
+ * where skip edges cross it.  `codecs` and `code_bufs` have one entry per
+ * boundary tensor -- the tensors of cut 0 in ascending id, then those of
+ * cut 1, ... (S-1 entries for a chain; may be NULL when S = 1); each buffer
+ * holds mopar_boundary_code_bytes of its tensor. */
 int mopar_model_forward(mopar_model_t model, const mopar_plan* plan, const mopar_codec* codecs,
                         const void* in_dev, void* out_dev, void* const* code_bufs, void* ws,
                         size_t ws_bytes, void* stream);
+
+/* The tensors a cut after node `node` (0 <= node < n_layers - 1) carries: the
+ * outputs of nodes <= node that nodes > node read (Sec. III-C: after node
+ * elimination, the parallel edges between the two sides are one merged edge
+ * whose size is their sum -- mopar_model_profile's out_bytes of that node).
+ * Writes up to `cap` tensor ids in ascending order to tids; *count = all. */
+int mopar_model_cut_tensors(mopar_model_t model, int32_t node, int32_t* tids, int32_t cap, int32_t* count);
 
 /* ------------------------------------------------------------------------ */
 /* Slice pipeline across requests                                           */
@@ -297,11 +311,11 @@ int mopar_model_forward(mopar_model_t model, const mopar_plan* plan, const mopar
  * streams:   replicas * n_slices caller-owned hipStream_t (default priority).
  * ws:        mopar_pipeline_workspace_bytes(replicas) bytes, used by no one
  *            else while the pipeline lives.
- * code_bufs: replicas * depth * (n_slices - 1) device buffers; the buffer of
- *            (instance r, ring slot q, cut c) is at
- *            [(r * depth + q) * (n_slices - 1) + c], each of
- *            mopar_boundary_code_bytes of that boundary.
- * codecs:    n_slices - 1 codecs (copied).  The plan is copied.
+ * code_bufs: replicas * depth * B device buffers, B = the plan's boundary
+ *            tensors (as for mopar_model_forward); the buffer of (instance r,
+ *            ring slot q, boundary tensor b) is at [(r * depth + q) * B + b],
+ *            each of mopar_boundary_code_bytes of its tensor.
+ * codecs:    B codecs (copied).  The plan is copied.
  * Per-op timing is not recorded by pipelined batches.
  * Errors: as mopar_model_forward; MOPAR_E_HIP if an event cannot be made. */
 typedef struct mopar_pipeline_s* mopar_pipeline_t;

@@ -28,7 +28,7 @@ import subprocess
 
 import numpy as np
 
-from .plan import (subslice_range, layer_profiles, plan_slices, brute_force_plan,  # noqa: F401
+from .plan import (subslice_range, layer_profiles, plan_slices, brute_force_plan, crossing_tensors,  # noqa: F401
                    PlanOpts, Plan)
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -300,7 +300,8 @@ def forward(model, x, k=None, cuts=(), codecs=None, sample=None, keep=False):
     else:
         env = {model.input_tid: round_to(x, model.dtype)}
     cuts = list(cuts)
-    codecs = codecs if codecs is not None else [None] * len(cuts)
+    if codecs is None:
+        codecs = [None] * sum(len(crossing_tensors(model, c)) for c in cuts)
     codes, bounds = {}, {}
     for li in range(len(model.layers)):
         for op in [o for o in model.ops if o["layer"] == li]:
@@ -319,17 +320,21 @@ def forward(model, x, k=None, cuts=(), codecs=None, sample=None, keep=False):
             else:
                 env[op["out"]] = res
         if li in cuts:
+            # every tensor crossing the cut goes through its own codec (cut-major, ascending id)
             ci = cuts.index(li)
-            tid = model.layer_output_tid(li)
-            cd = codecs[ci]
-            bounds[li] = env[tid]
-            if cd is None:
-                code = env[tid].copy()
-                env[tid] = code.copy()
-            else:
-                code = ae_encode(env[tid], cd["w_enc"], cd["b_enc"], model.dtype)
-                env[tid] = ae_decode(code, cd["w_dec"], cd["b_dec"], model.dtype)
-            codes[li] = code
+            base = sum(len(crossing_tensors(model, c)) for c in cuts[:ci])
+            for q, tid in enumerate(crossing_tensors(model, li)):
+                cd = codecs[base + q]
+                bounds[(li, tid)] = env[tid]
+                if cd is None:
+                    code = env[tid].copy()
+                    env[tid] = code.copy()
+                else:
+                    code = ae_encode(env[tid], cd["w_enc"], cd["b_enc"], model.dtype)
+                    env[tid] = ae_decode(code, cd["w_dec"], cd["b_dec"], model.dtype)
+                codes[(li, tid)] = code
+                if tid == model.layer_output_tid(li):
+                    bounds[li], codes[li] = bounds[(li, tid)], code
     y = env[model.output_tid]
     if keep:
         return y, env, codes, bounds

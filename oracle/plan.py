@@ -87,6 +87,22 @@ def op_profile(model, op):
     return mem, time, flop
 
 
+def node_outputs(model):
+    """The tensor leaving each planning node (the output of its last op)."""
+    return [[o for o in model.ops if o["layer"] == l][-1]["out"] for l in range(len(model.layers))]
+
+
+def crossing_tensors(model, j):
+    """Tensors a cut after node j carries (Sec. III-C, edge elimination): every node
+    output of a node <= j that an op of a node > j reads -- after the nodes between
+    them are merged, the edges from one side to the other are parallel edges, merged
+    into one whose size is the sum of these tensors.  Ascending tensor id."""
+    outs = node_outputs(model)
+    src = {t: l for l, t in enumerate(outs) if l <= j}
+    read_later = {t for o in model.ops if o["layer"] > j for t in o["inputs"]}
+    return sorted(t for t in src if t in read_later)
+
+
 @dataclass
 class LayerProfile:
     mem_bytes: float
@@ -153,8 +169,13 @@ def layer_profiles(model, dominant=None):
         tb = 0.0
         for p in sorted(pos_t):
             tb = tb + pos_t[p]
-        T = model.tensors[all_ops[-1]["out"]]
-        ob = float(_numel(T["shape"]) * DTYPE_BYTES[T["dtype"]])
+        if li + 1 < len(model.layers):      # the cut after this node: every crossing tensor
+            ob = 0.0
+            for t in crossing_tensors(model, li):
+                ob = ob + float(_numel(model.tensors[t]["shape"]) * DTYPE_BYTES[model.tensors[t]["dtype"]])
+        else:
+            T = model.tensors[all_ops[-1]["out"]]
+            ob = float(_numel(T["shape"]) * DTYPE_BYTES[T["dtype"]])
         widths = [o["cout"] if o["kind"] == "conv" else o["nout"] for o in all_ops if o.get("rd")]
         out.append(LayerProfile(max(mc, mb), tc + tb, ob, min(widths) if widths else 0))
     return out

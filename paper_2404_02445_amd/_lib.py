@@ -92,6 +92,7 @@ SIGNATURES = {
     "mopar_model_timing_slots": (c_i32, [c_vp, ctypes.POINTER(c_i32)]),
     "mopar_model_op_times": (c_i32, [c_vp, ctypes.POINTER(c_f32), c_i32]),
     "mopar_model_profile_dominant": (c_i32, [c_vp, c_f64, ctypes.POINTER(LayerProfile)]),
+    "mopar_model_cut_tensors": (c_i32, [c_vp, c_i32, ctypes.POINTER(c_i32), c_i32, ctypes.POINTER(c_i32)]),
     "mopar_model_measure": (c_i32, [c_vp, c_i32, c_i32, c_vp, c_vp, c_vp, ctypes.c_size_t, c_vp,
                                     ctypes.POINTER(c_f64)]),
     "mopar_last_error": (ctypes.c_char_p, []),

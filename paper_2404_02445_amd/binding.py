@@ -306,8 +306,20 @@ class SlicedModel:
         kw.update(opts)
         return mopar_plan_slices(self.profile(), **kw)
 
+    def cut_tensors(self, node):
+        """mopar_model_cut_tensors: tensor ids a cut after ``node`` carries."""
+        cnt = L.c_i32()
+        check(lib().mopar_model_cut_tensors(self.handle, node, None, 0, ctypes.byref(cnt)))
+        arr = (L.c_i32 * max(cnt.value, 1))()
+        check(lib().mopar_model_cut_tensors(self.handle, node, arr, cnt.value, ctypes.byref(cnt)))
+        return list(arr[:cnt.value])
+
+    def boundary_tensors(self, plan):
+        """Tensor ids handed over at the plan's cuts: cut-major, ascending id within a cut."""
+        return [t for e in plan.slice_end[:-1] for t in self.cut_tensors(e)]
+
     def cut_tensor_shapes(self, plan):
-        return [self.spec.tensors[self.spec.layer_output_tid(e)]["shape"] for e in plan.slice_end[:-1]]
+        return [self.spec.tensors[t]["shape"] for t in self.boundary_tensors(plan)]
 
     # -- buffers ------------------------------------------------------------
     def workspace_bytes(self, plan):
@@ -325,7 +337,7 @@ class SlicedModel:
     def codecs(self, plan, kind="ae", weights=None):
         """Codec structs (and their device weights) for the plan's cuts; ``weights`` from
         ``synth.make_codec_weights``.  Returns (ctypes array, device tensors kept alive)."""
-        n = max(plan.n_slices - 1, 0)
+        n = len(self.boundary_tensors(plan))
         arr = (L.Codec * max(n, 1))()
         keep = []
         for s in range(n):
@@ -348,8 +360,8 @@ class SlicedModel:
 
     # -- execution ------------------------------------------------------------
     def forward(self, plan, x, out, codecs=None, code_bufs=None, ws=None, stream=None):
-        n = max(plan.n_slices - 1, 0)
-        cb = (ctypes.c_void_p * max(n, 1))(*[b.data_ptr() for b in (code_bufs or [])])
+        bufs = list(code_bufs or [])
+        cb = (ctypes.c_void_p * max(len(bufs), 1))(*[b.data_ptr() for b in bufs])
         cod = codecs if codecs is not None else (L.Codec * 1)()
         check(lib().mopar_model_forward(self.handle, ctypes.byref(plan.raw), cod, _ptr(x), _ptr(out), cb,
                                         _ptr(ws), 0 if ws is None else ws.numel(), _stream_ptr(stream)))

@@ -28,6 +28,7 @@ void pipeline_destroy_impl(mopar_pipeline_s*);
 int set_timing_impl(mopar_model_s*, int32_t);
 int timing_slots_impl(const mopar_model_s*, int32_t*);
 int op_times_impl(const mopar_model_s*, float*, int32_t);
+int cut_tensors_impl(const mopar_model_s*, int32_t, int32_t*, int32_t, int32_t*);
 int measure_impl(mopar_model_s*, int32_t, int32_t, const void*, void*, void*, size_t, void*, double*);
 
 static thread_local std::string g_error;
@@ -143,6 +144,10 @@ int mopar_model_timing_slots(mopar_model_t model, int32_t* n) {
 
 int mopar_model_op_times(mopar_model_t model, float* ms, int32_t n) {
     return guarded("mopar_model_op_times", [&] { return op_times_impl(model, ms, n); });
+}
+
+int mopar_model_cut_tensors(mopar_model_t model, int32_t node, int32_t* tids, int32_t cap, int32_t* count) {
+    return guarded("mopar_model_cut_tensors", [&] { return cut_tensors_impl(model, node, tids, cap, count); });
 }
 
 int mopar_model_measure(mopar_model_t model, int32_t k_max, int32_t reps, const void* in_dev, void* out_dev,

@@ -56,6 +56,8 @@ struct mopar_model_s {
     size_t weights_bytes;
     std::vector<int> layer_first, layer_last;   // op index range per planning node
     std::vector<int> layer_out;                 // tensor leaving each node
+    std::vector<std::vector<int>> cross;        // per cut j (after node j): node outputs of nodes <= j
+                                                // that nodes > j read, ascending tensor id
     std::vector<size_t> offset;                 // workspace offset per tensor (SIZE_MAX: not in ws)
     size_t ws_bytes;
     // measurement (timing slots: ops, then encode / decode per cut): each kernel launched
@@ -202,10 +204,18 @@ int model_profile_impl(const mopar_model_s* m, mopar_layer_profile* out, double 
             mb = std::fmax(mb, sm);
             tb = tb + mt;
         }
-        const auto& t = m->tensors[m->layer_out[l]];
         out[l].mem_bytes = std::fmax(mc, mb);
         out[l].time_s = tc + tb;
-        out[l].out_bytes = static_cast<double>(numel(t) * static_cast<int64_t>(elt_bytes(t.dtype)));
+        // bytes a cut after this node moves: every tensor crossing it (the parallel edges of
+        // Sec. III-C's edge elimination merged, sizes summed in tensor-id order)
+        double ob = 0.0;
+        if (l + 1 < m->n_layers) {
+            for (int t : m->cross[l]) ob = ob + static_cast<double>(numel(m->tensors[t]) * static_cast<int64_t>(elt_bytes(m->tensors[t].dtype)));
+        } else {
+            const auto& t = m->tensors[m->layer_out[l]];
+            ob = static_cast<double>(numel(t) * static_cast<int64_t>(elt_bytes(t.dtype)));
+        }
+        out[l].out_bytes = ob;
         out[l].rd_width = rdw;
         out[l].reserved = 0;
     }
@@ -285,9 +295,11 @@ static int validate_and_build(mopar_model_s& m) {
             if (t == m.input) {
                 if (op.layer != 0) return set_error(MOPAR_E_ARG, nm + ": only node 0 may read the model input");
             } else {
+                // tensors of its own node, or the output of any earlier node (skip edges
+                // make a cut carry several tensors)
                 const int pl = m.ops[producer[t]].layer;
-                if (pl != op.layer && !(pl == op.layer - 1 && t == m.ops[m.layer_last[pl]].out))
-                    return set_error(MOPAR_E_ARG, nm + ": reads a tensor that does not cross the node boundary");
+                if (pl != op.layer && !(pl < op.layer && t == m.ops[m.layer_last[pl]].out))
+                    return set_error(MOPAR_E_ARG, nm + ": reads a tensor that is neither its node's nor an earlier node's output");
             }
         }
         if (op.in1 >= 0 && op.kind != MOPAR_OP_CONV && op.kind != MOPAR_OP_LINEAR && op.kind != MOPAR_OP_LAYERNORM)
@@ -432,6 +444,20 @@ static int validate_and_build(mopar_model_s& m) {
         return set_error(MOPAR_E_ARG, "model: the output must be produced by the last op");
     m.layer_out.resize(m.n_layers);
     for (int l = 0; l < m.n_layers; ++l) m.layer_out[l] = m.ops[m.layer_last[l]].out;
+    // tensors crossing each cut: produced as the output of a node <= j, read by a node > j
+    m.cross.assign(m.n_layers > 1 ? m.n_layers - 1 : 0, {});
+    {
+        std::vector<int> last_reader_node(nt, -1), out_node(nt, -1);
+        for (int l = 0; l < m.n_layers; ++l) out_node[m.layer_out[l]] = l;
+        for (const auto& op : m.ops)
+            for (int t : {op.in0, op.in1})
+                if (t >= 0) last_reader_node[t] = std::max(last_reader_node[t], op.layer);
+        for (int t = 0; t < nt; ++t)
+            if (out_node[t] >= 0)
+                for (int j = out_node[t]; j < last_reader_node[t] && j + 1 < m.n_layers; ++j) m.cross[j].push_back(t);
+        for (int j = 0; j + 1 < m.n_layers; ++j)
+            if (m.cross[j].empty()) return set_error(MOPAR_E_ARG, "model: nothing crosses the cut after node " + std::to_string(j));
+    }
 
     // workspace: every tensor except the model input and output gets a slot, live from
     // its producer to its last reader; op scratch lives for its op.  First-fit reuse.
@@ -908,50 +934,64 @@ int model_forward_impl(const mopar_model_s* m, const mopar_plan* p, const mopar_
         return set_error(MOPAR_E_WORKSPACE, "mopar_model_forward: workspace smaller than mopar_model_workspace_bytes");
     const int S = p->n_slices;
     if (S > 1 && (!codecs || !code_bufs)) return set_error(MOPAR_E_ARG, "mopar_model_forward: codecs / code buffers");
-    // validate every codec against its boundary before enqueuing anything
+    // boundary b: the tensors crossing cut 0, then cut 1, ... (ascending tensor id within a cut);
+    // validate every codec against its tensor before enqueuing anything
+    std::vector<int> base(S, 0);
     for (int s = 0; s + 1 < S; ++s) {
-        const auto& t = m->tensors[m->layer_out[p->slice_end[s]]];
-        int64_t pos;
-        int ch;
-        rc = codec_geometry(&codecs[s], &t, &pos, &ch, "mopar_model_forward");
-        if (rc) return rc;
-        if (!code_bufs[s]) return set_error(MOPAR_E_ARG, "mopar_model_forward: null code buffer");
+        const auto& cr = m->cross[p->slice_end[s]];
+        base[s + 1] = base[s] + static_cast<int>(cr.size());
+        for (size_t q = 0; q < cr.size(); ++q) {
+            int64_t pos;
+            int ch;
+            rc = codec_geometry(&codecs[base[s] + q], &m->tensors[cr[q]], &pos, &ch, "mopar_model_forward");
+            if (rc) return rc;
+            if (!code_bufs[base[s] + q]) return set_error(MOPAR_E_ARG, "mopar_model_forward: null code buffer");
+        }
     }
     const hipStream_t st = static_cast<hipStream_t>(stream);
     Ptrs P{m, static_cast<unsigned char*>(ws), in, m->input, out, m->output};
     reset_timing(*m);
     const int slot0 = static_cast<int>(m->ops.size());
+    // encode (to = true) or decode every tensor crossing the cut after slice c
+    auto hand_off = [&](int c, bool enc) -> hipError_t {
+        const auto& cr = m->cross[p->slice_end[c]];
+        for (size_t q = 0; q < cr.size(); ++q) {
+            const auto& t = m->tensors[cr[q]];
+            const int b = base[c] + static_cast<int>(q);
+            int64_t pos;
+            int ch;
+            codec_geometry(&codecs[b], &t, &pos, &ch, "mopar_model_forward");
+            const hipError_t e = enc ? codec_apply(codecs[b], t.dtype, pos, ch, P.get(cr[q]), code_bufs[b], true, st)
+                                     : codec_apply(codecs[b], t.dtype, pos, ch, code_bufs[b], P.get(cr[q]), false, st);
+            if (e != hipSuccess) return e;
+        }
+        return hipSuccess;
+    };
     int l0 = 0;
     for (int s = 0; s < S; ++s) {
         const int l1 = p->slice_end[s];
-        if (s > 0) {   // decode the previous boundary into this slice's input
-            const int bt = m->layer_out[l0 - 1];
-            const auto& t = m->tensors[bt];
-            int64_t pos;
-            int ch;
-            codec_geometry(&codecs[s - 1], &t, &pos, &ch, "mopar_model_forward");
-            rc = hip_check(timed(*m, slot0 + 2 * (s - 1) + 1, st,
-                                 [&] { return codec_apply(codecs[s - 1], t.dtype, pos, ch, code_bufs[s - 1], P.get(bt),
-                                                          false, st); }),
+        if (s > 0) {   // decode the previous boundary into this slice's inputs
+            rc = hip_check(timed(*m, slot0 + 2 * (s - 1) + 1, st, [&] { return hand_off(s - 1, false); }),
                            "boundary decode");
             if (rc) return rc;
         }
         rc = run_layers(*m, *p, l0, l1, P, st);
         if (rc) return rc;
-        if (s + 1 < S) {   // encode this slice's output into the boundary buffer
-            const int bt = m->layer_out[l1];
-            const auto& t = m->tensors[bt];
-            int64_t pos;
-            int ch;
-            codec_geometry(&codecs[s], &t, &pos, &ch, "mopar_model_forward");
-            rc = hip_check(timed(*m, slot0 + 2 * s, st,
-                                 [&] { return codec_apply(codecs[s], t.dtype, pos, ch, P.get(bt), code_bufs[s], true,
-                                                          st); }),
-                           "boundary encode");
+        if (s + 1 < S) {   // encode this slice's outputs into the boundary buffers
+            rc = hip_check(timed(*m, slot0 + 2 * s, st, [&] { return hand_off(s, true); }), "boundary encode");
             if (rc) return rc;
         }
         l0 = l1 + 1;
     }
+    return MOPAR_OK;
+}
+
+int cut_tensors_impl(const mopar_model_s* m, int32_t node, int32_t* tids, int32_t cap, int32_t* count) {
+    if (!m || !count || (cap > 0 && !tids)) return set_error(MOPAR_E_ARG, "mopar_model_cut_tensors: null argument");
+    if (node < 0 || node + 1 >= m->n_layers) return set_error(MOPAR_E_ARG, "mopar_model_cut_tensors: node out of range");
+    const auto& cr = m->cross[node];
+    *count = static_cast<int32_t>(cr.size());
+    for (int32_t i = 0; i < cap && i < *count; ++i) tids[i] = cr[i];
     return MOPAR_OK;
 }
 
@@ -969,7 +1009,9 @@ struct mopar_pipeline_s {
     int S = 0, depth = 0, replicas = 0;
     std::vector<hipStream_t> streams;              // [replicas][S]
     std::vector<unsigned char*> ws;                // [replicas][S], one model workspace each
-    std::vector<void*> codes;                      // [replicas][depth][S-1]
+    std::vector<int> base;                         // first boundary tensor of each cut
+    int nb = 0;                                    // boundary tensors over all cuts
+    std::vector<void*> codes;                      // [replicas][depth][nb]
     std::vector<hipEvent_t> enc_done, dec_done;    // [replicas][depth][S-1]
     int64_t submitted = 0;
     ~mopar_pipeline_s() {
@@ -1006,14 +1048,22 @@ int pipeline_create_impl(const mopar_model_s* m, const mopar_plan* p, const mopa
     if (need && (!ws || ws_bytes < need))
         return set_error(MOPAR_E_WORKSPACE, "mopar_pipeline_create: workspace smaller than mopar_pipeline_workspace_bytes");
     if (S > 1 && (!codecs || !code_bufs)) return set_error(MOPAR_E_ARG, "mopar_pipeline_create: codecs / code buffers");
+    std::vector<int> base(S > 1 ? S - 1 : 0, 0);
+    int nb = 0;
     for (int c = 0; c + 1 < S; ++c) {
-        const auto& t = m->tensors[m->layer_out[p->slice_end[c]]];
-        int64_t pos;
-        int ch;
-        rc = codec_geometry(&codecs[c], &t, &pos, &ch, "mopar_pipeline_create");
-        if (rc) return rc;
-        for (int q = 0; q < replicas * depth; ++q)
-            if (!code_bufs[q * (S - 1) + c]) return set_error(MOPAR_E_ARG, "mopar_pipeline_create: null code buffer");
+        base[c] = nb;
+        nb += static_cast<int>(m->cross[p->slice_end[c]].size());
+    }
+    for (int c = 0; c + 1 < S; ++c) {
+        const auto& cr = m->cross[p->slice_end[c]];
+        for (size_t q = 0; q < cr.size(); ++q) {
+            int64_t pos;
+            int ch;
+            rc = codec_geometry(&codecs[base[c] + q], &m->tensors[cr[q]], &pos, &ch, "mopar_pipeline_create");
+            if (rc) return rc;
+            for (int r = 0; r < replicas * depth; ++r)
+                if (!code_bufs[r * nb + base[c] + q]) return set_error(MOPAR_E_ARG, "mopar_pipeline_create: null code buffer");
+        }
     }
     auto* pp = new mopar_pipeline_s();
     pp->m = m;
@@ -1022,7 +1072,9 @@ int pipeline_create_impl(const mopar_model_s* m, const mopar_plan* p, const mopa
     pp->plan = *p;
     pp->plan.slice_end = pp->slice_end.data();
     pp->plan.k = pp->k.data();
-    if (S > 1) pp->codecs.assign(codecs, codecs + S - 1);
+    if (S > 1) pp->codecs.assign(codecs, codecs + nb);
+    pp->base = base;
+    pp->nb = nb;
     pp->S = S;
     pp->depth = depth;
     pp->replicas = replicas;
@@ -1031,8 +1083,8 @@ int pipeline_create_impl(const mopar_model_s* m, const mopar_plan* p, const mopa
         pp->ws.push_back(static_cast<unsigned char*>(ws) + slice_ws_stride(m) * static_cast<size_t>(i));
     }
     const int ncut = S - 1;
+    for (int i = 0; i < replicas * depth * nb; ++i) pp->codes.push_back(code_bufs[i]);
     for (int i = 0; i < replicas * depth * ncut; ++i) {
-        pp->codes.push_back(code_bufs[i]);
         hipEvent_t a, b;
         rc = hip_check(hipEventCreateWithFlags(&a, hipEventDisableTiming), "hipEventCreateWithFlags");
         if (rc) {
@@ -1066,17 +1118,27 @@ int pipeline_submit_impl(mopar_pipeline_s* pp, const void* in, void* out) {
         // slice s reads its input from the caller (s = 0) or from its own workspace (decoded)
         Ptrs P{&m, pp->ws[rep * S + s], in, s == 0 ? m.input : -1, out, s == S - 1 ? m.output : -1};
         int rc;
+        // encode / decode every tensor crossing cut c with its own codec and ring buffer
+        auto hand_off = [&](int c, bool enc) -> hipError_t {
+            const auto& cr = m.cross[pp->slice_end[c]];
+            for (size_t q = 0; q < cr.size(); ++q) {
+                const auto& t = m.tensors[cr[q]];
+                const int b = pp->base[c] + static_cast<int>(q);
+                int64_t pos;
+                int ch;
+                codec_geometry(&pp->codecs[b], &t, &pos, &ch, "mopar_pipeline_submit");
+                void* code = pp->codes[static_cast<size_t>(r) * pp->nb + b];
+                const hipError_t e = enc ? codec_apply(pp->codecs[b], t.dtype, pos, ch, P.get(cr[q]), code, true, st)
+                                         : codec_apply(pp->codecs[b], t.dtype, pos, ch, code, P.get(cr[q]), false, st);
+                if (e != hipSuccess) return e;
+            }
+            return hipSuccess;
+        };
         if (s > 0) {
             const int c = s - 1, slot = r * ncut + c;
-            const int bt = m.layer_out[l0 - 1];
-            const auto& t = m.tensors[bt];
-            int64_t pos;
-            int ch;
-            codec_geometry(&pp->codecs[c], &t, &pos, &ch, "mopar_pipeline_submit");
             rc = hip_check(hipStreamWaitEvent(st, pp->enc_done[slot], 0), "hipStreamWaitEvent");
             if (rc) return rc;
-            rc = hip_check(codec_apply(pp->codecs[c], t.dtype, pos, ch, pp->codes[slot], P.get(bt), false, st),
-                           "boundary decode");
+            rc = hip_check(hand_off(c, false), "boundary decode");
             if (rc) return rc;
             rc = hip_check(hipEventRecord(pp->dec_done[slot], st), "hipEventRecord");
             if (rc) return rc;
@@ -1089,16 +1151,10 @@ int pipeline_submit_impl(mopar_pipeline_s* pp, const void* in, void* out) {
             }
         if (s < S - 1) {
             const int c = s, slot = r * ncut + c;
-            const int bt = m.layer_out[l1];
-            const auto& t = m.tensors[bt];
-            int64_t pos;
-            int ch;
-            codec_geometry(&pp->codecs[c], &t, &pos, &ch, "mopar_pipeline_submit");
             // the slot is free once the previous batch using it has been decoded
             rc = hip_check(hipStreamWaitEvent(st, pp->dec_done[slot], 0), "hipStreamWaitEvent");
             if (rc) return rc;
-            rc = hip_check(codec_apply(pp->codecs[c], t.dtype, pos, ch, P.get(bt), pp->codes[slot], true, st),
-                           "boundary encode");
+            rc = hip_check(hand_off(c, true), "boundary encode");
             if (rc) return rc;
             rc = hip_check(hipEventRecord(pp->enc_done[slot], st), "hipEventRecord");
             if (rc) return rc;

@@ -412,8 +412,36 @@ def inception_mini(batch=2, hw=32, k_rd=2, seed=1006, dtype=BF16):
     return bld.finish(y, n_slices=3, k_by_layer=k_by_layer)
 
 
-BUILDERS = {1: tiny_vgg, 2: resnet50, 3: vgg16, 4: bert_base, 5: lstm_lm, 6: inception_mini}
-NAMES = {1: "tiny_vgg", 2: "resnet50", 3: "vgg16", 4: "bert_base", 5: "lstm_lm", 6: "inception_mini"}
+
+
+def skipnet_mini(batch=2, hw=16, k_rd=2, seed=1007, dtype=BF16):
+    """Small CNN with skip edges across planning nodes (U-Net / DenseNet style): node 3
+    adds the stem's output as a residual and node 4 concatenates node 1's output, so
+    the cuts after nodes 0-3 carry one, two, three and two tensors."""
+    bld = _Builder("skipnet_mini", dtype, batch, seed, cfg=7)
+    x = bld.tensor((batch, 3, hw, hw), F32)
+    bld.new_layer("stem")
+    x0 = bld.conv(x, 16, 3, 1, 1, "relu", "stem", bn_fold=True)
+    bld.new_layer("c1")
+    x1 = bld.conv(x0, 16, 3, 1, 1, "relu", "c1", bn_fold=True)
+    bld.new_layer("c2")
+    x2 = bld.conv(x1, 16, 3, 1, 1, "relu", "c2", bn_fold=True, rd=True)
+    rd_layer = bld.layer
+    bld.new_layer("c3")
+    x3 = bld.conv(x2, 16, 3, 1, 1, "relu", "c3", res=x0, bn_fold=True)
+    bld.new_layer("cat")
+    n, _, h, w = bld.shape(x3)
+    cat = bld.tensor((n, 32, h, w))
+    bld.conv(x3, 16, 1, 1, 0, "relu", "cat.a", bn_fold=True, branch=1, pos=1, into=(cat, 0))
+    bld.conv(x1, 16, 1, 1, 0, "relu", "cat.b", bn_fold=True, branch=2, pos=1, into=(cat, 16))
+    bld.new_layer("head")
+    y = bld.linear(bld.avgpool(cat, "gap"), 10, "none", "fc", "he")
+    return bld.finish(y, n_slices=3, k_by_layer={rd_layer: k_rd})
+
+
+BUILDERS = {1: tiny_vgg, 2: resnet50, 3: vgg16, 4: bert_base, 5: lstm_lm, 6: inception_mini, 7: skipnet_mini}
+NAMES = {1: "tiny_vgg", 2: "resnet50", 3: "vgg16", 4: "bert_base", 5: "lstm_lm", 6: "inception_mini",
+         7: "skipnet_mini"}
 
 
 def build(cfg: int, **kw) -> Model:
@@ -439,18 +467,28 @@ def boundary_channels(model: Model, layer: int) -> int:
     return t["shape"][1] if len(t["shape"]) == 4 else t["shape"][-1]
 
 
-def make_codec_weights(model: Model, cut_layers, ratio: int = 8, seed: int | None = None):
-    """Autoencoder weights for each cut: W_e ~ N(0, 1/C) [C_e][C], W_d ~ N(0, 1/C_e) [C][C_e], biases 0.
+def tensor_channels(model: Model, tid: int) -> int:
+    """Channel (images) or feature (sequences) count of tensor ``tid``."""
+    s = model.tensors[tid]["shape"]
+    return s[1] if len(s) == 4 else s[-1]
 
-    ``ratio`` may be an int or a list (one per cut).  Returns a list of dicts
-    with keys c, c_code, w_enc, b_enc, w_dec, b_dec (float32, model-dtype values).
+
+def make_codec_weights(model: Model, cut_layers, ratio: int = 8, seed: int | None = None, tensors=None):
+    """Autoencoder weights for each boundary: W_e ~ N(0, 1/C) [C_e][C], W_d ~ N(0, 1/C_e) [C][C_e], biases 0.
+
+    One set per cut (for the tensor leaving that node), or, when ``tensors`` lists
+    the boundary tensor ids (several per cut where skip edges cross it), one per
+    tensor in that order.  ``ratio`` may be an int or a list (one per boundary).
+    Returns a list of dicts with keys c, c_code, w_enc, b_enc, w_dec, b_dec
+    (float32, model-dtype values).
     """
     seed = 3000 + model.cfg if seed is None else seed
     rng = np.random.Generator(np.random.PCG64(seed))
-    ratios = ratio if isinstance(ratio, (list, tuple)) else [ratio] * len(cut_layers)
+    chans = ([tensor_channels(model, t) for t in tensors] if tensors is not None
+             else [boundary_channels(model, layer) for layer in cut_layers])
+    ratios = ratio if isinstance(ratio, (list, tuple)) else [ratio] * len(chans)
     out = []
-    for layer, r in zip(cut_layers, ratios):
-        c = boundary_channels(model, layer)
+    for c, r in zip(chans, ratios):
         if c % r:
             raise ValueError(f"channels {c} not divisible by ratio {r}")
         ce = c // r

@@ -14,6 +14,7 @@ SMALL = {
     4: dict(batch=2, seq=40, layers=3, hidden=128, heads=2, ffn=256, vocab=300, max_pos=64, slice_every=1),
     5: dict(batch=3, seq=9, hidden=64, emb=64, vocab=301),
     6: dict(batch=3, hw=32),
+    7: dict(batch=3, hw=16),
 }
 
 
@@ -37,3 +38,18 @@ def codec_ratios(model, cuts):
         c = synth.boundary_channels(model, li)
         out.append(next((r for r in (8, 4, 2) if c % r == 0 and (c // r) % g == 0), 1))
     return out
+
+
+def boundary_codecs(model, cuts, kind="ae"):
+    """Boundary tensors of the cuts (every tensor crossing each cut, cut-major, ascending id)
+    and AE codec weights for each, at the largest ratio the granule allows."""
+    import oracle
+    tids = [t for c in cuts for t in oracle.crossing_tensors(model, c)]
+    g = 8 if model.dtype == "bf16" else 4
+    ratios = []
+    for t in tids:
+        c = synth.tensor_channels(model, t)
+        ratios.append(next((r for r in (8, 4, 2) if c % r == 0 and (c // r) % g == 0), 1))
+    if kind != "ae" or not tids:
+        return tids, None
+    return tids, synth.make_codec_weights(model, cuts, ratio=ratios, tensors=tids)

@@ -11,7 +11,7 @@ import torch
 
 import oracle
 import synth
-from tests.helpers import SMALL, TOL, codec_ratios, rel_err
+from tests.helpers import SMALL, TOL, boundary_codecs, codec_ratios, rel_err
 
 pytestmark = pytest.mark.gpu
 
@@ -287,7 +287,7 @@ def test_codec_errors_enqueue_nothing():
 # whole models (shrunken workloads)
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6, 7])
 def test_small_model_sliced_ae_parity(cfg):
     m = synth.build(cfg, **SMALL[cfg])
     x = synth.make_input(m)
@@ -298,13 +298,14 @@ def test_small_model_sliced_ae_parity(cfg):
         n_slices=s["n_slices"], allowed_cut=s["allowed_cut"], elim_tau=s["elim_tau"], k_override=s["k_override"]))
     assert (plan.slice_end, plan.k) == (po.slice_end, po.k)
     cuts = plan.slice_end[:-1]
-    cw = synth.make_codec_weights(m, cuts, ratio=codec_ratios(m, cuts))
+    tids, cw = boundary_codecs(m, cuts)
+    assert tids == sm.boundary_tensors(plan)
     ref = oracle.forward(m, x, k=plan.k, cuts=cuts, codecs=cw)
     y, _, _ = run_gpu(m, x, plan, "ae", cw)
     assert rel_err(_np(y), ref) <= TOL[m.dtype]
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6, 7])
 def test_small_model_raw_slicing_and_subslicing_bitwise(cfg):
     m = synth.build(cfg, **SMALL[cfg])
     x = synth.make_input(m)

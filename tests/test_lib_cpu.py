@@ -96,7 +96,7 @@ def test_planner_error_paths():
     assert P.mopar_plan_slices(prof, n_slices=2).slice_end == [0, 1]
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6, 7])
 def test_model_profile_and_plan_equal_oracle(cfg):
     kw = {} if cfg != 3 else dict(batch=2, hw=64)
     m = synth.build(cfg, **kw)

@@ -104,10 +104,11 @@ SMALL = {
     4: dict(batch=2, seq=16, layers=2, hidden=64, heads=2, ffn=128, vocab=100, max_pos=32, slice_every=1),
     5: dict(batch=2, seq=6, hidden=32, emb=24, vocab=50),
     6: dict(batch=2, hw=16),
+    7: dict(batch=2, hw=8),
 }
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6, 7])
 def test_oracle_model_matches_torch_library_forward(cfg):
     m = synth.build(cfg, **SMALL[cfg])
     x = synth.make_input(m)
