@@ -184,6 +184,11 @@ __device__ __forceinline__ u32x4 lds_read16(unsigned addr) {
     return v;
 }
 __device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+template <int N>
+__device__ __forceinline__ void lds_wait_until() {
+    static_assert(N >= 0 && N <= 15, "lgkmcnt range");
+    asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+}
 __device__ __forceinline__ void pin(u32x4& v) { asm volatile("" : "+v"(v)); }
 
 // wait until at most `r` of this wave's stages (L loads each) are still in flight
@@ -455,14 +460,17 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const GemmParams p) 
         }
         const unsigned sbase = buf * STAGE * 16;
         u32x4 a0[FM], b0[FN], a1[FM], b1[FN];
+        // both k steps' fragment reads go out together; LDS reads complete in order, so once
+        // at most FM + FN are outstanding the first step's have landed and its MFMAs start
         read_frags(sbase, 0, a0, b0);
-        lds_wait();
+        read_frags(sbase, 1, a1, b1);
+        lds_wait_until<FM + FN>();
 #pragma unroll
         for (int a = 0; a < FM; ++a) pin(a0[a]);
 #pragma unroll
         for (int b = 0; b < FN; ++b) pin(b0[b]);
-        read_frags(sbase, 1, a1, b1);                  // second k step loads under the first's MFMAs
         mfmas(a0, b0);
+        __builtin_amdgcn_sched_barrier(0);             // keep these MFMAs ahead of the next wait
         lds_wait();
 #pragma unroll
         for (int a = 0; a < FM; ++a) pin(a1[a]);
