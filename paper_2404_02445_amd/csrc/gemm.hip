@@ -460,17 +460,30 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const GemmParams p) 
         }
         const unsigned sbase = buf * STAGE * 16;
         u32x4 a0[FM], b0[FN], a1[FM], b1[FN];
-        // both k steps' fragment reads go out together; LDS reads complete in order, so once
-        // at most FM + FN are outstanding the first step's have landed and its MFMAs start
-        read_frags(sbase, 0, a0, b0);
-        read_frags(sbase, 1, a1, b1);
-        lds_wait_until<FM + FN>();
+        if constexpr (FM + FN <= 3) {
+            // thin wave tiles: both k steps' fragment reads go out together; LDS reads complete
+            // in order, so once at most FM + FN are outstanding the first step's have landed
+            read_frags(sbase, 0, a0, b0);
+            read_frags(sbase, 1, a1, b1);
+            lds_wait_until<FM + FN>();
 #pragma unroll
-        for (int a = 0; a < FM; ++a) pin(a0[a]);
+            for (int a = 0; a < FM; ++a) pin(a0[a]);
 #pragma unroll
-        for (int b = 0; b < FN; ++b) pin(b0[b]);
-        mfmas(a0, b0);
-        __builtin_amdgcn_sched_barrier(0);             // keep these MFMAs ahead of the next wait
+            for (int b = 0; b < FN; ++b) pin(b0[b]);
+            mfmas(a0, b0);
+            __builtin_amdgcn_sched_barrier(0);         // keep these MFMAs ahead of the next wait
+        } else {
+            // wide wave tiles: holding both steps' fragments would cost the registers that
+            // keep two blocks per CU resident; the second step's reads follow the first's wait
+            read_frags(sbase, 0, a0, b0);
+            lds_wait();
+#pragma unroll
+            for (int a = 0; a < FM; ++a) pin(a0[a]);
+#pragma unroll
+            for (int b = 0; b < FN; ++b) pin(b0[b]);
+            read_frags(sbase, 1, a1, b1);
+            mfmas(a0, b0);
+        }
         lds_wait();
 #pragma unroll
         for (int a = 0; a < FM; ++a) pin(a1[a]);
