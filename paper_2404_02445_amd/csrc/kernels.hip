@@ -381,11 +381,138 @@ __global__ __launch_bounds__(ATT_MAXS) void attention_kernel(const T* __restrict
     for (int e = 0; e < ATT_D; ++e) yr[e] = from_f<T>(o[e] * inv);
 }
 
+// ---------------------------------------------------------------------------
+// bf16 attention on the matrix cores.  One block per (batch, head, 64-query
+// tile), four waves of 16 query rows.  Q, K (row-major) and V (transposed,
+// [dim][key]) are staged in LDS with padded rows so the 16 lanes of an MFMA
+// fragment hit distinct banks.  S = Q K^T accumulates in fp32
+// (v_mfma_f32_16x16x32_bf16, key fragment first so each lane holds four
+// consecutive keys of one query row); the row max and sum are butterflies over
+// the four lanes that share a row; P = exp(scale * (S - max)) goes to LDS as
+// bf16 and O = P V runs on the matrix cores again; O is divided by the row sum
+// in fp32 and stored.  Keys past seq are masked to -inf (zero K / V rows),
+// queries past seq are computed on zero rows and not stored.
+// ---------------------------------------------------------------------------
+constexpr int AM_Q = 64, AM_K = 128, AM_D = 64;
+constexpr int AM_LD = AM_D + 8;     // bf16 row stride of Q and K (144 bytes)
+constexpr int AM_LP = AM_K + 8;     // bf16 row stride of V^T and P (272 bytes)
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ bf16x8_t lds8(const __bf16* p) { return *reinterpret_cast<const bf16x8_t*>(p); }
+
+__global__ __launch_bounds__(256) void attention_mfma_kernel(const __bf16* __restrict__ qkv, __bf16* __restrict__ y,
+                                                             int seq, int heads, float scale) {
+    __shared__ __attribute__((aligned(16))) __bf16 sq[AM_Q * AM_LD];
+    __shared__ __attribute__((aligned(16))) __bf16 sk[AM_K * AM_LD];
+    __shared__ __attribute__((aligned(16))) __bf16 svt[AM_D * AM_LP];
+    __shared__ __attribute__((aligned(16))) __bf16 sp[4 * 16 * AM_LP];
+    const int qtiles = (seq + AM_Q - 1) / AM_Q;
+    const int qt = blockIdx.x % qtiles, bh = blockIdx.x / qtiles;
+    const int b = bh / heads, h = bh % heads;
+    const int f = heads * AM_D;
+    const int64_t row3 = 3 * static_cast<int64_t>(f);
+    const __bf16* base = qkv + static_cast<int64_t>(b) * seq * row3 + h * AM_D;
+    const int q0 = qt * AM_Q;
+    const int kpad = (seq + 31) / 32 * 32;          // keys processed (multiple of the k step)
+    const uint4 zero4 = make_uint4(0, 0, 0, 0);
+    // stage: 8 chunks of 8 dims per row
+    for (int i = threadIdx.x; i < AM_Q * 8; i += 256) {
+        const int r = i >> 3, c = i & 7, q = q0 + r;
+        const uint4 v = q < seq ? *reinterpret_cast<const uint4*>(base + q * row3 + c * 8) : zero4;
+        *reinterpret_cast<uint4*>(&sq[r * AM_LD + c * 8]) = v;
+    }
+    for (int i = threadIdx.x; i < kpad * 8; i += 256) {
+        const int r = i >> 3, c = i & 7;
+        uint4 kv = zero4, vv = zero4;
+        if (r < seq) {
+            kv = *reinterpret_cast<const uint4*>(base + r * row3 + f + c * 8);
+            vv = *reinterpret_cast<const uint4*>(base + r * row3 + 2 * f + c * 8);
+        }
+        *reinterpret_cast<uint4*>(&sk[r * AM_LD + c * 8]) = kv;
+        const __bf16* ve = reinterpret_cast<const __bf16*>(&vv);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) svt[(c * 8 + e) * AM_LP + r] = ve[e];
+    }
+    __syncthreads();
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lr = lane & 15, lg = lane >> 4;          // fragment row, k group
+    const int ntile = kpad / 16;
+    // S = Q K^T for query rows wave*16 .. +15
+    f32x4_t sacc[AM_K / 16];
+#pragma unroll
+    for (int t = 0; t < AM_K / 16; ++t) sacc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < AM_D / 32; ++ks) {
+        const bf16x8_t qa = lds8(&sq[(wave * 16 + lr) * AM_LD + ks * 32 + lg * 8]);
+#pragma unroll
+        for (int t = 0; t < AM_K / 16; ++t)
+            if (t < ntile) {
+                const bf16x8_t kb = lds8(&sk[(t * 16 + lr) * AM_LD + ks * 32 + lg * 8]);
+                sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb, qa, sacc[t], 0, 0, 0);
+            }
+    }
+    // softmax over the keys of row lr: this lane holds keys 16 t + 4 lg + e
+    float mx = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < AM_K / 16; ++t)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int key = t * 16 + lg * 4 + e;
+            if (t >= ntile || key >= seq) sacc[t][e] = -INFINITY;
+            mx = fmaxf(mx, sacc[t][e]);
+        }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    float sum = 0.0f;
+    __bf16* prow = &sp[(wave * 16 + lr) * AM_LP];
+#pragma unroll
+    for (int t = 0; t < AM_K / 16; ++t) {
+        if (t >= ntile) continue;
+        float pe[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            pe[e] = sacc[t][e] == -INFINITY ? 0.0f : __expf(scale * (sacc[t][e] - mx));
+            sum += pe[e];
+        }
+        const __bf16 pb[4] = {(__bf16)pe[0], (__bf16)pe[1], (__bf16)pe[2], (__bf16)pe[3]};
+        *reinterpret_cast<uint2*>(&prow[t * 16 + lg * 4]) = *reinterpret_cast<const uint2*>(pb);
+    }
+    sum += __shfl_xor(sum, 16, 64);
+    sum += __shfl_xor(sum, 32, 64);
+    __syncthreads();                                   // P rows written before their fragment reads
+    // O = P V: dims 16 dt + 4 lg + e of row lr
+    f32x4_t oacc[AM_D / 16];
+#pragma unroll
+    for (int dt = 0; dt < AM_D / 16; ++dt) oacc[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int ks = 0; ks < kpad / 32; ++ks) {
+        const bf16x8_t pa = lds8(&sp[(wave * 16 + lr) * AM_LP + ks * 32 + lg * 8]);
+#pragma unroll
+        for (int dt = 0; dt < AM_D / 16; ++dt) {
+            const bf16x8_t vb = lds8(&svt[(dt * 16 + lr) * AM_LP + ks * 32 + lg * 8]);
+            oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb, pa, oacc[dt], 0, 0, 0);
+        }
+    }
+    const int q = q0 + wave * 16 + lr;
+    if (q >= seq) return;
+    const float inv = 1.0f / sum;
+    __bf16* out = y + (static_cast<int64_t>(b) * seq + q) * f + h * AM_D;
+#pragma unroll
+    for (int dt = 0; dt < AM_D / 16; ++dt) {
+        const __bf16 ob[4] = {(__bf16)(oacc[dt][0] * inv), (__bf16)(oacc[dt][1] * inv), (__bf16)(oacc[dt][2] * inv),
+                              (__bf16)(oacc[dt][3] * inv)};
+        *reinterpret_cast<uint2*>(out + dt * 16 + lg * 4) = *reinterpret_cast<const uint2*>(ob);
+    }
+}
+
 hipError_t launch_attention(const void* qkv, void* y, int batch, int seq, int heads, float scale, int dtype,
                             hipStream_t s) {
+    if (seq < 1 || seq > AM_K) return hipErrorInvalidValue;
     if (dtype == MOPAR_BF16)
-        launch_kernel(attention_kernel<__bf16>, dim3(batch * heads), dim3(ATT_MAXS), 0, s,
-                           static_cast<const __bf16*>(qkv), static_cast<__bf16*>(y), seq, heads, scale);
+        launch_kernel(attention_mfma_kernel, dim3(batch * heads * ((seq + AM_Q - 1) / AM_Q)), dim3(256), 0, s,
+                      static_cast<const __bf16*>(qkv), static_cast<__bf16*>(y), seq, heads, scale);
     else
         launch_kernel(attention_kernel<float>, dim3(batch * heads), dim3(ATT_MAXS), 0, s,
                            static_cast<const float*>(qkv), static_cast<float*>(y), seq, heads, scale);

@@ -182,14 +182,17 @@ def test_layernorm_with_residual():
     assert rel_err(_np(y1), oracle.forward(m, ids)) <= TOL["bf16"]
 
 
-@pytest.mark.parametrize("seq,heads", [(128, 12), (37, 2)])
-def test_attention(seq, heads):
-    bld, x = seq_input_model("bf16", 2, seq, 3 * 64 * heads, scale=1.5)
+@pytest.mark.parametrize("dt,seq,heads", [("bf16", 128, 12), ("bf16", 37, 2), ("bf16", 1, 1), ("bf16", 64, 3),
+                                           ("bf16", 65, 2), ("bf16", 100, 4), ("f32", 40, 2)])
+def test_attention(dt, seq, heads):
+    # bf16 runs on the matrix cores (64-query tiles, keys padded to 32 and masked), f32 on
+    # the vector units; sequence lengths cover one key, whole and partial query tiles
+    bld, x = seq_input_model(dt, 2, seq, 3 * 64 * heads, scale=1.5)
     y = bld.attention(x, heads, "att")
     m = bld.finish(y, 1)
     ids = seq_ids(2, seq)
     y1, _, _ = run_gpu(m, ids, P.make_plan(1, [0], [1]))
-    assert rel_err(_np(y1), oracle.forward(m, ids)) <= TOL["bf16"]
+    assert rel_err(_np(y1), oracle.forward(m, ids)) <= TOL[dt]
 
 
 def test_embed_bert():
