@@ -209,62 +209,117 @@ hipError_t launch_avgpool(const void* x, void* y, int n, int hw, int c, int dtyp
 // ---------------------------------------------------------------------------
 // Layer norm over rows of F <= 64 * LN_MAXV elements: one wave per row, the
 // row held in registers, mean then centred variance by wave butterflies.
+// When F is a whole number of 16-byte chunks each lane holds whole chunks
+// (chunk lane + 64 j), read and written as vectors; otherwise element
+// lane + 64 i.
 // ---------------------------------------------------------------------------
 constexpr int LN_MAXV = 32;
 
-template <typename T>
+// column of register i of this lane
+template <typename T, bool VEC>
+__device__ __forceinline__ int ln_col(int lane, int i) {
+    constexpr int V = Vec<T>::N;
+    return VEC ? (lane + 64 * (i / V)) * V + i % V : lane + 64 * i;
+}
+
+template <typename T, bool VEC>
 __device__ __forceinline__ void ln_row(float (&v)[LN_MAXV], int f, int lane, const T* g, const T* b, float eps,
                                        T* out) {
+    constexpr int V = Vec<T>::N;
     float s = 0.0f;
 #pragma unroll
     for (int i = 0; i < LN_MAXV; ++i)
-        if (lane + i * 64 < f) s += v[i];
+        if (ln_col<T, VEC>(lane, i) < f) s += v[i];
     const float mean = wave_sum(s) / static_cast<float>(f);
     float q = 0.0f;
 #pragma unroll
     for (int i = 0; i < LN_MAXV; ++i)
-        if (lane + i * 64 < f) {
+        if (ln_col<T, VEC>(lane, i) < f) {
             const float d = v[i] - mean;
             q += d * d;
         }
     const float var = wave_sum(q) / static_cast<float>(f);
     const float inv = 1.0f / sqrtf(var + eps);
+    if constexpr (VEC) {
 #pragma unroll
-    for (int i = 0; i < LN_MAXV; ++i) {
-        const int col = lane + i * 64;
-        if (col < f) out[col] = from_f<T>((v[i] - mean) * inv * to_f(g[col]) + to_f(b[col]));
+        for (int j = 0; j < LN_MAXV / V; ++j) {
+            const int c0 = (lane + 64 * j) * V;
+            if (c0 >= f) continue;
+            const uint4 gr = *reinterpret_cast<const uint4*>(g + c0), br = *reinterpret_cast<const uint4*>(b + c0);
+            const T* ge = reinterpret_cast<const T*>(&gr);
+            const T* be = reinterpret_cast<const T*>(&br);
+            uint4 o;
+            T* oe = reinterpret_cast<T*>(&o);
+#pragma unroll
+            for (int e = 0; e < V; ++e) oe[e] = from_f<T>((v[j * V + e] - mean) * inv * to_f(ge[e]) + to_f(be[e]));
+            *reinterpret_cast<uint4*>(out + c0) = o;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < LN_MAXV; ++i) {
+            const int col = lane + i * 64;
+            if (col < f) out[col] = from_f<T>((v[i] - mean) * inv * to_f(g[col]) + to_f(b[col]));
+        }
     }
 }
 
-template <typename T>
+// v[i] = a[col] (+ c[col]) for this lane's columns (zeros past f)
+template <typename T, bool VEC>
+__device__ __forceinline__ void ln_load(const T* a, const T* c, int f, int lane, float (&v)[LN_MAXV]) {
+    constexpr int V = Vec<T>::N;
+    if constexpr (VEC) {
+#pragma unroll
+        for (int j = 0; j < LN_MAXV / V; ++j) {
+            const int c0 = (lane + 64 * j) * V;
+            uint4 ar = make_uint4(0, 0, 0, 0), cr = make_uint4(0, 0, 0, 0);
+            if (c0 < f) {
+                ar = *reinterpret_cast<const uint4*>(a + c0);
+                if (c) cr = *reinterpret_cast<const uint4*>(c + c0);
+            }
+            const T* ae = reinterpret_cast<const T*>(&ar);
+            const T* ce = reinterpret_cast<const T*>(&cr);
+#pragma unroll
+            for (int e = 0; e < V; ++e) v[j * V + e] = to_f(ae[e]) + (c ? to_f(ce[e]) : 0.0f);
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < LN_MAXV; ++i) {
+            const int col = lane + i * 64;
+            v[i] = col < f ? to_f(a[col]) + (c ? to_f(c[col]) : 0.0f) : 0.0f;
+        }
+    }
+}
+
+template <typename T, bool VEC>
 __global__ void layernorm_kernel(const T* __restrict__ x, const T* __restrict__ res, const T* __restrict__ g,
                                  const T* __restrict__ b, T* __restrict__ y, int64_t rows, int f, float eps) {
     const int lane = threadIdx.x & 63;
     const int64_t row = static_cast<int64_t>(blockIdx.x) * (blockDim.x / 64) + (threadIdx.x >> 6);
     if (row >= rows) return;
-    const T* xr = x + row * f;
-    const T* rr = res ? res + row * f : nullptr;
     float v[LN_MAXV];
-#pragma unroll
-    for (int i = 0; i < LN_MAXV; ++i) {
-        const int col = lane + i * 64;
-        v[i] = col < f ? to_f(xr[col]) + (rr ? to_f(rr[col]) : 0.0f) : 0.0f;
-    }
-    ln_row<T>(v, f, lane, g, b, eps, y + row * f);
+    ln_load<T, VEC>(x + row * f, res ? res + row * f : nullptr, f, lane, v);
+    ln_row<T, VEC>(v, f, lane, g, b, eps, y + row * f);
+}
+
+template <typename T>
+static void layernorm_launch(const void* x, const void* res, const void* g, const void* b, void* y, int64_t rows,
+                             int f, float eps, hipStream_t s) {
+    const T *xp = static_cast<const T*>(x), *rp = static_cast<const T*>(res);
+    const T *gp = static_cast<const T*>(g), *bp = static_cast<const T*>(b);
+    if (f % Vec<T>::N == 0)
+        launch_kernel(layernorm_kernel<T, true>, dim3(blocks_for(rows, 4)), dim3(256), 0, s, xp, rp, gp, bp,
+                      static_cast<T*>(y), rows, f, eps);
+    else
+        launch_kernel(layernorm_kernel<T, false>, dim3(blocks_for(rows, 4)), dim3(256), 0, s, xp, rp, gp, bp,
+                      static_cast<T*>(y), rows, f, eps);
 }
 
 hipError_t launch_layernorm(const void* x, const void* res, const void* g, const void* b, void* y, int64_t rows,
                             int f, float eps, int dtype, hipStream_t s) {
     if (dtype == MOPAR_BF16)
-        launch_kernel(layernorm_kernel<__bf16>, dim3(blocks_for(rows, 4)), dim3(256), 0, s,
-                           static_cast<const __bf16*>(x), static_cast<const __bf16*>(res),
-                           static_cast<const __bf16*>(g), static_cast<const __bf16*>(b), static_cast<__bf16*>(y),
-                           rows, f, eps);
+        layernorm_launch<__bf16>(x, res, g, b, y, rows, f, eps, s);
     else
-        launch_kernel(layernorm_kernel<float>, dim3(blocks_for(rows, 4)), dim3(256), 0, s,
-                           static_cast<const float*>(x), static_cast<const float*>(res),
-                           static_cast<const float*>(g), static_cast<const float*>(b), static_cast<float*>(y), rows,
-                           f, eps);
+        layernorm_launch<float>(x, res, g, b, y, rows, f, eps, s);
     return hipGetLastError();
 }
 
@@ -272,7 +327,7 @@ hipError_t launch_layernorm(const void* x, const void* res, const void* g, const
 // BERT embedding: v = tok[id] + pos[s] + type[0], then layer norm (one wave
 // per token).
 // ---------------------------------------------------------------------------
-template <typename T>
+template <typename T, bool VEC>
 __global__ void embed_bert_kernel(const int32_t* __restrict__ ids, const T* __restrict__ tok,
                                   const T* __restrict__ pos, const T* __restrict__ type, const T* __restrict__ g,
                                   const T* __restrict__ b, T* __restrict__ y, int64_t rows, int seq, int f,
@@ -284,12 +339,25 @@ __global__ void embed_bert_kernel(const int32_t* __restrict__ ids, const T* __re
     const T* tr = tok + static_cast<int64_t>(ids[row]) * f;
     const T* pr = pos + static_cast<int64_t>(sidx) * f;
     float v[LN_MAXV];
+    ln_load<T, VEC>(tr, pr, f, lane, v);
+    float t[LN_MAXV];
+    ln_load<T, VEC>(type, nullptr, f, lane, t);
 #pragma unroll
-    for (int i = 0; i < LN_MAXV; ++i) {
-        const int col = lane + i * 64;
-        v[i] = col < f ? (to_f(tr[col]) + to_f(pr[col])) + to_f(type[col]) : 0.0f;
-    }
-    ln_row<T>(v, f, lane, g, b, eps, y + row * f);
+    for (int i = 0; i < LN_MAXV; ++i) v[i] += t[i];
+    ln_row<T, VEC>(v, f, lane, g, b, eps, y + row * f);
+}
+
+template <typename T>
+static void embed_bert_launch(const int32_t* ids, const void* tok, const void* pos, const void* type, const void* g,
+                              const void* b, void* y, int64_t rows, int seq, int f, float eps, hipStream_t s) {
+    const T *tp = static_cast<const T*>(tok), *pp = static_cast<const T*>(pos), *yp = static_cast<const T*>(type);
+    const T *gp = static_cast<const T*>(g), *bp = static_cast<const T*>(b);
+    if (f % Vec<T>::N == 0)
+        launch_kernel(embed_bert_kernel<T, true>, dim3(blocks_for(rows, 4)), dim3(256), 0, s, ids, tp, pp, yp, gp,
+                      bp, static_cast<T*>(y), rows, seq, f, eps);
+    else
+        launch_kernel(embed_bert_kernel<T, false>, dim3(blocks_for(rows, 4)), dim3(256), 0, s, ids, tp, pp, yp, gp,
+                      bp, static_cast<T*>(y), rows, seq, f, eps);
 }
 
 hipError_t launch_embed_bert(const int32_t* ids, const void* tok, const void* pos, const void* type, const void* g,
@@ -297,15 +365,9 @@ hipError_t launch_embed_bert(const int32_t* ids, const void* tok, const void* po
                              hipStream_t s) {
     const int64_t rows = static_cast<int64_t>(batch) * seq;
     if (dtype == MOPAR_BF16)
-        launch_kernel(embed_bert_kernel<__bf16>, dim3(blocks_for(rows, 4)), dim3(256), 0, s, ids,
-                           static_cast<const __bf16*>(tok), static_cast<const __bf16*>(pos),
-                           static_cast<const __bf16*>(type), static_cast<const __bf16*>(g),
-                           static_cast<const __bf16*>(b), static_cast<__bf16*>(y), rows, seq, f, eps);
+        embed_bert_launch<__bf16>(ids, tok, pos, type, g, b, y, rows, seq, f, eps, s);
     else
-        launch_kernel(embed_bert_kernel<float>, dim3(blocks_for(rows, 4)), dim3(256), 0, s, ids,
-                           static_cast<const float*>(tok), static_cast<const float*>(pos),
-                           static_cast<const float*>(type), static_cast<const float*>(g),
-                           static_cast<const float*>(b), static_cast<float*>(y), rows, seq, f, eps);
+        embed_bert_launch<float>(ids, tok, pos, type, g, b, y, rows, seq, f, eps, s);
     return hipGetLastError();
 }
 
