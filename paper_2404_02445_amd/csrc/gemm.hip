@@ -49,8 +49,22 @@ template <typename T> struct Elt;
 template <> struct Elt<__bf16> { static constexpr int EPC = 8; };   // elements per 16-byte chunk
 template <> struct Elt<float> { static constexpr int EPC = 4; };
 
-// 16 zero bytes: the source of every out-of-range chunk.
-__device__ __attribute__((aligned(16))) const unsigned int kZeroChunk[4] = {0u, 0u, 0u, 0u};
+// 32 zero bytes: the source of absent epilogue operands.
+__device__ __attribute__((aligned(16))) const unsigned int kZeroChunk[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+
+// Raw buffer resources: word 3 of the descriptor (32-bit data format) and the lane offset
+// that lies past every resource (operand sizes are below 2^31 bytes) and so reads zeros.
+constexpr int kRsrcWord3 = 0x00020000;
+constexpr unsigned kOOB = 0x80000000u;
+
+// f(std::integral_constant<int, i>) for i = 0 .. N-1, unrolled at compile time
+template <int N, typename F, int I = 0>
+__device__ __forceinline__ void static_for(F&& f) {
+    if constexpr (I < N) {
+        f(std::integral_constant<int, I>{});
+        static_for<N, F, I + 1>(static_cast<F&&>(f));
+    }
+}
 
 __device__ __forceinline__ float ld_f(const __bf16* p, int64_t i) {
     unsigned short u = reinterpret_cast<const unsigned short*>(p)[i];
@@ -137,6 +151,13 @@ __device__ __forceinline__ void load8(const T* p, int64_t i, int nvalid, float (
     for (int q = 0; q < 8; ++q) v[q] = (p && q < nvalid) ? ld_f(p, i + q) : 0.0f;
 }
 
+// the 16 (bf16) or 32 (float) bytes at q, or zeros from the zero page when q is null: one
+// unconditional load either way
+template <typename T>
+__device__ __forceinline__ Raw8<T> load_raw8(const T* q, const void* zero_page) {
+    return *reinterpret_cast<const Raw8<T>*>(q ? static_cast<const void*>(q) : zero_page);
+}
+
 template <typename T>
 __device__ __forceinline__ void store8(T* c, int64_t idx, const float (&v)[8], int nvalid) {
     if (nvalid == 8 && aligned16(c + idx)) {
@@ -183,6 +204,24 @@ __device__ __forceinline__ u32x4 lds_read16(unsigned addr) {
     asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr));
     return v;
 }
+// One 16-byte chunk per lane from the raw buffer [base, base + size) at byte offset voff + soff
+// (soff wave-uniform) into LDS slot lane of the 1 KB block at dst; an offset voff >= size
+// writes zeros.  (The resource is built here, in a plain device function, and not in the
+// kernel templates.)
+__device__ __forceinline__ void buffer_load_lds(const void* base, unsigned size, lds_ptr_t dst, unsigned voff,
+                                                unsigned soff) {
+    const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
+                                                                      static_cast<int>(size), kRsrcWord3);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff, soff, 0, 0);
+}
+
+template <int OFF>
+__device__ __forceinline__ u32x4 lds_read16_at(unsigned addr) {
+    static_assert(OFF >= 0 && OFF < 65536, "ds offset");
+    u32x4 v;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "n"(OFF));
+    return v;
+}
 __device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 template <int N>
 __device__ __forceinline__ void lds_wait_until() {
@@ -206,22 +245,25 @@ __device__ __forceinline__ void wait_stages(int r) {
     }
 }
 
-template <typename T, int BM, int BN, int WM, int WN, int NS, bool CONV>
+template <typename T, int BM, int BN, int WM, int WN, int NS, int KH, bool CONV>
 __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const GemmParams p) {
     constexpr int EPC = Elt<T>::EPC;
-    constexpr int BK = 8 * EPC;                 // K elements per stage: two 32-wide (bf16) k steps
+    constexpr int BK = 8 * EPC;                 // K elements per sub-stage: two 32-wide (bf16) k steps
     constexpr int TM = BM / WM, TN = BN / WN;   // wave tile
     constexpr int FM = TM / 16, FN = TN / 16;   // 16x16 MFMA tiles per wave
     constexpr int NBA = BM / 16 * 2, NBB = BN / 16 * 2;
     constexpr int NBLK = NBA + NBB;             // 1 KB fragment blocks per stage
     constexpr int NW = WM * WN, NT = NW * 64;   // waves and threads per block
-    constexpr int LMAX = (NBLK + NW - 1) / NW, LMIN = NBLK / NW;
-    constexpr int STAGE = NBLK * 64;            // uint4 per stage
+    constexpr int LA = (NBA + NW - 1) / NW, LB = (NBB + NW - 1) / NW;   // load slots per wave
+    constexpr int LMIN = NBA / NW + NBB / NW;   // loads per sub-stage issued by every wave
+    constexpr int STAGE = NBLK * 64;            // uint4 per sub-stage
+    constexpr int SSTAGE = KH * STAGE;          // uint4 per stage: KH sub-stages, one barrier
     static_assert((NW == 4 || NW == 8) && FM >= 1 && FN >= 1 && NS >= 2 && NS <= 9 && LMIN >= 1, "tile");
-    static_assert((NS - 2) * LMIN <= 63, "vmcnt range");
+    static_assert(KH == 1 || KH == 2 || KH == 4, "sub-stages per stage");
+    static_assert((NS - 2) * LMIN * KH <= 63, "vmcnt range");
 
     constexpr int LDT = BN + 4;                 // fp32 row stride of the staged output tile (padded)
-    constexpr int LDS_U4 = NS * STAGE > (BM * LDT + 3) / 4 ? NS * STAGE : (BM * LDT + 3) / 4;
+    constexpr int LDS_U4 = NS * SSTAGE > (BM * LDT + 3) / 4 ? NS * SSTAGE : (BM * LDT + 3) / 4;
     __shared__ uint4 lds[LDS_U4];
 
     const int lane = threadIdx.x & 63;
@@ -254,65 +296,68 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const GemmParams p) 
     if (n0 >= n_hi) return;                     // block-uniform, before any barrier
     const int64_t m0 = static_cast<int64_t>(mti) * BM;
 
+    // this split's sub-stages [u0, u1): boundaries in BK units, whatever KH is
     const int nk = (p.K + BK - 1) / BK;
-    const int kt0 = static_cast<int>(static_cast<int64_t>(nk) * split / p.splits);
-    const int kt1 = static_cast<int>(static_cast<int64_t>(nk) * (split + 1) / p.splits);
+    const int u0 = static_cast<int>(static_cast<int64_t>(nk) * split / p.splits);
+    const int u1 = static_cast<int>(static_cast<int64_t>(nk) * (split + 1) / p.splits);
+    const int nst = (u1 - u0 + KH - 1) / KH;    // stages; sub-stages past u1 load zeros, run no MFMA
 
-    const T* __restrict__ Ap = static_cast<const T*>(p.A);
-    const T* __restrict__ Bp = static_cast<const T*>(p.B);
-    const gptr_t zero = (gptr_t)(kZeroChunk);
-
-    // --- this lane's rows in the blocks its wave loads ------------------------------------
-    // Load block blk of a stage covers 8 rows x 128 bytes (whole cache lines): lane l loads
-    // row 8 * blk + l / 8, k chunk cl = (l % 8) ^ (l / 8) -- the XOR swizzle that keeps the
-    // fragment reads conflict-free -- into LDS slot l of the block.
-    const int cl = (lane & 7) ^ (lane >> 3);    // this lane's chunk of every stage, 0..7
+    // --- operand loads ----------------------------------------------------------------------
+    // Each operand is read through a raw buffer resource: a lane's chunk address is a fixed
+    // per-lane byte offset (VGPR) plus a per-sub-stage offset that only the scalar unit
+    // advances (dense operands), and a lane whose offset is kOOB -- past the resource's size
+    // -- writes zeros to LDS without touching memory (image padding, K tail).
+    // Load block blk of a sub-stage covers 8 rows x 128 bytes (whole cache lines): lane l
+    // loads row 8 * blk + l / 8, k chunk cl = (l % 8) ^ (l / 8) -- the XOR swizzle that keeps
+    // the fragment reads conflict-free -- into LDS slot l of the block.  Wave w loads A blocks
+    // w, w + NW, ... and B blocks w, w + NW, ...: slots are fixed at compile time, and only a
+    // last, partial round of slots tests the wave index.
+    const int cl = (lane & 7) ^ (lane >> 3);    // this lane's chunk of every sub-stage, 0..7
     // Rows past M (A) or past the sub-slice (B) load a real row (the last valid one) instead:
-    // the products they feed are never stored, and every load stays unconditional.
-    // Dense operands: a 32-bit byte offset per lane from a wave-uniform base that advances by
-    // one stage per step.  Conv A: a per-row pointer to the window plus its top-left corner.
-    unsigned voff[LMAX];
-    const T* rowp[LMAX];
-    int hb[LMAX], wb[LMAX];
+    // the products they feed are never stored.
+    // Dense A and B: voff = byte offset of (row, chunk cl of sub-stage 0).  Conv A: voff =
+    // offset of the window's top-left pixel (two's complement when the window starts in the
+    // padding), with the window corner (hb, wb) for the bounds test.
+    unsigned voffA[LA], voffB[LB];
+    int hb[LA], wb[LA];
 #pragma unroll
-    for (int i = 0; i < LMAX; ++i) {
-        const int blk = wave + NW * i;
-        voff[i] = 0;
-        rowp[i] = Bp;
+    for (int i = 0; i < LA; ++i) {
+        const int blk = min(wave + NW * i, NBA - 1);
+        const int64_t m = m0 + blk * 8 + (lane >> 3);
+        const int64_t mc = m < p.M ? m : p.M - 1;
         hb[i] = wb[i] = 0;
-        if (blk >= NBLK) continue;
-        if (blk < NBA) {
-            const int64_t m = m0 + blk * 8 + (lane >> 3);
-            const int64_t mc = m < p.M ? m : p.M - 1;
-            if (CONV) {
-                // M < 2^31, so the pixel decode runs in 32 bits with precomputed divisors;
-                // the row pointer already includes the window's top-left offset
-                const unsigned mu = static_cast<unsigned>(mc);
-                const unsigned img = p.div_hw.div(mu);
-                const unsigned rem = mu - img * static_cast<unsigned>(p.out_h * p.out_w);
-                const unsigned ho = p.div_w.div(rem), wo = rem - ho * static_cast<unsigned>(p.out_w);
-                hb[i] = static_cast<int>(ho) * p.stride - p.pad;
-                wb[i] = static_cast<int>(wo) * p.stride - p.pad;
-                rowp[i] = Ap + static_cast<int64_t>(img) * p.img_h * p.img_w * p.cs +
-                          static_cast<int64_t>(hb[i] * p.img_w + wb[i]) * p.cs;
-            } else {
-                voff[i] = static_cast<unsigned>((mc * p.lda + cl * EPC) * static_cast<int64_t>(sizeof(T)));
-            }
+        if constexpr (CONV) {
+            // M < 2^31, so the pixel decode runs in 32 bits with precomputed divisors
+            const unsigned mu = static_cast<unsigned>(mc);
+            const unsigned img = p.div_hw.div(mu);
+            const unsigned rem = mu - img * static_cast<unsigned>(p.out_h * p.out_w);
+            const unsigned ho = p.div_w.div(rem), wo = rem - ho * static_cast<unsigned>(p.out_w);
+            hb[i] = static_cast<int>(ho) * p.stride - p.pad;
+            wb[i] = static_cast<int>(wo) * p.stride - p.pad;
+            const int pix = (static_cast<int>(img) * p.img_h + hb[i]) * p.img_w + wb[i];
+            voffA[i] = static_cast<unsigned>(pix) * static_cast<unsigned>(p.cs * sizeof(T));
         } else {
-            const int n = n0 + (blk - NBA) * 8 + (lane >> 3);
-            const int nc = n < n_hi ? n : n_hi - 1;
-            voff[i] = static_cast<unsigned>((static_cast<int64_t>(nc) * p.K + cl * EPC) * static_cast<int64_t>(sizeof(T)));
+            voffA[i] = static_cast<unsigned>((mc * p.lda + cl * EPC) * static_cast<int64_t>(sizeof(T)));
         }
+    }
+#pragma unroll
+    for (int i = 0; i < LB; ++i) {
+        const int blk = min(wave + NW * i, NBB - 1);
+        const int n = n0 + blk * 8 + (lane >> 3);
+        const int nc = n < n_hi ? n : n_hi - 1;
+        voffB[i] = static_cast<unsigned>((static_cast<int64_t>(nc) * p.K + cl * EPC) * static_cast<int64_t>(sizeof(T)));
     }
 
     // im2col coordinates (tap row, tap column, channel) of this lane's chunk, advanced
-    // incrementally by one stage (BK = dq * cs + dc elements)
+    // incrementally by one sub-stage: BK = (dqr * kw + dqc) * cs + dc elements
     int tr = 0, tcol = 0, tci = 0;
-    int dq = 0, dc = 0;
+    int dqr = 0, dqc = 0, dc = 0;
     if (CONV) {
-        dq = BK / p.cs;
+        const int dq = BK / p.cs;
         dc = BK - dq * p.cs;
-        const int k = kt0 * BK + cl * EPC;
+        dqr = dq / p.kw;
+        dqc = dq - dqr * p.kw;
+        const int k = u0 * BK + cl * EPC;
         const int tap = k / p.cs;
         tci = k - tap * p.cs;
         tr = tap / p.kw;
@@ -320,49 +365,52 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const GemmParams p) 
     }
     auto advance = [&]() {
         tci += dc;
-        int dt = dq;
-        if (tci >= p.cs) {
-            tci -= p.cs;
-            ++dt;
-        }
-        tcol += dt;
-        while (tcol >= p.kw) {
+        const int carry = tci >= p.cs ? 1 : 0;
+        tci -= carry * p.cs;
+        tcol += dqc + carry;                    // < 2 kw: one wrap at most
+        tr += dqr;
+        if (tcol >= p.kw) {
             tcol -= p.kw;
             ++tr;
         }
     };
 
-    // issue the loads of stage kt (coordinates must be those of stage kt) into LDS buffer buf
-    auto issue = [&](int kt, int buf) {
-        const int k = kt * BK + cl * EPC;
-        const bool tail = (kt + 1) * BK > p.K;          // uniform: only the last stage may pass K
-        // conv: offset of the tap / channel within the window
-        const int koff = CONV ? (tr * p.img_w + tcol) * p.cs + tci : 0;
-        const char* abase = reinterpret_cast<const char*>(Ap) + static_cast<int64_t>(kt) * BK * sizeof(T);
-        const char* bbase = reinterpret_cast<const char*>(Bp) + static_cast<int64_t>(kt) * BK * sizeof(T);
-        auto conv_src = [&](int i) -> gptr_t {
-            const bool ok = (!tail || k < p.K) &&
-                            static_cast<unsigned>(hb[i] + tr) < static_cast<unsigned>(p.img_h) &&
-                            static_cast<unsigned>(wb[i] + tcol) < static_cast<unsigned>(p.img_w);
-            return ok ? (gptr_t)(rowp[i] + koff) : zero;
-        };
-        if (!tail) {
+    // Loads of sub-stage kt (conv coordinates must be those of kt) into LDS at dst.  A dead
+    // sub-stage (past the split: its MFMAs are skipped) re-reads sub-stage u0, so that every
+    // sub-stage issues the same loads and the wait counts stay exact.
+    const int ktail = (p.K % BK) ? nk - 1 : nk;   // the one sub-stage whose chunks may pass K
+    auto issue = [&](int kt, uint4* dst, bool live) {
+        const int ku = live ? kt : u0;
+        const unsigned soff = static_cast<unsigned>(ku) * (BK * sizeof(T));
+        const bool tail = ku == ktail;          // uniform
+        const bool kin = !tail || ku * BK + cl * EPC < p.K;
+        const unsigned koff = CONV ? static_cast<unsigned>(((tr * p.img_w + tcol) * p.cs + tci) * sizeof(T)) : 0u;
 #pragma unroll
-            for (int i = 0; i < LMAX; ++i) {
-                const int blk = wave + NW * i;
-                if (blk >= NBLK) continue;      // wave-uniform
-                const gptr_t src = (CONV && blk < NBA) ? conv_src(i) : (gptr_t)((blk < NBA ? abase : bbase) + voff[i]);
-                __builtin_amdgcn_global_load_lds(src, (lds_ptr_t)(&lds[buf * STAGE + blk * 64]), 16, 0, 0);
+        for (int i = 0; i < LA; ++i) {
+            if (NBA % NW != 0 && i == LA - 1 && wave + NW * i >= NBA) break;   // wave-uniform
+            unsigned v;
+            if constexpr (CONV) {
+                const bool ok = kin && static_cast<unsigned>(hb[i] + tr) < static_cast<unsigned>(p.img_h) &&
+                                static_cast<unsigned>(wb[i] + tcol) < static_cast<unsigned>(p.img_w);
+                v = ok ? voffA[i] + koff : kOOB;
+            } else {
+                v = kin ? voffA[i] : kOOB;
             }
-        } else {                                // K tail: chunks past K read zeros on both operands
+            buffer_load_lds(p.A, p.a_bytes, (lds_ptr_t)(dst + (wave + NW * i) * 64), v, CONV ? 0u : soff);
+        }
 #pragma unroll
-            for (int i = 0; i < LMAX; ++i) {
-                const int blk = wave + NW * i;
-                if (blk >= NBLK) continue;
-                gptr_t src = (CONV && blk < NBA) ? conv_src(i) : (gptr_t)((blk < NBA ? abase : bbase) + voff[i]);
-                if (k >= p.K) src = zero;
-                __builtin_amdgcn_global_load_lds(src, (lds_ptr_t)(&lds[buf * STAGE + blk * 64]), 16, 0, 0);
-            }
+        for (int i = 0; i < LB; ++i) {
+            if (NBB % NW != 0 && i == LB - 1 && wave + NW * i >= NBB) break;
+            buffer_load_lds(p.B, p.b_bytes, (lds_ptr_t)(dst + (NBA + wave + NW * i) * 64), kin ? voffB[i] : kOOB, soff);
+        }
+    };
+    // stage st: sub-stages u0 + st * KH + h into buffer buf, conv coordinates advanced past them
+    auto issue_stage = [&](int st, int buf) {
+#pragma unroll
+        for (int h = 0; h < KH; ++h) {
+            const int kt = u0 + st * KH + h;
+            issue(kt, &lds[buf * SSTAGE + h * STAGE], kt < u1);
+            if (CONV) advance();
         }
     };
 
@@ -389,47 +437,47 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const GemmParams p) 
     const int cc = threadIdx.x % CPR, cr = threadIdx.x / CPR;
     const int c0 = n0 + cc * 8;
     const int cval = max(0, min(8, n_hi - c0));
-    float bias8[8];
-    load8<T>(static_cast<const T*>(p.bias), c0, cval, bias8);
-    if (p.bias2) {
-        float t8[8];
-        load8<T>(static_cast<const T*>(p.bias2), c0, cval, t8);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) bias8[e] += t8[e];
-    }
     const bool direct = p.splits == 1 && p.epi == EPI_STD;   // this block finishes its outputs
-    // residual kept as raw bits so the prefetch costs few registers
+    // Epilogue operands (bias, second bias, residual), fetched now as raw bits so their
+    // latency hides under the main loop.  Each is one unconditional 16-byte load -- from the
+    // zero page when the chunk is absent, partial or misaligned -- so no branch makes the
+    // wave wait for it here; partial chunks are read element by element in the epilogue.
+    const T* biasp = static_cast<const T*>(p.bias);
+    const T* bias2p = static_cast<const T*>(p.bias2);
+    const T* resp = static_cast<const T*>(p.res);
+    const bool bfast = cval == 8 && (!biasp || aligned16(biasp + c0)) && (!bias2p || aligned16(bias2p + c0));
+    const Raw8<T> braw = load_raw8<T>(direct && bfast && biasp ? biasp + c0 : nullptr, kZeroChunk);
+    const Raw8<T> b2raw = load_raw8<T>(direct && bfast && bias2p ? bias2p + c0 : nullptr, kZeroChunk);
     Raw8<T> rraw[NCH];
     bool rfast[NCH];
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
         const int64_t m = m0 + cr + i * RPP;
         const int64_t idx = m * p.ldc + c0;
-        rfast[i] = direct && p.res && cr + i * RPP < BM && m < p.M && cval == 8 &&
-                   aligned16(static_cast<const T*>(p.res) + idx);
-        rraw[i] = Raw8<T>{};
-        if (rfast[i]) rraw[i] = *reinterpret_cast<const Raw8<T>*>(static_cast<const T*>(p.res) + idx);
+        rfast[i] = direct && resp && cr + i * RPP < BM && m < p.M && cval == 8 && aligned16(resp + idx);
+        rraw[i] = load_raw8<T>(rfast[i] ? resp + idx : nullptr, kZeroChunk);
     }
 
-    // prologue: NS-1 stages in flight (coordinates then stand at stage kt0 + NS - 1)
+    // prologue: NS-1 stages in flight (coordinates then stand at stage NS - 1)
 #pragma unroll
-    for (int s = 0; s < NS - 1; ++s) {
-        if (kt0 + s < kt1) issue(kt0 + s, s);
-        if (CONV) advance();
-    }
+    for (int s = 0; s < NS - 1; ++s)
+        if (s < nst) issue_stage(s, s);
 
-    // LDS byte offsets of this lane's MFMA fragment (row l % 16 of a 16-row block, chunk
-    // 4 * ks + l / 16) for the two k steps of a stage, relative to the block's first 8 rows
+    // LDS byte addresses of this lane's MFMA fragments (row l % 16 of a 16-row block, chunk
+    // 4 * ks + l / 16) in stage buffer 0, sub-stage 0, for the wave's first A and B rows;
+    // the other fragments sit at compile-time offsets from them
     const unsigned lds0 = static_cast<unsigned>(reinterpret_cast<size_t>((lds_ptr_t)(&lds[0])));
-    unsigned foff[2];
+    unsigned fa[2], fb[2];
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
-        foff[ks] = lds0 + ((((lane >> 3) & 1) * 64 + (lane & 7) * 8 + ((ks * 4 + (lane >> 4)) ^ (lane & 7))) * 16);
+    for (int ks = 0; ks < 2; ++ks) {
+        const unsigned f = lds0 + ((((lane >> 3) & 1) * 64 + (lane & 7) * 8 + ((ks * 4 + (lane >> 4)) ^ (lane & 7))) * 16);
+        fa[ks] = f + ((wm * TM) >> 3) * 1024;
+        fb[ks] = f + (NBA + ((wn * TN) >> 3)) * 1024;
+    }
     auto read_frags = [&](unsigned sbase, int ks, u32x4 (&af)[FM], u32x4 (&bf)[FN]) {
-#pragma unroll
-        for (int a = 0; a < FM; ++a) af[a] = lds_read16(sbase + foff[ks] + ((wm * TM + a * 16) >> 3) * 1024);
-#pragma unroll
-        for (int b = 0; b < FN; ++b) bf[b] = lds_read16(sbase + foff[ks] + (NBA + ((wn * TN + b * 16) >> 3)) * 1024);
+        const unsigned ab = sbase + fa[ks], bb = sbase + fb[ks];
+        static_for<FM>([&](auto a) { af[a] = lds_read16_at<a * 2048>(ab); });
+        static_for<FN>([&](auto b) { bf[b] = lds_read16_at<b * 2048>(bb); });
     };
     auto mfmas = [&](u32x4 (&af)[FM], u32x4 (&bf)[FN]) {
 #pragma unroll
@@ -449,18 +497,39 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const GemmParams p) 
             }
     };
 
-    for (int kt = kt0; kt < kt1; ++kt) {
-        const int buf = (kt - kt0) % NS;
-        const int later = min(NS - 2, kt1 - 1 - kt);   // stages issued after this one
-        wait_stages<LMIN>(later);                      // this wave's share of stage kt has landed
-        __builtin_amdgcn_s_barrier();                  // every wave's share has; stage kt-1 fully consumed
-        if (kt + NS - 1 < kt1) {
-            issue(kt + NS - 1, (kt - kt0 + NS - 1) % NS);
-            if (CONV) advance();
-        }
-        const unsigned sbase = buf * STAGE * 16;
+    for (int st = 0; st < nst; ++st) {
+        const int buf = st % NS;
+        const int later = min(NS - 2, nst - 1 - st);   // stages issued after this one
+        wait_stages<LMIN * KH>(later);                 // this wave's share of stage st has landed
+        __builtin_amdgcn_s_barrier();                  // every wave's share has; stage st-1 fully consumed
+        if (st + NS - 1 < nst) issue_stage(st + NS - 1, (st + NS - 1) % NS);
+        const unsigned sbase = buf * SSTAGE * 16;
         u32x4 a0[FM], b0[FN], a1[FM], b1[FN];
-        if constexpr (FM + FN <= 3) {
+        if constexpr (KH > 1) {
+            // k steps 2h, 2h + 1 of sub-stage h; each step's fragment reads are issued before
+            // the previous step's MFMAs, so LDS latency hides under them
+            const int steps = 2 * min(KH, u1 - (u0 + st * KH));   // live k steps (uniform)
+            read_frags(sbase, 0, a0, b0);
+#pragma unroll
+            for (int j = 0; j < 2 * KH; j += 2) {
+                if (j >= steps) break;
+                lds_wait();
+#pragma unroll
+                for (int a = 0; a < FM; ++a) pin(a0[a]);
+#pragma unroll
+                for (int b = 0; b < FN; ++b) pin(b0[b]);
+                read_frags(sbase + (j / 2) * STAGE * 16, 1, a1, b1);
+                mfmas(a0, b0);
+                lds_wait();
+#pragma unroll
+                for (int a = 0; a < FM; ++a) pin(a1[a]);
+#pragma unroll
+                for (int b = 0; b < FN; ++b) pin(b1[b]);
+                if (j + 2 < steps) read_frags(sbase + (j / 2 + 1) * STAGE * 16, 0, a0, b0);
+                mfmas(a1, b1);
+            }
+            continue;
+        } else if constexpr (FM + FN <= 3) {
             // thin wave tiles: both k steps' fragment reads go out together; LDS reads complete
             // in order, so once at most FM + FN are outstanding the first step's have landed
             read_frags(sbase, 0, a0, b0);
@@ -541,7 +610,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const GemmParams p) 
     };
     // (v + bias) + residual, activation, store: the same operations, in the same order,
     // whether the sums come from this block or from the split-K partials
-    auto finish = [&](int64_t m, float (&v)[8], const float (&rsd)[8]) {
+    auto finish = [&](int64_t m, float (&v)[8], const float (&bias8)[8], const float (&rsd)[8]) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] = act_f((v[e] + bias8[e]) + rsd[e], p.act);
         const int64_t idx = m * p.ldc + c0;
@@ -552,6 +621,24 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const GemmParams p) 
     };
 
     if (direct) {
+        float bias8[8];
+        if (bfast) {
+            unpack8<T>(braw, bias8);
+            if (bias2p) {
+                float t8[8];
+                unpack8<T>(b2raw, t8);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) bias8[e] += t8[e];
+            }
+        } else {
+            load8<T>(biasp, c0, cval, bias8);
+            if (bias2p) {
+                float t8[8];
+                load8<T>(bias2p, c0, cval, t8);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) bias8[e] += t8[e];
+            }
+        }
 #pragma unroll
         for (int i = 0; i < NCH; ++i) {
             const int r = cr + i * RPP;
@@ -563,7 +650,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const GemmParams p) 
                 unpack8<T>(rraw[i], rsd);
             else
                 load8<T>(static_cast<const T*>(p.res), m * p.ldc + c0, p.res ? cval : 0, rsd);
-            finish(m, v, rsd);
+            finish(m, v, bias8, rsd);
         }
         return;
     }
@@ -628,15 +715,17 @@ int gemm_splits(int64_t M, int N, int K, int dtype, int epi) {
     return s;
 }
 
-template <typename T, int BM, int BN, int WM, int WN, int NS>
+template <typename T, int BM, int BN, int WM, int WN, int NS, int KH = 1>
 static hipError_t launch_cfg(const GemmParams& p, int width, hipStream_t st) {
     const int64_t total = ((p.M + BM - 1) / BM) * ((width + BN - 1) / BN) * p.ksub * p.splits;
     const int64_t grid = (total + 7) / 8 * 8;
     const dim3 block(WM * WN * 64);
     if (p.conv)
-        launch_kernel((gemm_kernel<T, BM, BN, WM, WN, NS, true>), dim3(static_cast<unsigned>(grid)), block, 0, st, p);
+        launch_kernel((gemm_kernel<T, BM, BN, WM, WN, NS, KH, true>), dim3(static_cast<unsigned>(grid)), block, 0, st,
+                      p);
     else
-        launch_kernel((gemm_kernel<T, BM, BN, WM, WN, NS, false>), dim3(static_cast<unsigned>(grid)), block, 0, st, p);
+        launch_kernel((gemm_kernel<T, BM, BN, WM, WN, NS, KH, false>), dim3(static_cast<unsigned>(grid)), block, 0, st,
+                      p);
     return hipGetLastError();
 }
 
@@ -670,10 +759,15 @@ hipError_t launch_gemm(const GemmParams& params, int dtype, hipStream_t stream) 
         p.div_w = FastDiv(static_cast<unsigned>(p.out_w));
     }
     if (p.M <= 0 || p.N <= 0) return hipSuccess;
-    // dense operands are addressed with 32-bit byte offsets
+    // operands are read through buffer resources with 32-bit byte offsets, and offset 2^31
+    // must lie past both of them
     const int64_t esz = dtype == MOPAR_BF16 ? 2 : 4;
-    if ((!p.conv && p.M * p.lda * esz >= (int64_t(1) << 32)) || int64_t(p.N) * p.K * esz >= (int64_t(1) << 32))
-        return hipErrorInvalidValue;
+    const int64_t a_bytes = p.conv ? p.M / (int64_t(p.out_h) * p.out_w) * p.img_h * p.img_w * p.cs * esz
+                                   : p.M * p.lda * esz;
+    const int64_t b_bytes = int64_t(p.N) * p.K * esz;
+    if (a_bytes >= (int64_t(1) << 31) || b_bytes >= (int64_t(1) << 31)) return hipErrorInvalidValue;
+    p.a_bytes = static_cast<uint32_t>(a_bytes);
+    p.b_bytes = static_cast<uint32_t>(b_bytes);
     if (p.splits < 1 || (p.splits > 1 && (!p.partial || p.epi != EPI_STD))) return hipErrorInvalidValue;
     hipError_t e = dtype == MOPAR_BF16 ? dispatch<__bf16>(p, stream) : dispatch<float>(p, stream);
     if (e != hipSuccess || p.splits == 1) return e;

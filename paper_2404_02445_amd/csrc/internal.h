@@ -88,6 +88,7 @@ struct GemmParams {
     int kh, kw, stride, pad;
     FastDiv div_hw, div_w;  // conv: divide by out_h * out_w and by out_w (set by launch_gemm)
     const void* B;          // [N][K]
+    uint32_t a_bytes, b_bytes;   // extent of A (the whole image for conv) and B (set by launch_gemm)
     const void* bias;       // [N] or null
     const void* res;        // [M][ldc] or null
     void* C;
