@@ -55,6 +55,8 @@ __device__ __attribute__((aligned(16))) const unsigned int kZeroChunk[8] = {0u, 
 // Raw buffer resources: word 3 of the descriptor (32-bit data format) and the lane offset
 // that lies past every resource (operand sizes are below 2^31 bytes) and so reads zeros.
 constexpr int kRsrcWord3 = 0x00020000;
+// m tiles per group in the XCD-local block order
+constexpr int kGroupM = 8;
 constexpr unsigned kOOB = 0x80000000u;
 
 // f(std::integral_constant<int, i>) for i = 0 .. N-1, unrolled at compile time
@@ -271,35 +273,34 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const GemmParams p) 
     const int wm = wave / WN, wn = wave % WN;
 
     // --- block -> (m tile, split, sub-slice, n tile), XCD-grouped -------------------------
-    const int width = (p.N + p.ksub - 1) / p.ksub;
-    const int mt = static_cast<int>((p.M + BM - 1) / BM), nt = (width + BN - 1) / BN;
-    const int total = mt * p.splits * p.ksub * nt;
-    const int per_xcd = (total + 7) / 8;
-    const int t = static_cast<int>(blockIdx.x % 8) * per_xcd + static_cast<int>(blockIdx.x / 8);
-    if (t >= total) return;
+    // (all divisions by launch constants go through precomputed multipliers)
+    const unsigned t = (blockIdx.x % 8) * static_cast<unsigned>(p.g_per_xcd) + blockIdx.x / 8;
+    if (t >= static_cast<unsigned>(p.g_total)) return;
     // within an XCD's run, tiles go in groups of GM m-tiles x every column (split, sub-slice,
     // n-tile), m fastest: the blocks resident together share both A rows and B rows in L2
-    constexpr int GM = 8;
-    const int cols = p.splits * p.ksub * nt;
-    const int group = t / (GM * cols), within = t - group * (GM * cols);
-    const int gm = min(GM, mt - group * GM);
-    const int mti = group * GM + within % gm;
-    int col = within / gm;
-    const int nti = col % nt;
-    col /= nt;
-    const int j = col % p.ksub;
-    const int split = col / p.ksub;
+    constexpr int GM = kGroupM;
+    const unsigned group = p.g_div_group.div(t);
+    const unsigned within = t - group * static_cast<unsigned>(GM * p.g_cols);
+    const bool last = static_cast<int>(group) == (p.g_mt - 1) / GM;   // the last group may be short
+    const unsigned gm = last ? static_cast<unsigned>(p.g_mt - group * GM) : GM;
+    const unsigned colu = last ? p.g_div_last.div(within) : within / GM;
+    const int mti = static_cast<int>(group * GM + (within - colu * gm));
+    const unsigned c1 = p.g_div_nt.div(colu);
+    const int nti = static_cast<int>(colu - c1 * static_cast<unsigned>(p.g_nt));
+    const unsigned c2 = p.g_div_ksub.div(c1);
+    const int j = static_cast<int>(c1 - c2 * static_cast<unsigned>(p.ksub));
+    const int split = static_cast<int>(c2);
 
-    const int q = p.N / p.ksub, rr = p.N % p.ksub;
+    const int q = p.g_q, rr = p.g_rr;
     const int n_lo = j * q + min(j, rr), n_hi = (j + 1) * q + min(j + 1, rr);
     const int n0 = n_lo + nti * BN;
     if (n0 >= n_hi) return;                     // block-uniform, before any barrier
     const int64_t m0 = static_cast<int64_t>(mti) * BM;
 
     // this split's sub-stages [u0, u1): boundaries in BK units, whatever KH is
-    const int nk = (p.K + BK - 1) / BK;
-    const int u0 = static_cast<int>(static_cast<int64_t>(nk) * split / p.splits);
-    const int u1 = static_cast<int>(static_cast<int64_t>(nk) * (split + 1) / p.splits);
+    const int nk = p.g_nk;
+    const int u0 = static_cast<int>(p.g_div_splits.div(static_cast<unsigned>(nk * split)));
+    const int u1 = static_cast<int>(p.g_div_splits.div(static_cast<unsigned>(nk * (split + 1))));
     const int nst = (u1 - u0 + KH - 1) / KH;    // stages; sub-stages past u1 load zeros, run no MFMA
 
     // --- operand loads ----------------------------------------------------------------------
@@ -351,17 +352,14 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const GemmParams p) 
     // im2col coordinates (tap row, tap column, channel) of this lane's chunk, advanced
     // incrementally by one sub-stage: BK = (dqr * kw + dqc) * cs + dc elements
     int tr = 0, tcol = 0, tci = 0;
-    int dqr = 0, dqc = 0, dc = 0;
+    const int dqr = p.dqr, dqc = p.dqc, dc = p.dc;
     if (CONV) {
-        const int dq = BK / p.cs;
-        dc = BK - dq * p.cs;
-        dqr = dq / p.kw;
-        dqc = dq - dqr * p.kw;
-        const int k = u0 * BK + cl * EPC;
-        const int tap = k / p.cs;
-        tci = k - tap * p.cs;
-        tr = tap / p.kw;
-        tcol = tap - tr * p.kw;
+        const unsigned k = static_cast<unsigned>(u0 * BK + cl * EPC);
+        const unsigned tap = p.div_cs.div(k);
+        tci = static_cast<int>(k - tap * static_cast<unsigned>(p.cs));
+        const unsigned r = p.div_kw.div(tap);
+        tr = static_cast<int>(r);
+        tcol = static_cast<int>(tap - r * static_cast<unsigned>(p.kw));
     }
     auto advance = [&]() {
         tci += dc;
@@ -716,8 +714,33 @@ int gemm_splits(int64_t M, int N, int K, int dtype, int epi) {
 }
 
 template <typename T, int BM, int BN, int WM, int WN, int NS, int KH = 1>
-static hipError_t launch_cfg(const GemmParams& p, int width, hipStream_t st) {
-    const int64_t total = ((p.M + BM - 1) / BM) * ((width + BN - 1) / BN) * p.ksub * p.splits;
+static hipError_t launch_cfg(const GemmParams& params, int width, hipStream_t st) {
+    GemmParams p = params;
+    const int64_t mt = (p.M + BM - 1) / BM, nt = (width + BN - 1) / BN;
+    const int64_t total = mt * nt * p.ksub * p.splits;
+    if (total >= (int64_t(1) << 31) / kGroupM) return hipErrorInvalidValue;
+    p.g_mt = static_cast<int>(mt);
+    p.g_nt = static_cast<int>(nt);
+    p.g_total = static_cast<int>(total);
+    p.g_per_xcd = static_cast<int>((total + 7) / 8);
+    p.g_cols = static_cast<int>(nt * p.ksub * p.splits);
+    p.g_nk = (p.K + 8 * Elt<T>::EPC - 1) / (8 * Elt<T>::EPC);
+    p.g_q = p.N / p.ksub;
+    p.g_rr = p.N % p.ksub;
+    p.g_div_group = FastDiv(static_cast<unsigned>(kGroupM * p.g_cols));
+    const int last = static_cast<int>(mt - (mt - 1) / kGroupM * kGroupM);   // m tiles in the last group
+    p.g_div_last = FastDiv(static_cast<unsigned>(last));
+    p.g_div_nt = FastDiv(static_cast<unsigned>(nt));
+    p.g_div_ksub = FastDiv(static_cast<unsigned>(p.ksub));
+    p.g_div_splits = FastDiv(static_cast<unsigned>(p.splits));
+    if (p.conv) {
+        const int bk = 8 * Elt<T>::EPC, dq = bk / p.cs;
+        p.dc = bk - dq * p.cs;
+        p.dqr = dq / p.kw;
+        p.dqc = dq - p.dqr * p.kw;
+        p.div_cs = FastDiv(static_cast<unsigned>(p.cs));
+        p.div_kw = FastDiv(static_cast<unsigned>(p.kw));
+    }
     const int64_t grid = (total + 7) / 8 * 8;
     const dim3 block(WM * WN * 64);
     if (p.conv)

@@ -87,6 +87,8 @@ struct GemmParams {
     int out_h, out_w;       // output H, W
     int kh, kw, stride, pad;
     FastDiv div_hw, div_w;  // conv: divide by out_h * out_w and by out_w (set by launch_gemm)
+    FastDiv div_cs, div_kw; // conv: divide by cs and by kw (set by launch_gemm)
+    int dqr, dqc, dc;       // conv: one k sub-stage = (dqr * kw + dqc) taps and dc channels
     const void* B;          // [N][K]
     uint32_t a_bytes, b_bytes;   // extent of A (the whole image for conv) and B (set by launch_gemm)
     const void* bias;       // [N] or null
@@ -107,6 +109,11 @@ struct GemmParams {
     // the new hidden state of unit u goes to C[m * ldc + u]
     int splits;             // split-K factor (>= 1); > 1 needs `partial`
     float* partial;         // [splits][M][N] float32 partial sums (split-K only)
+    // launch geometry, set by the tile launcher: m / n tiles, blocks in all and per XCD,
+    // columns (split, sub-slice, n tile) of an m tile, k sub-stages, sub-slice width q and
+    // remainder rr, and divisors for the block-index decode
+    int g_mt, g_nt, g_total, g_per_xcd, g_cols, g_nk, g_q, g_rr;
+    FastDiv g_div_group, g_div_last, g_div_nt, g_div_ksub, g_div_splits;
 };
 
 // Split-K factor used for an (M, N, K) product.  A function of the shape
