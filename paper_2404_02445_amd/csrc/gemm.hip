@@ -10,25 +10,30 @@
 // Horizontal sub-slicing (the k equal-size sub-slices of an RD operator): a
 // block's sub-slice index selects output columns [lo, hi) and weight rows
 // [lo, hi), split as mopar_subslice_range does; each sub-slice is tiled on its
-// own and masked at hi.  The K loop -- stage depth, MFMA shape, chunk order,
-// split-K boundaries and the order partial sums are added -- depends only on
-// (M, N, K) and the dtype, never on the tile shape or the sub-slice, so every
-// output element goes through the same fp32 operations whatever k is:
-// sub-sliced output equals the unsplit output bit for bit.
+// own and masked at hi.  What fixes the arithmetic -- the MFMA shape, the order
+// of the 32-wide k steps, the split-K boundaries (in 64-element units) and the
+// order partial sums are added -- depends only on (M, N, K) and the dtype, never
+// on the tile shape, the stage depth or the sub-slice, so every output element
+// goes through the same fp32 operations whatever k is: sub-sliced output equals
+// the unsplit output bit for bit.
 //
-// Data path.  Operands stream from HBM straight into LDS with
-// global_load_lds_dwordx4 (16 bytes per lane, no VGPR staging), NS stages deep.
-// A stage holds 64 bf16 (32 float) of k for every row: 128 bytes, one cache
-// line.  Each load instruction fetches 8 whole rows (the DMA writes lane l's
-// 16 bytes to slot l of a 1 KB LDS block); lanes take the chunks of a row in
-// XOR-swizzled order (chunk (l % 8) ^ row), so the ds_read_b128 of an MFMA
-// fragment -- 16 rows, one chunk each -- hits distinct banks.  Out-of-range chunks (image padding, M/N/K
-// tails) are loaded from a zero page, so every lane issues the same number of
-// loads and the wait counts are exact.  Four waves run v_mfma_f32_16x16x32_bf16
-// (bf16) or v_mfma_f32_16x16x4_f32 (fp32) on their wave tile, with the weight
-// fragment as the first operand: each lane ends up holding four consecutive
-// output columns of one row, so bias, residual, activation, the LSTM cell and
-// the store work on 4-wide vectors.
+// Data path.  Operands stream from HBM straight into LDS with buffer_load_dwordx4
+// ... lds (16 bytes per lane, no VGPR staging), NS stages deep; a stage holds KH
+// sub-stages and costs one barrier.  A sub-stage holds 64 bf16 (32 float) of k for
+// every row: 128 bytes, one cache line.  Each load instruction fetches 8 whole rows
+// (the DMA writes lane l's 16 bytes to slot l of a 1 KB LDS block); lanes take the
+// chunks of a row in XOR-swizzled order (chunk (l % 8) ^ row), so the ds_read_b128
+// of an MFMA fragment -- 16 rows, one chunk each -- hits distinct banks.  Each
+// operand is a raw buffer resource: a lane's offset is fixed at set-up, the k
+// advance of dense operands is a scalar offset, and out-of-range chunks (image
+// padding, the K tail) use an offset past the resource, which writes zeros without
+// a memory access -- every lane issues the same loads, so the wait counts are
+// exact.  The waves run v_mfma_f32_16x16x32_bf16 (bf16) or v_mfma_f32_16x16x4_f32
+// (fp32) on their wave tile, with the weight fragment as the first operand: each
+// lane ends up holding four consecutive output columns of one row.  The epilogue
+// stages the fp32 tile through LDS so that each thread finishes whole 8-column
+// chunks (bias, residual, activation, one 16-byte store); the LSTM cell works on
+// the MFMA layout directly.
 //
 // Blocks are numbered so that the eight XCDs (which take blocks round-robin)
 // each receive a contiguous run of tiles, grouped eight m-tiles at a time so
