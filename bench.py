@@ -168,6 +168,8 @@ def main():
                     help="config: the workload's prescribed cuts and k; measured: Alg. 1 free mode with the "
                          "parallelism search over t_p(l, k) measured on this GPU")
     ap.add_argument("--k-max", type=int, default=4, help="largest sub-slice count of the measured search")
+    ap.add_argument("--no-measured-plan", action="store_true",
+                    help="skip the measured-profile planning pass (profiler runs: only the step's launches)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="print the traffic summary from two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) "
                          "of this script with --calibrate-copy-mib, and exit")
@@ -198,10 +200,14 @@ def main():
                    k_override=s["k_override"])
     x = torch.from_numpy(x_host).to(dev)
     # measured-profile planning (Alg. 1 + Eq. 5 over t_p measured here), reported in every run
-    mplan, tp, mprof = sm.measured_plan(x, k_max=args.k_max, reps=3)
-    measured = {"k_max": args.k_max, "n_slices": mplan.n_slices, "slice_end": mplan.slice_end,
-                "k": mplan.k, "t_tau_ms": round(mplan.t_tau * 1e3, 4),
-                "tp_ms_by_k": [round(sum(r[e] for r in tp) * 1e3, 4) for e in range(args.k_max)]}
+    if args.no_measured_plan and args.plan == "measured":
+        sys.exit("--plan measured needs the measured-profile pass")
+    measured = None
+    if not args.no_measured_plan:
+        mplan, tp, mprof = sm.measured_plan(x, k_max=args.k_max, reps=3)
+        measured = {"k_max": args.k_max, "n_slices": mplan.n_slices, "slice_end": mplan.slice_end,
+                    "k": mplan.k, "t_tau_ms": round(mplan.t_tau * 1e3, 4),
+                    "tp_ms_by_k": [round(sum(r[e] for r in tp) * 1e3, 4) for e in range(args.k_max)]}
     if args.plan == "measured":
         plan = mplan
         prof_fixed = mprof
