@@ -252,30 +252,37 @@ __device__ __forceinline__ void wait_stages(int r) {
     }
 }
 
-template <typename T, int BM, int BN, int WM, int WN, int NS, int KH, bool CONV>
-__global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const GemmParams p) {
+// KS > 1: the KS waves of a block share one wave tile (the whole block tile) and split K
+// instead: a stage holds KH = KS sub-stages and wave w computes sub-stage w of each, so the
+// serial K loop is KS times shorter; the waves' sums are added in wave order at the end.
+template <typename T, int BM, int BN, int WM, int WN, int NS, int KH, int KS, bool CONV>
+__global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParams p) {
     constexpr int EPC = Elt<T>::EPC;
     constexpr int BK = 8 * EPC;                 // K elements per sub-stage: two 32-wide (bf16) k steps
     constexpr int TM = BM / WM, TN = BN / WN;   // wave tile
     constexpr int FM = TM / 16, FN = TN / 16;   // 16x16 MFMA tiles per wave
     constexpr int NBA = BM / 16 * 2, NBB = BN / 16 * 2;
     constexpr int NBLK = NBA + NBB;             // 1 KB fragment blocks per stage
-    constexpr int NW = WM * WN, NT = NW * 64;   // waves and threads per block
+    constexpr int NW = WM * WN * KS, NT = NW * 64;   // waves and threads per block
     constexpr int LA = (NBA + NW - 1) / NW, LB = (NBB + NW - 1) / NW;   // load slots per wave
     constexpr int LMIN = NBA / NW + NBB / NW;   // loads per sub-stage issued by every wave
     constexpr int STAGE = NBLK * 64;            // uint4 per sub-stage
     constexpr int SSTAGE = KH * STAGE;          // uint4 per stage: KH sub-stages, one barrier
     static_assert((NW == 4 || NW == 8) && FM >= 1 && FN >= 1 && NS >= 2 && NS <= 9 && LMIN >= 1, "tile");
     static_assert(KH == 1 || KH == 2 || KH == 4, "sub-stages per stage");
+    static_assert(KS == 1 || (KS == KH && WM == 1 && WN == 1), "K split across waves");
     static_assert((NS - 2) * LMIN * KH <= 63, "vmcnt range");
 
     constexpr int LDT = BN + 4;                 // fp32 row stride of the staged output tile (padded)
-    constexpr int LDS_U4 = NS * SSTAGE > (BM * LDT + 3) / 4 ? NS * SSTAGE : (BM * LDT + 3) / 4;
+    constexpr int TILE_U4 = (KS * BM * LDT + 3) / 4;   // staged output tile(s), one per K-split wave
+    constexpr int LDS_U4 = NS * SSTAGE > TILE_U4 ? NS * SSTAGE : TILE_U4;
     __shared__ uint4 lds[LDS_U4];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // scalar: load blocks are wave-uniform
-    const int wm = wave / WN, wn = wave % WN;
+    const int wt = KS > 1 ? 0 : wave;           // wave-tile index
+    const int kw = KS > 1 ? wave : 0;           // K-split index
+    const int wm = wt / WN, wn = wt % WN;
 
     // --- block -> (m tile, split, sub-slice, n tile), XCD-grouped -------------------------
     // (all divisions by launch constants go through precomputed multipliers)
@@ -508,7 +515,19 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const GemmParams p) 
         if (st + NS - 1 < nst) issue_stage(st + NS - 1, (st + NS - 1) % NS);
         const unsigned sbase = buf * SSTAGE * 16;
         u32x4 a0[FM], b0[FN], a1[FM], b1[FN];
-        if constexpr (KH > 1) {
+        if constexpr (KS > 1) {
+            // this wave's sub-stage of the stage (uniform skip when it lies past the split)
+            if (u0 + st * KH + kw >= u1) continue;
+            const unsigned hb = sbase + kw * STAGE * 16;
+            read_frags(hb, 0, a0, b0);
+            lds_wait();
+#pragma unroll
+            for (int a = 0; a < FM; ++a) pin(a0[a]);
+#pragma unroll
+            for (int b = 0; b < FN; ++b) pin(b0[b]);
+            read_frags(hb, 1, a1, b1);
+            mfmas(a0, b0);
+        } else if constexpr (KH > 1) {
             // k steps 2h, 2h + 1 of sub-stage h; each step's fragment reads are issued before
             // the previous step's MFMAs, so LDS latency hides under them
             const int steps = 2 * min(KH, u1 - (u0 + st * KH));   // live k steps (uniform)
@@ -565,15 +584,45 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const GemmParams p) 
     }
 
     // --- epilogue --------------------------------------------------------------------------
+    // The fp32 tile goes through LDS (row-major, padded rows; one copy per K-split wave,
+    // added in wave order when read back).
+    float* tile = reinterpret_cast<float*>(lds);
+    auto stage_tile = [&]() {
+        __syncthreads();                      // every wave is done with the operand stages
+#pragma unroll
+        for (int a = 0; a < FM; ++a)
+#pragma unroll
+            for (int b = 0; b < FN; ++b) {
+                const int row = wm * TM + a * 16 + (lane & 15), col = wn * TN + b * 16 + (lane >> 4) * 4;
+                *reinterpret_cast<f32x4*>(tile + (kw * BM + row) * LDT + col) = acc[a][b];
+            }
+        __syncthreads();
+    };
+    auto tile4 = [&](int row, int col) {
+        f32x4 v = *reinterpret_cast<const f32x4*>(tile + row * LDT + col);
+#pragma unroll
+        for (int w = 1; w < KS; ++w) v += *reinterpret_cast<const f32x4*>(tile + (w * BM + row) * LDT + col);
+        return v;
+    };
+    if constexpr (KS > 1) {
+        stage_tile();
+        // the summed tile back in the MFMA layout, for the row tiles this wave finishes
+#pragma unroll
+        for (int a = 0; a < FM; ++a)
+#pragma unroll
+            for (int b = 0; b < FN; ++b)
+                if (a % KS == kw) acc[a][b] = tile4(a * 16 + (lane & 15), b * 16 + (lane >> 4) * 4);
+    }
     if (p.epi == EPI_LSTM) {
-        // gates i, f, g, o of unit n / 4 (n is a multiple of 4 and the whole group is valid)
+        // gates i, f, g, o of unit n / 4 (n is a multiple of 4 and the whole group is valid);
+        // with K split across waves, wave w finishes row tiles a = w (mod KS)
         f32x4 g4[FM][FN];
         float cprev[FM][FN];
 #pragma unroll
         for (int a = 0; a < FM; ++a)
 #pragma unroll
             for (int b = 0; b < FN; ++b) {
-                const bool ok = mrow[a] < p.M && nval[b] == 4;
+                const bool ok = a % KS == kw && mrow[a] < p.M && nval[b] == 4;
                 const int64_t mm = ok ? mrow[a] : 0;
                 const int nn = ok ? ncol[b] : 0;
                 g4[a][b] = *reinterpret_cast<const f32x4*>(p.gx + mm * p.ldgx + nn);
@@ -583,7 +632,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const GemmParams p) 
         for (int a = 0; a < FM; ++a)
 #pragma unroll
             for (int b = 0; b < FN; ++b) {
-                if (mrow[a] >= p.M || nval[b] != 4) continue;
+                if (a % KS != kw || mrow[a] >= p.M || nval[b] != 4) continue;
                 const f32x4 v = acc[a][b] + g4[a][b];
                 const float c = sigmoidf_(v[1]) * cprev[a][b] + sigmoidf_(v[0]) * tanhf(v[2]);
                 const int u = ncol[b] >> 2;
@@ -593,21 +642,11 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const GemmParams p) 
         return;
     }
 
-    // Stage the fp32 tile through LDS (row-major, padded rows) so that every thread then
-    // owns whole 8-column chunks: full-line stores, and bias / residual as vector loads.
-    __syncthreads();                          // every wave is done with the operand stages
-    float* tile = reinterpret_cast<float*>(lds);
-#pragma unroll
-    for (int a = 0; a < FM; ++a)
-#pragma unroll
-        for (int b = 0; b < FN; ++b) {
-            const int row = wm * TM + a * 16 + (lane & 15), col = wn * TN + b * 16 + (lane >> 4) * 4;
-            *reinterpret_cast<f32x4*>(tile + row * LDT + col) = acc[a][b];
-        }
-    __syncthreads();
+    // Every thread then owns whole 8-column chunks of the staged tile: full-line stores, and
+    // bias / residual as vector loads.
+    if constexpr (KS == 1) stage_tile();
     auto tile8 = [&](int r, float (&v)[8]) {
-        const f32x4 lo = *reinterpret_cast<const f32x4*>(tile + r * LDT + cc * 8);
-        const f32x4 hi = *reinterpret_cast<const f32x4*>(tile + r * LDT + cc * 8 + 4);
+        const f32x4 lo = tile4(r, cc * 8), hi = tile4(r, cc * 8 + 4);
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = lo[e], v[4 + e] = hi[e];
     };
@@ -718,7 +757,7 @@ int gemm_splits(int64_t M, int N, int K, int dtype, int epi) {
     return s;
 }
 
-template <typename T, int BM, int BN, int WM, int WN, int NS, int KH = 1>
+template <typename T, int BM, int BN, int WM, int WN, int NS, int KH = 1, int KS = 1>
 static hipError_t launch_cfg(const GemmParams& params, int width, hipStream_t st) {
     GemmParams p = params;
     const int64_t mt = (p.M + BM - 1) / BM, nt = (width + BN - 1) / BN;
@@ -747,23 +786,24 @@ static hipError_t launch_cfg(const GemmParams& params, int width, hipStream_t st
         p.div_kw = FastDiv(static_cast<unsigned>(p.kw));
     }
     const int64_t grid = (total + 7) / 8 * 8;
-    const dim3 block(WM * WN * 64);
+    const dim3 block(WM * WN * KS * 64);
     if (p.conv)
-        launch_kernel((gemm_kernel<T, BM, BN, WM, WN, NS, KH, true>), dim3(static_cast<unsigned>(grid)), block, 0, st,
-                      p);
+        launch_kernel((gemm_kernel<T, BM, BN, WM, WN, NS, KH, KS, true>), dim3(static_cast<unsigned>(grid)), block, 0,
+                      st, p);
     else
-        launch_kernel((gemm_kernel<T, BM, BN, WM, WN, NS, KH, false>), dim3(static_cast<unsigned>(grid)), block, 0, st,
-                      p);
+        launch_kernel((gemm_kernel<T, BM, BN, WM, WN, NS, KH, KS, false>), dim3(static_cast<unsigned>(grid)), block, 0,
+                      st, p);
     return hipGetLastError();
 }
 
 template <typename T>
 static hipError_t dispatch(const GemmParams& p, hipStream_t st) {
     const int width = (p.N + p.ksub - 1) / p.ksub;   // widest sub-slice
-    if (p.M <= 16) return launch_cfg<T, 16, 64, 1, 4, 4>(p, width, st);
+    // few rows: the four waves split K (four 64-wide sub-stages per stage) instead of the tile
+    if (p.M <= 16) return launch_cfg<T, 16, 64, 1, 1, 3, 4, 4>(p, width, st);
     if (p.M <= 64 || p.epi == EPI_LSTM) {
-        if (width >= 64 && p.epi != EPI_LSTM) return launch_cfg<T, 64, 64, 2, 4, 4>(p, width, st);
-        return launch_cfg<T, 64, 16, 4, 1, 4>(p, width, st);
+        if (width >= 64 && p.epi != EPI_LSTM) return launch_cfg<T, 64, 64, 1, 1, 2, 4, 4>(p, width, st);
+        return launch_cfg<T, 64, 16, 1, 1, 3, 4, 4>(p, width, st);
     }
     const int64_t mt = (p.M + 127) / 128;
     auto blocks = [&](int64_t bm_tiles, int bn) { return bm_tiles * ((width + bn - 1) / bn) * p.ksub * p.splits; };
