@@ -114,6 +114,11 @@ def seq_ids(b, s):
     ("bf16", 16, 1, 1024, 512, "relu", False, 8),  # M = 16 (fc-like)
     ("bf16", 1, 5, 64, 10, "none", False, 1),      # N = 10
     ("f32", 2, 7, 36, 44, "relu", True, 2),
+    # few rows: K split across the waves of a block, with split-K and a K tail (2000 = 31*64 + 16)
+    ("bf16", 16, 1, 2000, 96, "relu", False, 3),
+    # M = 40: the 64x64 and 64x16 K-split tiles (k = 1 vs k = 4) must agree bit for bit
+    ("bf16", 5, 8, 1504, 70, "gelu", True, 4),
+    ("f32", 4, 4, 700, 33, "none", True, 2),
 ])
 def test_linear_parity_and_subslice_bitwise(dt, b, s, k, nout, act, res, ksub):
     bld, x = seq_input_model(dt, b, s, k)
