@@ -477,7 +477,6 @@ __global__ __launch_bounds__(256) void attention_mfma_kernel(const __bf16* __res
     const int64_t row3 = 3 * static_cast<int64_t>(f);
     const __bf16* base = qkv + static_cast<int64_t>(b) * seq * row3 + h * AM_D;
     const int q0 = qt * AM_Q;
-    const int kpad = (seq + 31) / 32 * 32;          // keys processed (multiple of the k step)
     const uint4 zero4 = make_uint4(0, 0, 0, 0);
     // stage: 8 chunks of 8 dims per row
     for (int i = threadIdx.x; i < AM_Q * 8; i += 256) {
@@ -485,7 +484,10 @@ __global__ __launch_bounds__(256) void attention_mfma_kernel(const __bf16* __res
         const uint4 v = q < seq ? *reinterpret_cast<const uint4*>(base + q * row3 + c * 8) : zero4;
         *reinterpret_cast<uint4*>(&sq[r * AM_LD + c * 8]) = v;
     }
-    for (int i = threadIdx.x; i < kpad * 8; i += 256) {
+    // every key row of the tile is staged (zeros past seq), so the products below run over all
+    // AM_K keys with no data-dependent branches; the softmax masks keys >= seq
+    unsigned short* svt16 = reinterpret_cast<unsigned short*>(svt);
+    for (int i = threadIdx.x; i < AM_K * 8; i += 256) {
         const int r = i >> 3, c = i & 7;
         uint4 kv = zero4, vv = zero4;
         if (r < seq) {
@@ -493,15 +495,17 @@ __global__ __launch_bounds__(256) void attention_mfma_kernel(const __bf16* __res
             vv = *reinterpret_cast<const uint4*>(base + r * row3 + 2 * f + c * 8);
         }
         *reinterpret_cast<uint4*>(&sk[r * AM_LD + c * 8]) = kv;
-        const __bf16* ve = reinterpret_cast<const __bf16*>(&vv);
+        const unsigned w[4] = {vv.x, vv.y, vv.z, vv.w};
 #pragma unroll
-        for (int e = 0; e < 8; ++e) svt[(c * 8 + e) * AM_LP + r] = ve[e];
+        for (int e = 0; e < 4; ++e) {
+            svt16[(c * 8 + 2 * e) * AM_LP + r] = static_cast<unsigned short>(w[e] & 0xffffu);
+            svt16[(c * 8 + 2 * e + 1) * AM_LP + r] = static_cast<unsigned short>(w[e] >> 16);
+        }
     }
     __syncthreads();
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int lr = lane & 15, lg = lane >> 4;          // fragment row, k group
-    const int ntile = kpad / 16;
     // S = Q K^T for query rows wave*16 .. +15
     f32x4_t sacc[AM_K / 16];
 #pragma unroll
@@ -510,11 +514,10 @@ __global__ __launch_bounds__(256) void attention_mfma_kernel(const __bf16* __res
     for (int ks = 0; ks < AM_D / 32; ++ks) {
         const bf16x8_t qa = lds8(&sq[(wave * 16 + lr) * AM_LD + ks * 32 + lg * 8]);
 #pragma unroll
-        for (int t = 0; t < AM_K / 16; ++t)
-            if (t < ntile) {
-                const bf16x8_t kb = lds8(&sk[(t * 16 + lr) * AM_LD + ks * 32 + lg * 8]);
-                sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb, qa, sacc[t], 0, 0, 0);
-            }
+        for (int t = 0; t < AM_K / 16; ++t) {
+            const bf16x8_t kb = lds8(&sk[(t * 16 + lr) * AM_LD + ks * 32 + lg * 8]);
+            sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb, qa, sacc[t], 0, 0, 0);
+        }
     }
     // softmax over the keys of row lr: this lane holds keys 16 t + 4 lg + e
     float mx = -INFINITY;
@@ -523,7 +526,7 @@ __global__ __launch_bounds__(256) void attention_mfma_kernel(const __bf16* __res
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int key = t * 16 + lg * 4 + e;
-            if (t >= ntile || key >= seq) sacc[t][e] = -INFINITY;
+            if (key >= seq) sacc[t][e] = -INFINITY;
             mx = fmaxf(mx, sacc[t][e]);
         }
     mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
@@ -532,7 +535,6 @@ __global__ __launch_bounds__(256) void attention_mfma_kernel(const __bf16* __res
     __bf16* prow = &sp[(wave * 16 + lr) * AM_LP];
 #pragma unroll
     for (int t = 0; t < AM_K / 16; ++t) {
-        if (t >= ntile) continue;
         float pe[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -549,7 +551,8 @@ __global__ __launch_bounds__(256) void attention_mfma_kernel(const __bf16* __res
     f32x4_t oacc[AM_D / 16];
 #pragma unroll
     for (int dt = 0; dt < AM_D / 16; ++dt) oacc[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    for (int ks = 0; ks < kpad / 32; ++ks) {
+#pragma unroll
+    for (int ks = 0; ks < AM_K / 32; ++ks) {
         const bf16x8_t pa = lds8(&sp[(wave * 16 + lr) * AM_LP + ks * 32 + lg * 8]);
 #pragma unroll
         for (int dt = 0; dt < AM_D / 16; ++dt) {
