@@ -465,13 +465,19 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ bf16x8_t lds8(const __bf16* p) { return *reinterpret_cast<const bf16x8_t*>(p); }
 
 __global__ __launch_bounds__(256) void attention_mfma_kernel(const __bf16* __restrict__ qkv, __bf16* __restrict__ y,
-                                                             int seq, int heads, float scale) {
+                                                             int seq, int heads, float scale, int n_tiles) {
     __shared__ __attribute__((aligned(16))) __bf16 sq[AM_Q * AM_LD];
     __shared__ __attribute__((aligned(16))) __bf16 sk[AM_K * AM_LD];
     __shared__ __attribute__((aligned(16))) __bf16 svt[AM_D * AM_LP];
     __shared__ __attribute__((aligned(16))) __bf16 sp[4 * 16 * AM_LP];
+    // The XCDs take blocks round-robin: number the tiles so that each XCD runs a contiguous
+    // range, and the query tiles of one (batch, head) -- which read the same K and V -- run
+    // on the same XCD at about the same time, K and V coming from its L2 after the first.
     const int qtiles = (seq + AM_Q - 1) / AM_Q;
-    const int qt = blockIdx.x % qtiles, bh = blockIdx.x / qtiles;
+    const int tiles = gridDim.x;                       // a multiple of 8 (padded by the launcher)
+    const int ti = static_cast<int>(blockIdx.x % 8) * (tiles / 8) + static_cast<int>(blockIdx.x / 8);
+    if (ti >= n_tiles) return;
+    const int qt = ti % qtiles, bh = ti / qtiles;
     const int b = bh / heads, h = bh % heads;
     const int f = heads * AM_D;
     const int64_t row3 = 3 * static_cast<int64_t>(f);
@@ -575,12 +581,14 @@ __global__ __launch_bounds__(256) void attention_mfma_kernel(const __bf16* __res
 hipError_t launch_attention(const void* qkv, void* y, int batch, int seq, int heads, float scale, int dtype,
                             hipStream_t s) {
     if (seq < 1 || seq > AM_K) return hipErrorInvalidValue;
-    if (dtype == MOPAR_BF16)
-        launch_kernel(attention_mfma_kernel, dim3(batch * heads * ((seq + AM_Q - 1) / AM_Q)), dim3(256), 0, s,
-                      static_cast<const __bf16*>(qkv), static_cast<__bf16*>(y), seq, heads, scale);
-    else
+    if (dtype == MOPAR_BF16) {
+        const int n_tiles = batch * heads * ((seq + AM_Q - 1) / AM_Q);
+        launch_kernel(attention_mfma_kernel, dim3((n_tiles + 7) / 8 * 8), dim3(256), 0, s,
+                      static_cast<const __bf16*>(qkv), static_cast<__bf16*>(y), seq, heads, scale, n_tiles);
+    } else {
         launch_kernel(attention_kernel<float>, dim3(batch * heads), dim3(ATT_MAXS), 0, s,
-                           static_cast<const float*>(qkv), static_cast<float*>(y), seq, heads, scale);
+                      static_cast<const float*>(qkv), static_cast<float*>(y), seq, heads, scale);
+    }
     return hipGetLastError();
 }
 
