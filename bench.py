@@ -159,8 +159,9 @@ def main():
     ap.add_argument("--op-report", action="store_true", help="print per-op times (ms) to stderr")
     ap.add_argument("--pipeline", type=int, default=2, metavar="D",
                     help="run batches through the slice pipeline with D code slots per cut (0: sequential)")
-    ap.add_argument("--replicas", type=int, default=3,
-                    help="pipeline instances of the sliced model (3 instances + torch's stream = 4 hardware queues)")
+    ap.add_argument("--replicas", type=int, default=0,
+                    help="pipeline instances of the sliced model; 0: try 1, 2 and 3 before the timed region "
+                         "and keep the fastest (3 instances + torch's stream = 4 hardware queues)")
     ap.add_argument("--stream-per-slice", type=int, default=0, help="1: one stream per slice, 0: one per instance")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run a raw boundary copy of this many MiB per step (counter calibration)")
@@ -252,15 +253,39 @@ def main():
     torch.cuda.synchronize()
 
     pipe = None
+    replicas, replica_tuning = args.replicas, None
     if args.pipeline:
-        pipe = sm.pipeline(plan, args.codec, cw, depth=args.pipeline, replicas=args.replicas,
-                           stream_per_slice=bool(args.stream_per_slice))
+        def make_pipe(r):
+            return sm.pipeline(plan, args.codec, cw, depth=args.pipeline, replicas=r,
+                               stream_per_slice=bool(args.stream_per_slice))
 
-        def pstep():
+        def pstep_on(pp):
             prof = prof_fixed or sm.profile()
             pl = P.mopar_plan_slices(prof, **plan_kw)
-            pipe.submit(x, out)
+            pp.submit(x, out)
             return pl
+
+        if replicas == 0:
+            # instance count: each candidate warmed up, then timed over a few steps, before
+            # (and outside) the timed region
+            replica_tuning = {}
+            n_try = max(5, min(args.steps, 10))
+            for r in (1, 2, 3):
+                pp = make_pipe(r)
+                for _ in range(max(args.warmup, 2)):
+                    pstep_on(pp)
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                for _ in range(n_try):
+                    pstep_on(pp)
+                torch.cuda.synchronize()
+                replica_tuning[r] = round(m.batch * n_try / (time.perf_counter() - t0), 1)
+                del pp
+            replicas = max(replica_tuning, key=replica_tuning.get)
+        pipe = make_pipe(replicas)
+
+        def pstep():
+            return pstep_on(pipe)
 
         for _ in range(args.warmup):
             pstep()
@@ -311,9 +336,11 @@ def main():
                    "batch": m.batch, "slices": plan.n_slices, "k": plan.k, "codec": args.codec},
         "latency_ms": {"p50": round(statistics.median(per_step), 4),
                        "p95": round(float(np.percentile(per_step, 95)), 4)},
-        "mode": (f"slice pipeline: {args.replicas} instance(s) x {plan.n_slices} slices on "
+        "mode": (f"slice pipeline: {replicas} instance(s) x {plan.n_slices} slices on "
                  f"{len(set(id(s) for s in pipe.streams))} streams, {args.pipeline} code slots per (instance, cut); "
                  f"latency_ms is one batch at a time") if pipe else "sequential: one batch at a time",
+        "replicas": replicas if pipe else None,
+        "replica_tuning_inf_per_s": replica_tuning,
         "wall_s_timed_region": round(wall, 4),
         "sequential_value": round(seq_value, 2),
         "host_plan_us": round(plan_us, 1),
