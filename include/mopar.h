@@ -21,6 +21,11 @@
  * Streams.   `stream` is a hipStream_t passed as void* (NULL = the default
  *            stream).  Work is enqueued asynchronously in call order.
  * Alignment. Device pointers must be 16-byte aligned.
+ * Sizes.     Every GEMM operand -- an op's input activation (for a conv, the
+ *            whole input image batch), its weight matrix, a boundary tensor
+ *            and its code -- must stay under 2 GiB; a model or codec that
+ *            needs more is rejected with MOPAR_E_UNSUPPORTED before anything
+ *            is enqueued.
  * Layouts.   Tensor descriptors give logical dims in canonical order:
  *            images (N, C, H, W), flattened (N, F), sequences (B, S, F),
  *            token ids (B, S).  Physically, the model input is stored as

@@ -128,6 +128,12 @@ enum { EPI_STD = 0, EPI_LSTM = 1 };
 
 hipError_t launch_gemm(const GemmParams& p, int dtype, hipStream_t stream);
 
+// The GEMM reads its operands through buffer resources with 32-bit offsets and uses offset
+// 2^31 as its out-of-range marker: A (the whole image for a conv) and B must stay below it.
+inline bool gemm_operands_fit(int64_t a_bytes, int64_t b_bytes) {
+    return a_bytes < (int64_t(1) << 31) && b_bytes < (int64_t(1) << 31);
+}
+
 // NCHW float32 -> NHWC (model dtype), channels padded with zeros to cs.
 hipError_t launch_nchw_to_nhwc(const float* x, void* y, int n, int c, int h, int w, int cs, int dtype,
                                hipStream_t s);

@@ -332,6 +332,8 @@ static int validate_and_build(mopar_model_s& m) {
                 inf.cs = static_cast<int>(xin ? round_up(x.dims[1], epc) : x.dims[1]);
                 inf.K = static_cast<int64_t>(op.kh) * op.kw * inf.cs;
                 inf.M = x.dims[0] * ho * wo;
+                if (!gemm_operands_fit(x.dims[0] * x.dims[2] * x.dims[3] * inf.cs * es, op.n_out * inf.K * es))
+                    return set_error(MOPAR_E_UNSUPPORTED, nm + ": a GEMM operand reaches 2 GiB");
                 if (!wcheck(op.w, op.n_out * inf.K, "w") || !wcheck(op.b, op.n_out, "b"))
                     return set_error(MOPAR_E_ARG, nm + ": weight offsets out of range or not 16-byte aligned");
                 if (xin) inf.temps.push_back(static_cast<size_t>(x.dims[0] * x.dims[2] * x.dims[3] * inf.cs) * es);
@@ -352,6 +354,8 @@ static int validate_and_build(mopar_model_s& m) {
                 if (op.in1 >= 0 && numel(m.tensors[op.in1]) != numel(y))
                     return set_error(MOPAR_E_SHAPE, nm + ": residual shape");
                 if (K % epc != 0) return set_error(MOPAR_E_UNSUPPORTED, nm + ": K must be a multiple of " + std::to_string(epc));
+                if (!gemm_operands_fit(M * K * es, op.n_out * K * es))
+                    return set_error(MOPAR_E_UNSUPPORTED, nm + ": a GEMM operand reaches 2 GiB");
                 inf.K = K;
                 inf.M = M;
                 if (!wcheck(op.w, op.n_out * K, "w") || !wcheck(op.b, op.n_out, "b"))
@@ -423,6 +427,8 @@ static int validate_and_build(mopar_model_s& m) {
                     !wcheck(op.w3, 4 * h, "b_hh"))
                     return set_error(MOPAR_E_ARG, nm + ": weight offsets out of range or not 16-byte aligned");
                 const int64_t bt = x.dims[0] * x.dims[1];
+                if (!gemm_operands_fit(bt * std::max(e, h) * es, 4 * h * std::max(e, h) * es))
+                    return set_error(MOPAR_E_UNSUPPORTED, nm + ": a GEMM operand reaches 2 GiB");
                 inf.temps.push_back(static_cast<size_t>(bt * 4 * h) * 4);       // input projection, f32
                 inf.temps.push_back(static_cast<size_t>(x.dims[0] * h) * 4);    // cell state, f32
                 inf.temps.push_back(static_cast<size_t>(x.dims[0] * h) * es);   // h_0 = 0
@@ -870,6 +876,9 @@ static int codec_geometry(const mopar_codec* c, const mopar_tensor_desc* x, int6
         return set_error(MOPAR_E_UNSUPPORTED, std::string(who) + ": c and c_code must be multiples of " +
                                                   std::to_string(g));
     if (!c->w_enc || !c->w_dec) return set_error(MOPAR_E_ARG, std::string(who) + ": null codec weights");
+    const int64_t es = elt_bytes(x->dtype);
+    if (!gemm_operands_fit(*positions * std::max<int64_t>(ch, c->c_code) * es, int64_t(c->c_code) * ch * es))
+        return set_error(MOPAR_E_UNSUPPORTED, std::string(who) + ": a codec GEMM operand reaches 2 GiB");
     return MOPAR_OK;
 }
 

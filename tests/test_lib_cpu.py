@@ -148,6 +148,27 @@ def test_model_create_validation_errors():
     assert b"op" in P.lib().mopar_last_error()
 
 
+def test_gemm_operand_of_2gib_rejected_at_create():
+    """A GEMM operand of 2 GiB or more (here a 1x1 conv's input image batch) is rejected when
+    the model is created, before anything could be enqueued."""
+    bld = synth._Builder("big", "bf16", 1, 7)
+    x = bld.tensor((1, 8, 16384, 16384), "f32")
+    bld.new_layer("L0")
+    y = bld.conv(x, 8, 1, 1, 0, "none", "c")
+    m = bld.finish(y, 1)
+    tens, ops, blob = P.binding._pack(m)
+    host = np.zeros(blob.size, dtype=np.uint8)
+    d = L.ModelDesc()
+    d.dtype = L.MOPAR_BF16
+    d.n_tensors, d.tensors = len(m.tensors), ctypes.cast(tens, ctypes.POINTER(L.TensorDesc))
+    d.n_ops, d.ops = len(m.ops), ctypes.cast(ops, ctypes.POINTER(L.Op))
+    d.n_layers, d.input, d.output = len(m.layers), m.input_tid, m.output_tid
+    h = ctypes.c_void_p()
+    st = P.lib().mopar_model_create(ctypes.byref(d), host.ctypes.data_as(ctypes.c_void_p), blob.size, ctypes.byref(h))
+    assert st == L.MOPAR_E_UNSUPPORTED
+    assert b"2 GiB" in P.lib().mopar_last_error()
+
+
 def test_plan_model_mismatch_rejected():
     m = synth.build(1)
     sm = P.SlicedModel(m, device="cpu")
