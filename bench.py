@@ -163,6 +163,8 @@ def main():
                     help="pipeline instances of the sliced model; 0: try 1, 2 and 3 before the timed region "
                          "and keep the fastest (3 instances + torch's stream = 4 hardware queues)")
     ap.add_argument("--stream-per-slice", type=int, default=0, help="1: one stream per slice, 0: one per instance")
+    ap.add_argument("--no-graphs", action="store_true",
+                    help="launch the pipeline's kernels one by one instead of replaying captured HIP graphs")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run a raw boundary copy of this many MiB per step (counter calibration)")
     ap.add_argument("--plan", choices=["config", "measured"], default="config",
@@ -255,9 +257,12 @@ def main():
     pipe = None
     replicas, replica_tuning = args.replicas, None
     if args.pipeline:
+        use_graphs = not args.no_graphs and not args.stream_per_slice
+
         def make_pipe(r):
-            return sm.pipeline(plan, args.codec, cw, depth=args.pipeline, replicas=r,
-                               stream_per_slice=bool(args.stream_per_slice))
+            pp = sm.pipeline(plan, args.codec, cw, depth=args.pipeline, replicas=r,
+                             stream_per_slice=bool(args.stream_per_slice))
+            return pp.use_graphs(True) if use_graphs else pp
 
         def pstep_on(pp):
             prof = prof_fixed or sm.profile()
@@ -269,10 +274,10 @@ def main():
             # instance count: each candidate warmed up, then timed over a few steps, before
             # (and outside) the timed region
             replica_tuning = {}
-            n_try = max(5, min(args.steps, 10))
+            n_try = max(10, min(args.steps, 20))
             for r in (1, 2, 3):
                 pp = make_pipe(r)
-                for _ in range(max(args.warmup, 2)):
+                for _ in range(max(args.warmup, 5)):
                     pstep_on(pp)
                 torch.cuda.synchronize()
                 t0 = time.perf_counter()
@@ -340,6 +345,7 @@ def main():
                  f"{len(set(id(s) for s in pipe.streams))} streams, {args.pipeline} code slots per (instance, cut); "
                  f"latency_ms is one batch at a time") if pipe else "sequential: one batch at a time",
         "replicas": replicas if pipe else None,
+        "graphs": bool(pipe) and not args.no_graphs and not args.stream_per_slice,
         "replica_tuning_inf_per_s": replica_tuning,
         "wall_s_timed_region": round(wall, 4),
         "sequential_value": round(seq_value, 2),

@@ -335,6 +335,21 @@ int mopar_pipeline_create(mopar_model_t model, const mopar_plan* plan, const mop
  * finished this batch (e.g. synchronise that stream).  Never blocks. */
 int mopar_pipeline_submit(mopar_pipeline_t pipe, const void* in_dev, void* out_dev);
 
+/* Graph replay (HIP graphs; off by default).  With `enable` set, each later
+ * mopar_pipeline_submit replays an executable graph of the batch's kernels
+ * instead of launching them one by one: the graph of a (ring slot, in_dev,
+ * out_dev) triple is captured from the instance's stream the first time that
+ * triple is submitted (nothing runs during capture) and kept until the
+ * pipeline is destroyed or graphs are disabled; each distinct triple adds one
+ * graph.  Replays run exactly the kernels of an ordinary submit, so outputs
+ * are bitwise identical.  Needs every instance to run all of its slices on one
+ * stream (the cross-stream events are then implied by stream order):
+ * otherwise MOPAR_E_UNSUPPORTED.  `enable` = 0 destroys the cached graphs --
+ * only once the batches submitted with them have finished.
+ * Errors: MOPAR_E_ARG (null pipeline), MOPAR_E_UNSUPPORTED, and MOPAR_E_HIP
+ * from a later submit if capture or instantiation fails. */
+int mopar_pipeline_use_graphs(mopar_pipeline_t pipe, int32_t enable);
+
 /* Destroy the pipeline's events; the caller must have synchronised its streams. */
 void mopar_pipeline_destroy(mopar_pipeline_t pipe);
 

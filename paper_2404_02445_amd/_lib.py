@@ -87,6 +87,7 @@ SIGNATURES = {
                                       ctypes.POINTER(c_vp), c_vp, ctypes.c_size_t, ctypes.POINTER(c_vp),
                                       ctypes.POINTER(c_vp)]),
     "mopar_pipeline_submit": (c_i32, [c_vp, c_vp, c_vp]),
+    "mopar_pipeline_use_graphs": (c_i32, [c_vp, c_i32]),
     "mopar_pipeline_destroy": (None, [c_vp]),
     "mopar_model_set_timing": (c_i32, [c_vp, c_i32]),
     "mopar_model_timing_slots": (c_i32, [c_vp, ctypes.POINTER(c_i32)]),

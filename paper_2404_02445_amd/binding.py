@@ -448,6 +448,13 @@ class SlicePipeline:
         check(lib().mopar_pipeline_submit(self.handle, _ptr(x), _ptr(out)))
         return out
 
+    def use_graphs(self, enable=True):
+        """Replay captured HIP graphs for later submits (needs one stream per instance)."""
+        if not enable:
+            self.synchronize()
+        check(lib().mopar_pipeline_use_graphs(self.handle, 1 if enable else 0))
+        return self
+
     def synchronize(self):
         for s in self.streams:
             s.synchronize()

@@ -24,6 +24,7 @@ int pipeline_ws_bytes_impl(const mopar_model_s*, const mopar_plan*, int32_t, siz
 int pipeline_create_impl(const mopar_model_s*, const mopar_plan*, const mopar_codec*, int32_t, int32_t, void* const*,
                          void*, size_t, void* const*, mopar_pipeline_t*);
 int pipeline_submit_impl(mopar_pipeline_s*, const void*, void*);
+int pipeline_use_graphs_impl(mopar_pipeline_s*, int32_t);
 void pipeline_destroy_impl(mopar_pipeline_s*);
 int set_timing_impl(mopar_model_s*, int32_t);
 int timing_slots_impl(const mopar_model_s*, int32_t*);
@@ -130,6 +131,10 @@ int mopar_pipeline_create(mopar_model_t model, const mopar_plan* plan, const mop
 
 int mopar_pipeline_submit(mopar_pipeline_t pipe, const void* in_dev, void* out_dev) {
     return guarded("mopar_pipeline_submit", [&] { return pipeline_submit_impl(pipe, in_dev, out_dev); });
+}
+
+int mopar_pipeline_use_graphs(mopar_pipeline_t pipe, int32_t enable) {
+    return guarded("mopar_pipeline_use_graphs", [&] { return pipeline_use_graphs_impl(pipe, enable); });
 }
 
 void mopar_pipeline_destroy(mopar_pipeline_t pipe) { pipeline_destroy_impl(pipe); }

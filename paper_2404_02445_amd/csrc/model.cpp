@@ -1023,7 +1023,21 @@ struct mopar_pipeline_s {
     std::vector<void*> codes;                      // [replicas][depth][nb]
     std::vector<hipEvent_t> enc_done, dec_done;    // [replicas][depth][S-1]
     int64_t submitted = 0;
+    // graph replay: one executable graph per (ring slot, input, output), captured on first use
+    bool graphs = false;
+    struct Graph {
+        int slot;
+        const void* in;
+        void* out;
+        hipGraphExec_t exec;
+    };
+    std::vector<Graph> gexec;
+    void drop_graphs() {
+        for (auto& g : gexec) (void)hipGraphExecDestroy(g.exec);
+        gexec.clear();
+    }
     ~mopar_pipeline_s() {
+        drop_graphs();
         for (auto e : enc_done) (void)hipEventDestroy(e);
         for (auto e : dec_done) (void)hipEventDestroy(e);
     }
@@ -1113,13 +1127,12 @@ int pipeline_create_impl(const mopar_model_s* m, const mopar_plan* p, const mopa
     return MOPAR_OK;
 }
 
-int pipeline_submit_impl(mopar_pipeline_s* pp, const void* in, void* out) {
-    if (!pp) return set_error(MOPAR_E_ARG, "mopar_pipeline_submit: null pipeline");
-    if (!in || !out) return set_error(MOPAR_E_ARG, "mopar_pipeline_submit: null input or output");
+// Enqueue batch `in` -> `out` on instance `rep`, ring slot `r`.  `events` = false leaves out the
+// cross-stream events: valid when the instance runs all its slices on one stream, whose order
+// then already puts slice s after slice s-1 and a slot's encode after its previous decode.
+static int enqueue_batch(mopar_pipeline_s* pp, int rep, int r, const void* in, void* out, bool events) {
     const mopar_model_s& m = *pp->m;
     const int S = pp->S, ncut = S - 1;
-    const int rep = static_cast<int>(pp->submitted % pp->replicas);               // instance
-    const int r = static_cast<int>((pp->submitted / pp->replicas) % pp->depth) + rep * pp->depth;  // ring slot
     int l0 = 0;
     for (int s = 0; s < S; ++s) {
         const int l1 = pp->slice_end[s];
@@ -1145,12 +1158,16 @@ int pipeline_submit_impl(mopar_pipeline_s* pp, const void* in, void* out) {
         };
         if (s > 0) {
             const int c = s - 1, slot = r * ncut + c;
-            rc = hip_check(hipStreamWaitEvent(st, pp->enc_done[slot], 0), "hipStreamWaitEvent");
-            if (rc) return rc;
+            if (events) {
+                rc = hip_check(hipStreamWaitEvent(st, pp->enc_done[slot], 0), "hipStreamWaitEvent");
+                if (rc) return rc;
+            }
             rc = hip_check(hand_off(c, false), "boundary decode");
             if (rc) return rc;
-            rc = hip_check(hipEventRecord(pp->dec_done[slot], st), "hipEventRecord");
-            if (rc) return rc;
+            if (events) {
+                rc = hip_check(hipEventRecord(pp->dec_done[slot], st), "hipEventRecord");
+                if (rc) return rc;
+            }
         }
         for (int l = l0; l <= l1; ++l)
             for (int i = m.layer_first[l]; i <= m.layer_last[l]; ++i) {
@@ -1161,16 +1178,68 @@ int pipeline_submit_impl(mopar_pipeline_s* pp, const void* in, void* out) {
         if (s < S - 1) {
             const int c = s, slot = r * ncut + c;
             // the slot is free once the previous batch using it has been decoded
-            rc = hip_check(hipStreamWaitEvent(st, pp->dec_done[slot], 0), "hipStreamWaitEvent");
-            if (rc) return rc;
+            if (events) {
+                rc = hip_check(hipStreamWaitEvent(st, pp->dec_done[slot], 0), "hipStreamWaitEvent");
+                if (rc) return rc;
+            }
             rc = hip_check(hand_off(c, true), "boundary encode");
             if (rc) return rc;
-            rc = hip_check(hipEventRecord(pp->enc_done[slot], st), "hipEventRecord");
-            if (rc) return rc;
+            if (events) {
+                rc = hip_check(hipEventRecord(pp->enc_done[slot], st), "hipEventRecord");
+                if (rc) return rc;
+            }
         }
         l0 = l1 + 1;
     }
+    return MOPAR_OK;
+}
+
+int pipeline_submit_impl(mopar_pipeline_s* pp, const void* in, void* out) {
+    if (!pp) return set_error(MOPAR_E_ARG, "mopar_pipeline_submit: null pipeline");
+    if (!in || !out) return set_error(MOPAR_E_ARG, "mopar_pipeline_submit: null input or output");
+    const int rep = static_cast<int>(pp->submitted % pp->replicas);               // instance
+    const int r = static_cast<int>((pp->submitted / pp->replicas) % pp->depth) + rep * pp->depth;  // ring slot
+    if (!pp->graphs) {
+        const int rc = enqueue_batch(pp, rep, r, in, out, true);
+        if (rc) return rc;
+        ++pp->submitted;
+        return MOPAR_OK;
+    }
+    const hipStream_t st = pp->streams[rep * pp->S];
+    hipGraphExec_t exec = nullptr;
+    for (const auto& g : pp->gexec)
+        if (g.slot == r && g.in == in && g.out == out) exec = g.exec;
+    if (!exec) {
+        // capture the batch's kernels once; nothing reaches the GPU until the launch below
+        int rc = hip_check(hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal), "hipStreamBeginCapture");
+        if (rc) return rc;
+        rc = enqueue_batch(pp, rep, r, in, out, false);
+        hipGraph_t graph = nullptr;
+        const hipError_t e = hipStreamEndCapture(st, &graph);
+        if (rc == MOPAR_OK) rc = hip_check(e, "hipStreamEndCapture");
+        if (rc == MOPAR_OK) rc = hip_check(hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0), "hipGraphInstantiate");
+        if (graph) (void)hipGraphDestroy(graph);
+        if (rc) return rc;
+        pp->gexec.push_back({r, in, out, exec});
+    }
+    const int rc = hip_check(hipGraphLaunch(exec, st), "hipGraphLaunch");
+    if (rc) return rc;
     ++pp->submitted;
+    return MOPAR_OK;
+}
+
+int pipeline_use_graphs_impl(mopar_pipeline_s* pp, int32_t enable) {
+    if (!pp) return set_error(MOPAR_E_ARG, "mopar_pipeline_use_graphs: null pipeline");
+    if (enable) {
+        for (int rep = 0; rep < pp->replicas; ++rep)
+            for (int s = 1; s < pp->S; ++s)
+                if (pp->streams[rep * pp->S + s] != pp->streams[rep * pp->S])
+                    return set_error(MOPAR_E_UNSUPPORTED,
+                                     "mopar_pipeline_use_graphs: an instance runs its slices on several streams");
+    } else {
+        pp->drop_graphs();
+    }
+    pp->graphs = enable != 0;
     return MOPAR_OK;
 }
 
