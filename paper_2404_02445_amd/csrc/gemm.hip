@@ -158,6 +158,47 @@ __device__ __forceinline__ void load8(const T* p, int64_t i, int nvalid, float (
     for (int q = 0; q < 8; ++q) v[q] = (p && q < nvalid) ? ld_f(p, i + q) : 0.0f;
 }
 
+// four consecutive elements as raw bits (8 bytes for bf16, 16 for float)
+template <typename T> struct Raw4Sel { using type = uint4; };
+template <> struct Raw4Sel<__bf16> { using type = uint2; };
+template <typename T> using Raw4 = typename Raw4Sel<T>::type;
+
+// the 4 elements at q (8-byte aligned for bf16, 16 for float), or zeros from the zero page when
+// q is null: one unconditional load either way
+template <typename T>
+__device__ __forceinline__ Raw4<T> load_raw4(const T* q, const void* zero_page) {
+    // through a global-address-space pointer, so it is a global (not flat) load
+    const void* src = q ? static_cast<const void*>(q) : zero_page;
+    Raw4<T> r;
+    if constexpr (sizeof(T) == 2) {
+        const unsigned long long v = *(const __attribute__((address_space(1))) unsigned long long*)(src);
+        r.x = static_cast<unsigned>(v);
+        r.y = static_cast<unsigned>(v >> 32);
+    } else {
+        typedef unsigned w4_t __attribute__((ext_vector_type(4)));
+        const w4_t v = *(const __attribute__((address_space(1))) w4_t*)(src);
+        r.x = v[0], r.y = v[1], r.z = v[2], r.w = v[3];
+    }
+    return r;
+}
+template <typename T>
+__device__ __forceinline__ void unpack4(const Raw4<T>& r, float (&v)[4]) {
+    if constexpr (sizeof(T) == 2) {
+        v[0] = __uint_as_float(r.x << 16);
+        v[1] = __uint_as_float(r.x & 0xffff0000u);
+        v[2] = __uint_as_float(r.y << 16);
+        v[3] = __uint_as_float(r.y & 0xffff0000u);
+    } else {
+        v[0] = __uint_as_float(r.x), v[1] = __uint_as_float(r.y), v[2] = __uint_as_float(r.z), v[3] = __uint_as_float(r.w);
+    }
+}
+// p[i .. i+nvalid-1] (zeros after them, and everywhere when p is null), element by element
+template <typename T>
+__device__ __forceinline__ void ld4_or_zero(const T* p, int64_t i, int nvalid, float (&v)[4]) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = (p && q < nvalid) ? ld_f(p, i + q) : 0.0f;
+}
+
 // the 16 (bf16) or 32 (float) bytes at q, or zeros from the zero page when q is null: one
 // unconditional load either way
 template <typename T>
@@ -430,8 +471,8 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
 #pragma unroll
         for (int b = 0; b < FN; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // --- epilogue operands, fetched now so their latency hides under the main loop ---------
-    // MFMA layout (used by the LSTM cell): lane holds row mrow[a], columns ncol[b]..+3
+    // --- epilogue set-up ---------------------------------------------------------------------
+    // MFMA layout: lane holds row mrow[a], columns ncol[b]..+3
     int64_t mrow[FM];
     int ncol[FN], nval[FN];
 #pragma unroll
@@ -448,30 +489,59 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
     const int c0 = n0 + cc * 8;
     const int cval = max(0, min(8, n_hi - c0));
     const bool direct = p.splits == 1 && p.epi == EPI_STD;   // this block finishes its outputs
-    // Epilogue operands (bias, second bias, residual), fetched now as raw bits so their
-    // latency hides under the main loop.  Each is one unconditional 16-byte load -- from the
-    // zero page when the chunk is absent, partial or misaligned -- so no branch makes the
-    // wave wait for it here; partial chunks are read element by element in the epilogue.
+    // A direct launch starts its accumulators at (bias + second bias) + residual.  Their raw
+    // bits (MFMA layout: 4 columns of one row per lane and fragment) are loaded here, before the
+    // operand stages, and added after the prologue: the latency hides under the first stage's,
+    // and no branch makes the wave wait for them early.  Each is one unconditional load, from
+    // the zero page when absent; partial or misaligned column groups are read element by
+    // element when added.  With K split across waves only wave 0 starts from them.
     const T* biasp = static_cast<const T*>(p.bias);
     const T* bias2p = static_cast<const T*>(p.bias2);
     const T* resp = static_cast<const T*>(p.res);
-    const bool bfast = cval == 8 && (!biasp || aligned16(biasp + c0)) && (!bias2p || aligned16(bias2p + c0));
-    const Raw8<T> braw = load_raw8<T>(direct && bfast && biasp ? biasp + c0 : nullptr, kZeroChunk);
-    const Raw8<T> b2raw = load_raw8<T>(direct && bfast && bias2p ? bias2p + c0 : nullptr, kZeroChunk);
-    Raw8<T> rraw[NCH];
-    bool rfast[NCH];
+    const bool init_here = direct && (KS == 1 || kw == 0);
+    Raw4<T> rb[FN], rb2[FN], rres[FM][FN];
+    bool bfast[FN], rfast[FM][FN];
 #pragma unroll
-    for (int i = 0; i < NCH; ++i) {
-        const int64_t m = m0 + cr + i * RPP;
-        const int64_t idx = m * p.ldc + c0;
-        rfast[i] = direct && resp && cr + i * RPP < BM && m < p.M && cval == 8 && aligned16(resp + idx);
-        rraw[i] = load_raw8<T>(rfast[i] ? resp + idx : nullptr, kZeroChunk);
+    for (int b = 0; b < FN; ++b) {
+        bfast[b] = nval[b] == 4;
+        rb[b] = load_raw4<T>(init_here && bfast[b] && biasp ? biasp + ncol[b] : nullptr, kZeroChunk);
+        rb2[b] = load_raw4<T>(init_here && bfast[b] && bias2p ? bias2p + ncol[b] : nullptr, kZeroChunk);
+#pragma unroll
+        for (int a = 0; a < FM; ++a) {
+            rfast[a][b] = bfast[b] && mrow[a] < p.M && ((mrow[a] * p.ldc + ncol[b]) & 3) == 0;
+            rres[a][b] = load_raw4<T>(init_here && rfast[a][b] && resp ? resp + mrow[a] * p.ldc + ncol[b] : nullptr,
+                                    kZeroChunk);
+        }
     }
 
     // prologue: NS-1 stages in flight (coordinates then stand at stage NS - 1)
 #pragma unroll
     for (int s = 0; s < NS - 1; ++s)
         if (s < nst) issue_stage(s, s);
+
+    if (init_here) {
+#pragma unroll
+        for (int b = 0; b < FN; ++b) {
+            float bv[4], b2v[4];
+            if (bfast[b]) {
+                unpack4<T>(rb[b], bv);
+                unpack4<T>(rb2[b], b2v);
+            } else {
+                ld4_or_zero<T>(biasp, ncol[b], nval[b], bv);
+                ld4_or_zero<T>(bias2p, ncol[b], nval[b], b2v);
+            }
+#pragma unroll
+            for (int a = 0; a < FM; ++a) {
+                float rv[4];
+                if (rfast[a][b])
+                    unpack4<T>(rres[a][b], rv);
+                else
+                    ld4_or_zero<T>(mrow[a] < p.M ? resp : nullptr, mrow[a] * p.ldc + ncol[b], nval[b], rv);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) acc[a][b][e] = (bv[e] + b2v[e]) + rv[e];
+            }
+        }
+    }
 
     // LDS byte addresses of this lane's MFMA fragments (row l % 16 of a 16-row block, chunk
     // 4 * ks + l / 16) in stage buffer 0, sub-stage 0, for the wave's first A and B rows;
@@ -650,49 +720,22 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = lo[e], v[4 + e] = hi[e];
     };
-    // (v + bias) + residual, activation, store: the same operations, in the same order,
-    // whether the sums come from this block or from the split-K partials
-    auto finish = [&](int64_t m, float (&v)[8], const float (&bias8)[8], const float (&rsd)[8]) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = act_f((v[e] + bias8[e]) + rsd[e], p.act);
-        const int64_t idx = m * p.ldc + c0;
-        if (p.out_f32)
-            store8<float>(static_cast<float*>(p.C), idx, v, cval);
-        else
-            store8<T>(static_cast<T*>(p.C), idx, v, cval);
-    };
-
     if (direct) {
-        float bias8[8];
-        if (bfast) {
-            unpack8<T>(braw, bias8);
-            if (bias2p) {
-                float t8[8];
-                unpack8<T>(b2raw, t8);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) bias8[e] += t8[e];
-            }
-        } else {
-            load8<T>(biasp, c0, cval, bias8);
-            if (bias2p) {
-                float t8[8];
-                load8<T>(bias2p, c0, cval, t8);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) bias8[e] += t8[e];
-            }
-        }
+        // bias and residual are already in the sums: activation and store only
 #pragma unroll
         for (int i = 0; i < NCH; ++i) {
             const int r = cr + i * RPP;
             const int64_t m = m0 + r;
             if (r >= BM || m >= p.M || cval == 0) continue;
-            float v[8], rsd[8];
+            float v[8];
             tile8(r, v);
-            if (rfast[i])
-                unpack8<T>(rraw[i], rsd);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = act_f(v[e], p.act);
+            const int64_t idx = m * p.ldc + c0;
+            if (p.out_f32)
+                store8<float>(static_cast<float*>(p.C), idx, v, cval);
             else
-                load8<T>(static_cast<const T*>(p.res), m * p.ldc + c0, p.res ? cval : 0, rsd);
-            finish(m, v, bias8, rsd);
+                store8<T>(static_cast<T*>(p.C), idx, v, cval);
         }
         return;
     }
