@@ -327,6 +327,15 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
 
     // --- block -> (m tile, split, sub-slice, n tile), XCD-grouped -------------------------
     // (all divisions by launch constants go through precomputed multipliers)
+    // Touch every 64-byte line of the kernel arguments at entry: their scalar-cache misses then
+    // overlap in one wait here instead of arriving phase by phase as fields are first used.
+    {
+        const auto* ka = (const __attribute__((address_space(4))) unsigned*)(__builtin_amdgcn_kernarg_segment_ptr());
+        unsigned x = 0;
+#pragma unroll
+        for (int o = 0; o < static_cast<int>(sizeof(GemmParams) / 4); o += 16) x |= ka[o];
+        asm volatile("" ::"s"(x));
+    }
     const unsigned t = (blockIdx.x % 8) * static_cast<unsigned>(p.g_per_xcd) + blockIdx.x / 8;
     if (t >= static_cast<unsigned>(p.g_total)) return;
     // within an XCD's run, tiles go in groups of GM m-tiles x every column (split, sub-slice,
