@@ -64,6 +64,17 @@ constexpr int kRsrcWord3 = 0x00020000;
 constexpr int kGroupM = 8;
 constexpr unsigned kOOB = 0x80000000u;
 
+// Touch every 64-byte line of a kernel's BYTES of arguments at entry: their scalar-cache misses
+// then overlap in one wait instead of arriving phase by phase as fields are first used.
+template <size_t BYTES>
+__device__ __forceinline__ void touch_kernargs() {
+    const auto* ka = (const __attribute__((address_space(4))) unsigned*)(__builtin_amdgcn_kernarg_segment_ptr());
+    unsigned x = 0;
+#pragma unroll
+    for (int o = 0; o < static_cast<int>(BYTES / 4); o += 16) x |= ka[o];
+    asm volatile("" ::"s"(x));
+}
+
 // f(std::integral_constant<int, i>) for i = 0 .. N-1, unrolled at compile time
 template <int N, typename F, int I = 0>
 __device__ __forceinline__ void static_for(F&& f) {
@@ -327,15 +338,7 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
 
     // --- block -> (m tile, split, sub-slice, n tile), XCD-grouped -------------------------
     // (all divisions by launch constants go through precomputed multipliers)
-    // Touch every 64-byte line of the kernel arguments at entry: their scalar-cache misses then
-    // overlap in one wait here instead of arriving phase by phase as fields are first used.
-    {
-        const auto* ka = (const __attribute__((address_space(4))) unsigned*)(__builtin_amdgcn_kernarg_segment_ptr());
-        unsigned x = 0;
-#pragma unroll
-        for (int o = 0; o < static_cast<int>(sizeof(GemmParams) / 4); o += 16) x |= ka[o];
-        asm volatile("" ::"s"(x));
-    }
+    touch_kernargs<sizeof(GemmParams)>();
     const unsigned t = (blockIdx.x % 8) * static_cast<unsigned>(p.g_per_xcd) + blockIdx.x / 8;
     if (t >= static_cast<unsigned>(p.g_total)) return;
     // within an XCD's run, tiles go in groups of GM m-tiles x every column (split, sub-slice,
@@ -765,6 +768,7 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
 // Split-K finish: sum the partials in split order, then the usual epilogue.
 template <typename T>
 __global__ void splitk_reduce_kernel(const GemmParams p) {
+    touch_kernargs<sizeof(GemmParams)>();
     const int groups = (p.N + 3) / 4;
     const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     if (t >= p.M * groups) return;
