@@ -203,6 +203,13 @@ __device__ __forceinline__ void unpack4(const Raw4<T>& r, float (&v)[4]) {
         v[0] = __uint_as_float(r.x), v[1] = __uint_as_float(r.y), v[2] = __uint_as_float(r.z), v[3] = __uint_as_float(r.w);
     }
 }
+// the 4 floats at q (16-byte aligned), or zeros from the zero page when q is null: one
+// unconditional global load either way
+__device__ __forceinline__ f32x4 load_f32x4(const float* q, const void* zero_page) {
+    const void* src = q ? static_cast<const void*>(q) : zero_page;
+    return *(const __attribute__((address_space(1))) f32x4*)(src);
+}
+
 // p[i .. i+nvalid-1] (zeros after them, and everywhere when p is null), element by element
 template <typename T>
 __device__ __forceinline__ void ld4_or_zero(const T* p, int64_t i, int nvalid, float (&v)[4]) {
@@ -525,12 +532,29 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
                                     kZeroChunk);
         }
     }
+    // An LSTM step starts wave 0's accumulators at the gate pre-activations gx (fp32, loaded
+    // here in the same way): the epilogue then only applies the cell.
+    const bool lstm_here = p.epi == EPI_LSTM && (KS == 1 || kw == 0);
+    f32x4 rgx[FM][FN];
+#pragma unroll
+    for (int a = 0; a < FM; ++a)
+#pragma unroll
+        for (int b = 0; b < FN; ++b) {
+            const bool ok = lstm_here && mrow[a] < p.M && nval[b] == 4;
+            rgx[a][b] = load_f32x4(ok ? p.gx + mrow[a] * p.ldgx + ncol[b] : nullptr, kZeroChunk);
+        }
 
     // prologue: NS-1 stages in flight (coordinates then stand at stage NS - 1)
 #pragma unroll
     for (int s = 0; s < NS - 1; ++s)
         if (s < nst) issue_stage(s, s);
 
+    if (lstm_here) {
+#pragma unroll
+        for (int a = 0; a < FM; ++a)
+#pragma unroll
+            for (int b = 0; b < FN; ++b) acc[a][b] = rgx[a][b];
+    }
     if (init_here) {
 #pragma unroll
         for (int b = 0; b < FN; ++b) {
@@ -696,9 +720,9 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
                 if (a % KS == kw) acc[a][b] = tile4(a * 16 + (lane & 15), b * 16 + (lane >> 4) * 4);
     }
     if (p.epi == EPI_LSTM) {
-        // gates i, f, g, o of unit n / 4 (n is a multiple of 4 and the whole group is valid);
-        // with K split across waves, wave w finishes row tiles a = w (mod KS)
-        f32x4 g4[FM][FN];
+        // gates i, f, g, o of unit n / 4 (n is a multiple of 4 and the whole group is valid),
+        // gx already in the sums; with K split across waves, wave w finishes row tiles
+        // a = w (mod KS)
         float cprev[FM][FN];
 #pragma unroll
         for (int a = 0; a < FM; ++a)
@@ -707,7 +731,6 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
                 const bool ok = a % KS == kw && mrow[a] < p.M && nval[b] == 4;
                 const int64_t mm = ok ? mrow[a] : 0;
                 const int nn = ok ? ncol[b] : 0;
-                g4[a][b] = *reinterpret_cast<const f32x4*>(p.gx + mm * p.ldgx + nn);
                 cprev[a][b] = p.cstate[mm * (p.N >> 2) + (nn >> 2)];
             }
 #pragma unroll
@@ -715,7 +738,7 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
 #pragma unroll
             for (int b = 0; b < FN; ++b) {
                 if (a % KS != kw || mrow[a] >= p.M || nval[b] != 4) continue;
-                const f32x4 v = acc[a][b] + g4[a][b];
+                const f32x4 v = acc[a][b];
                 const float c = sigmoidf_(v[1]) * cprev[a][b] + sigmoidf_(v[0]) * tanhf(v[2]);
                 const int u = ncol[b] >> 2;
                 p.cstate[mrow[a] * (p.N >> 2) + u] = c;
