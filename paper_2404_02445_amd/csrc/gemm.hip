@@ -886,7 +886,9 @@ static hipError_t dispatch(const GemmParams& p, hipStream_t st) {
     }
     const int64_t mt = (p.M + 127) / 128;
     auto blocks = [&](int64_t bm_tiles, int bn) { return bm_tiles * ((width + bn - 1) / bn) * p.ksub * p.splits; };
-    if (width >= 128 && blocks(mt, 128) >= kCUs) return launch_cfg<T, 128, 128, 2, 4, 2>(p, width, st);
+    // 128-wide tiles unless they would leave more than a tenth of the columns they cover empty
+    const bool w128 = width >= 128 && (width + 127) / 128 * 128 * 10 <= width * 11;
+    if (w128 && blocks(mt, 128) >= kCUs) return launch_cfg<T, 128, 128, 2, 4, 2>(p, width, st);
     if (width >= 64 && blocks(mt, 64) >= kCUs) return launch_cfg<T, 128, 64, 4, 2, 3>(p, width, st);
     if (width >= 64) return launch_cfg<T, 64, 64, 2, 4, 4>(p, width, st);
     if (width >= 32) {
