@@ -747,8 +747,29 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
         return;
     }
 
-    // Every thread then owns whole 8-column chunks of the staged tile: full-line stores, and
-    // bias / residual as vector loads.
+    // Narrow tiles (32 columns or fewer) store straight from the MFMA layout: a lane's four
+    // consecutive columns are one 8-byte (bf16) store, and the LDS round trip costs more than
+    // the shorter stores save (measured).
+    if constexpr (KS == 1 && BN <= 32) {
+        if (direct) {
+#pragma unroll
+            for (int a = 0; a < FM; ++a)
+#pragma unroll
+                for (int b = 0; b < FN; ++b) {
+                    if (mrow[a] >= p.M || nval[b] == 0) continue;
+                    float v[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] = act_f(acc[a][b][e], p.act);
+                    const int64_t idx = mrow[a] * p.ldc + ncol[b];
+                    if (p.out_f32)
+                        store4<float>(static_cast<float*>(p.C), idx, v, nval[b]);
+                    else
+                        store4<T>(static_cast<T*>(p.C), idx, v, nval[b]);
+                }
+            return;
+        }
+    }
+    // Otherwise every thread owns whole 8-column chunks of the staged tile: full-line stores.
     if constexpr (KS == 1) stage_tile();
     auto tile8 = [&](int r, float (&v)[8]) {
         const f32x4 lo = tile4(r, cc * 8), hi = tile4(r, cc * 8 + 4);
