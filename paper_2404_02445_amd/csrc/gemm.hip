@@ -508,29 +508,25 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
     const int c0 = n0 + cc * 8;
     const int cval = max(0, min(8, n_hi - c0));
     const bool direct = p.splits == 1 && p.epi == EPI_STD;   // this block finishes its outputs
-    // A direct launch starts its accumulators at (bias + second bias) + residual.  Their raw
-    // bits (MFMA layout: 4 columns of one row per lane and fragment) are loaded here, before the
-    // operand stages, and added after the prologue: the latency hides under the first stage's,
-    // and no branch makes the wave wait for them early.  Each is one unconditional load, from
-    // the zero page when absent; partial or misaligned column groups are read element by
-    // element when added.  With K split across waves only wave 0 starts from them.
+    // A direct launch starts its accumulators at bias + second bias.  Their raw bits (MFMA
+    // layout: 4 columns per lane and fragment) are loaded here, before the operand stages, and
+    // added after the prologue: the latency hides under the first stage's, and no branch makes
+    // the wave wait for them early.  Each is one unconditional load, from the zero page when
+    // absent; partial column groups are read element by element when added.  With K split
+    // across waves only wave 0 starts from them.  (The residual is added in the epilogue, in
+    // the chunk layout whose 16-byte loads cover whole lines: in the MFMA layout its 8-byte
+    // loads were measured slower.)
     const T* biasp = static_cast<const T*>(p.bias);
     const T* bias2p = static_cast<const T*>(p.bias2);
     const T* resp = static_cast<const T*>(p.res);
     const bool init_here = direct && (KS == 1 || kw == 0);
-    Raw4<T> rb[FN], rb2[FN], rres[FM][FN];
-    bool bfast[FN], rfast[FM][FN];
+    Raw4<T> rb[FN], rb2[FN];
+    bool bfast[FN];
 #pragma unroll
     for (int b = 0; b < FN; ++b) {
         bfast[b] = nval[b] == 4;
         rb[b] = load_raw4<T>(init_here && bfast[b] && biasp ? biasp + ncol[b] : nullptr, kZeroChunk);
         rb2[b] = load_raw4<T>(init_here && bfast[b] && bias2p ? bias2p + ncol[b] : nullptr, kZeroChunk);
-#pragma unroll
-        for (int a = 0; a < FM; ++a) {
-            rfast[a][b] = bfast[b] && mrow[a] < p.M && ((mrow[a] * p.ldc + ncol[b]) & 3) == 0;
-            rres[a][b] = load_raw4<T>(init_here && rfast[a][b] && resp ? resp + mrow[a] * p.ldc + ncol[b] : nullptr,
-                                    kZeroChunk);
-        }
     }
     // An LSTM step starts wave 0's accumulators at the gate pre-activations gx (fp32, loaded
     // here in the same way): the epilogue then only applies the cell.
@@ -567,15 +563,9 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
                 ld4_or_zero<T>(bias2p, ncol[b], nval[b], b2v);
             }
 #pragma unroll
-            for (int a = 0; a < FM; ++a) {
-                float rv[4];
-                if (rfast[a][b])
-                    unpack4<T>(rres[a][b], rv);
-                else
-                    ld4_or_zero<T>(mrow[a] < p.M ? resp : nullptr, mrow[a] * p.ldc + ncol[b], nval[b], rv);
+            for (int a = 0; a < FM; ++a)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) acc[a][b][e] = (bv[e] + b2v[e]) + rv[e];
-            }
+                for (int e = 0; e < 4; ++e) acc[a][b][e] = bv[e] + b2v[e];
         }
     }
 
@@ -757,10 +747,11 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
 #pragma unroll
                 for (int b = 0; b < FN; ++b) {
                     if (mrow[a] >= p.M || nval[b] == 0) continue;
-                    float v[4];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) v[e] = act_f(acc[a][b][e], p.act);
                     const int64_t idx = mrow[a] * p.ldc + ncol[b];
+                    float v[4], rv[4] = {0.f, 0.f, 0.f, 0.f};
+                    if (resp) ld4<T>(resp, idx, nval[b], rv);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] = act_f(acc[a][b][e] + rv[e], p.act);
                     if (p.out_f32)
                         store4<float>(static_cast<float*>(p.C), idx, v, nval[b]);
                     else
@@ -777,17 +768,18 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
         for (int e = 0; e < 4; ++e) v[e] = lo[e], v[4 + e] = hi[e];
     };
     if (direct) {
-        // bias and residual are already in the sums: activation and store only
+        // bias is already in the sums: residual, activation, store
 #pragma unroll
         for (int i = 0; i < NCH; ++i) {
             const int r = cr + i * RPP;
             const int64_t m = m0 + r;
             if (r >= BM || m >= p.M || cval == 0) continue;
-            float v[8];
+            float v[8], rsd[8];
             tile8(r, v);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) v[e] = act_f(v[e], p.act);
             const int64_t idx = m * p.ldc + c0;
+            load8<T>(resp, idx, resp ? cval : 0, rsd);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = act_f(v[e] + rsd[e], p.act);
             if (p.out_f32)
                 store8<float>(static_cast<float*>(p.C), idx, v, cval);
             else
