@@ -329,7 +329,7 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
     constexpr int SSTAGE = KH * STAGE;          // uint4 per stage: KH sub-stages, one barrier
     static_assert((NW == 4 || NW == 8) && FM >= 1 && FN >= 1 && NS >= 2 && NS <= 9 && LMIN >= 1, "tile");
     static_assert(KH == 1 || KH == 2 || KH == 4, "sub-stages per stage");
-    static_assert(KS == 1 || (KS == KH && WM == 1 && WN == 1), "K split across waves");
+    static_assert(KS == KH && (KS == 1 || (WM == 1 && WN == 1)), "K split across waves: one sub-stage per wave");
     static_assert((NS - 2) * LMIN * KH <= 63, "vmcnt range");
 
     constexpr int LDT = BN + 4;                 // fp32 row stride of the staged output tile (padded)
@@ -623,30 +623,6 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
             for (int b = 0; b < FN; ++b) pin(b0[b]);
             read_frags(hb, 1, a1, b1);
             mfmas(a0, b0);
-        } else if constexpr (KH > 1) {
-            // k steps 2h, 2h + 1 of sub-stage h; each step's fragment reads are issued before
-            // the previous step's MFMAs, so LDS latency hides under them
-            const int steps = 2 * min(KH, u1 - (u0 + st * KH));   // live k steps (uniform)
-            read_frags(sbase, 0, a0, b0);
-#pragma unroll
-            for (int j = 0; j < 2 * KH; j += 2) {
-                if (j >= steps) break;
-                lds_wait();
-#pragma unroll
-                for (int a = 0; a < FM; ++a) pin(a0[a]);
-#pragma unroll
-                for (int b = 0; b < FN; ++b) pin(b0[b]);
-                read_frags(sbase + (j / 2) * STAGE * 16, 1, a1, b1);
-                mfmas(a0, b0);
-                lds_wait();
-#pragma unroll
-                for (int a = 0; a < FM; ++a) pin(a1[a]);
-#pragma unroll
-                for (int b = 0; b < FN; ++b) pin(b1[b]);
-                if (j + 2 < steps) read_frags(sbase + (j / 2 + 1) * STAGE * 16, 0, a0, b0);
-                mfmas(a1, b1);
-            }
-            continue;
         } else if constexpr (FM + FN <= 3) {
             // thin wave tiles: both k steps' fragment reads go out together; LDS reads complete
             // in order, so once at most FM + FN are outstanding the first step's have landed
