@@ -510,40 +510,60 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
     const bool direct = p.splits == 1 && p.epi == EPI_STD;   // this block finishes its outputs
     // A direct launch starts its accumulators at bias + second bias.  Their raw bits (MFMA
     // layout: 4 columns per lane and fragment) are loaded here, before the operand stages, and
-    // added after the prologue: the latency hides under the first stage's, and no branch makes
-    // the wave wait for them early.  Each is one unconditional load, from the zero page when
-    // absent; partial column groups are read element by element when added.  With K split
-    // across waves only wave 0 starts from them.  (The residual is added in the epilogue, in
+    // added after the prologue: the latency hides under the first stage's.  Each is one load
+    // per lane, from the zero page when absent; partial column groups are read element by
+    // element up front.  With K split across waves only wave 0 starts from them.  (The residual is added in the epilogue, in
     // the chunk layout whose 16-byte loads cover whole lines: in the MFMA layout its 8-byte
     // loads were measured slower.)
     const T* biasp = static_cast<const T*>(p.bias);
     const T* bias2p = static_cast<const T*>(p.bias2);
     const T* resp = static_cast<const T*>(p.res);
     const bool init_here = direct && (KS == 1 || kw == 0);
+    // (Loads whose results a path never reads would leave their registers pending there, and
+    // the compiler would then drain every load in flight, operand stages included, when it
+    // reuses those registers inside the K loop: each of these loads is issued only under the
+    // wave-uniform condition under which it is added.)
     Raw4<T> rb[FN], rb2[FN];
     bool bfast[FN];
+    float bslow[FN][4];                         // partial groups: summed bias, read up front
 #pragma unroll
     for (int b = 0; b < FN; ++b) {
         bfast[b] = nval[b] == 4;
-        rb[b] = load_raw4<T>(init_here && bfast[b] && biasp ? biasp + ncol[b] : nullptr, kZeroChunk);
-        rb2[b] = load_raw4<T>(init_here && bfast[b] && bias2p ? bias2p + ncol[b] : nullptr, kZeroChunk);
+        if (init_here) {
+            rb[b] = load_raw4<T>(bfast[b] && biasp ? biasp + ncol[b] : nullptr, kZeroChunk);
+            rb2[b] = load_raw4<T>(bfast[b] && bias2p ? bias2p + ncol[b] : nullptr, kZeroChunk);
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) bslow[b][e] = 0.0f;
+        // (element loads under a per-lane branch: done before any operand load is in flight,
+        // since the wait they need would otherwise drain the operand stages too)
+        if (init_here && !bfast[b]) {
+            float bv[4], b2v[4];
+            ld4_or_zero<T>(biasp, ncol[b], nval[b], bv);
+            ld4_or_zero<T>(bias2p, ncol[b], nval[b], b2v);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) bslow[b][e] = bv[e] + b2v[e];
+        }
     }
     // An LSTM step starts wave 0's accumulators at the gate pre-activations gx (fp32, loaded
     // here in the same way): the epilogue then only applies the cell.
     const bool lstm_here = p.epi == EPI_LSTM && (KS == 1 || kw == 0);
     f32x4 rgx[FM][FN];
+    if (lstm_here) {
 #pragma unroll
-    for (int a = 0; a < FM; ++a)
+        for (int a = 0; a < FM; ++a)
 #pragma unroll
-        for (int b = 0; b < FN; ++b) {
-            const bool ok = lstm_here && mrow[a] < p.M && nval[b] == 4;
-            rgx[a][b] = load_f32x4(ok ? p.gx + mrow[a] * p.ldgx + ncol[b] : nullptr, kZeroChunk);
-        }
+            for (int b = 0; b < FN; ++b) {
+                const bool ok = mrow[a] < p.M && nval[b] == 4;
+                rgx[a][b] = load_f32x4(ok ? p.gx + mrow[a] * p.ldgx + ncol[b] : nullptr, kZeroChunk);
+            }
+    }
 
-    // prologue: NS-1 stages in flight (coordinates then stand at stage NS - 1)
+    // prologue: NS-1 stages in flight (coordinates then stand at stage NS - 1); stages past
+    // the split re-read its first sub-stage, and are issued anyway so that the loads in flight
+    // at this point do not depend on the path
 #pragma unroll
-    for (int s = 0; s < NS - 1; ++s)
-        if (s < nst) issue_stage(s, s);
+    for (int s = 0; s < NS - 1; ++s) issue_stage(s, s);
 
     if (lstm_here) {
 #pragma unroll
@@ -555,19 +575,22 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
 #pragma unroll
         for (int b = 0; b < FN; ++b) {
             float bv[4], b2v[4];
-            if (bfast[b]) {
-                unpack4<T>(rb[b], bv);
-                unpack4<T>(rb2[b], b2v);
-            } else {
-                ld4_or_zero<T>(biasp, ncol[b], nval[b], bv);
-                ld4_or_zero<T>(bias2p, ncol[b], nval[b], b2v);
-            }
+            unpack4<T>(rb[b], bv);
+            unpack4<T>(rb2[b], b2v);
 #pragma unroll
             for (int a = 0; a < FM; ++a)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) acc[a][b][e] = bv[e] + b2v[e];
+                for (int e = 0; e < 4; ++e) acc[a][b][e] = bfast[b] ? bv[e] + b2v[e] : bslow[b][e];
         }
     }
+    // The accumulators now hold values computed from loads; pinning them here makes the
+    // compiler settle those loads once, before the K loop.  (Otherwise it treats the
+    // accumulators as possibly pending loads inside the loop and waits there for every load
+    // in flight, the operand stages just issued included.)
+#pragma unroll
+    for (int a = 0; a < FM; ++a)
+#pragma unroll
+        for (int b = 0; b < FN; ++b) asm volatile("" : "+v"(acc[a][b]));
 
     // LDS byte addresses of this lane's MFMA fragments (row l % 16 of a 16-row block, chunk
     // 4 * ks + l / 16) in stage buffer 0, sub-stage 0, for the wave's first A and B rows;
