@@ -240,24 +240,6 @@ __device__ __forceinline__ void store8(T* c, int64_t idx, const float (&v)[8], i
     for (int q = 0; q < nvalid; ++q) c[idx + q] = static_cast<T>(v[q]);
 }
 
-// bias, second bias, residual, activation and the store of 4 consecutive columns
-template <typename T>
-__device__ __forceinline__ void epilogue4(const GemmParams& p, int64_t m, int n, int nvalid, float* v) {
-    float t[4], bias[4] = {0.f, 0.f, 0.f, 0.f}, rsd[4] = {0.f, 0.f, 0.f, 0.f};
-    if (p.bias) ld4(static_cast<const T*>(p.bias), n, nvalid, bias);
-    if (p.bias2) {
-        ld4(static_cast<const T*>(p.bias2), n, nvalid, t);
-        for (int q = 0; q < 4; ++q) bias[q] += t[q];
-    }
-    if (p.res) ld4(static_cast<const T*>(p.res), m * p.ldc + n, nvalid, rsd);
-    for (int q = 0; q < 4; ++q) v[q] = act_f((v[q] + bias[q]) + rsd[q], p.act);
-    const int64_t idx = m * p.ldc + n;
-    if (p.out_f32)
-        store4<float>(static_cast<float*>(p.C), idx, v, nvalid);
-    else
-        store4<T>(static_cast<T*>(p.C), idx, v, nvalid);
-}
-
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 // LDS fragment reads.  They are issued as inline asm so the compiler does not
@@ -367,7 +349,9 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
     const int n_lo = j * q + min(j, rr), n_hi = (j + 1) * q + min(j + 1, rr);
     const int n0 = n_lo + nti * BN;
     if (n0 >= n_hi) return;                     // block-uniform, before any barrier
-    const int64_t m0 = static_cast<int64_t>(mti) * BM;
+    // rows fit in 32 bits (M <= 2^31 - 256, checked at launch); output offsets are 64-bit
+    const int Mi = static_cast<int>(p.M);
+    const int m0 = mti * BM;
 
     // this split's sub-stages [u0, u1): boundaries in BK units, whatever KH is
     const int nk = p.g_nk;
@@ -396,8 +380,8 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
 #pragma unroll
     for (int i = 0; i < LA; ++i) {
         const int blk = min(wave + NW * i, NBA - 1);
-        const int64_t m = m0 + blk * 8 + (lane >> 3);
-        const int64_t mc = m < p.M ? m : p.M - 1;
+        const int m = m0 + blk * 8 + (lane >> 3);
+        const int mc = m < Mi ? m : Mi - 1;
         hb[i] = wb[i] = 0;
         if constexpr (CONV) {
             // M < 2^31, so the pixel decode runs in 32 bits with precomputed divisors
@@ -410,7 +394,8 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
             const int pix = (static_cast<int>(img) * p.img_h + hb[i]) * p.img_w + wb[i];
             voffA[i] = static_cast<unsigned>(pix) * static_cast<unsigned>(p.cs * sizeof(T));
         } else {
-            voffA[i] = static_cast<unsigned>((mc * p.lda + cl * EPC) * static_cast<int64_t>(sizeof(T)));
+            // (A spans less than 2^31 bytes, so the offset of row mc fits in 32 bits)
+            voffA[i] = static_cast<unsigned>(mc) * static_cast<unsigned>(p.lda * sizeof(T)) + static_cast<unsigned>(cl * 16);
         }
     }
 #pragma unroll
@@ -418,7 +403,7 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
         const int blk = min(wave + NW * i, NBB - 1);
         const int n = n0 + blk * 8 + (lane >> 3);
         const int nc = n < n_hi ? n : n_hi - 1;
-        voffB[i] = static_cast<unsigned>((static_cast<int64_t>(nc) * p.K + cl * EPC) * static_cast<int64_t>(sizeof(T)));
+        voffB[i] = static_cast<unsigned>(nc) * static_cast<unsigned>(p.K * sizeof(T)) + static_cast<unsigned>(cl * 16);
     }
 
     // im2col coordinates (tap row, tap column, channel) of this lane's chunk, advanced
@@ -492,7 +477,7 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
 
     // --- epilogue set-up ---------------------------------------------------------------------
     // MFMA layout: lane holds row mrow[a], columns ncol[b]..+3
-    int64_t mrow[FM];
+    int mrow[FM];
     int ncol[FN], nval[FN];
 #pragma unroll
     for (int a = 0; a < FM; ++a) mrow[a] = m0 + wm * TM + a * 16 + (lane & 15);
@@ -554,8 +539,8 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
         for (int a = 0; a < FM; ++a)
 #pragma unroll
             for (int b = 0; b < FN; ++b) {
-                const bool ok = mrow[a] < p.M && nval[b] == 4;
-                rgx[a][b] = load_f32x4(ok ? p.gx + mrow[a] * p.ldgx + ncol[b] : nullptr, kZeroChunk);
+                const bool ok = mrow[a] < Mi && nval[b] == 4;
+                rgx[a][b] = load_f32x4(ok ? p.gx + static_cast<int64_t>(mrow[a]) * p.ldgx + ncol[b] : nullptr, kZeroChunk);
             }
     }
 
@@ -717,7 +702,7 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
         for (int a = 0; a < FM; ++a)
 #pragma unroll
             for (int b = 0; b < FN; ++b) {
-                const bool ok = a % KS == kw && mrow[a] < p.M && nval[b] == 4;
+                const bool ok = a % KS == kw && mrow[a] < Mi && nval[b] == 4;
                 const int64_t mm = ok ? mrow[a] : 0;
                 const int nn = ok ? ncol[b] : 0;
                 cprev[a][b] = p.cstate[mm * (p.N >> 2) + (nn >> 2)];
@@ -726,12 +711,12 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
         for (int a = 0; a < FM; ++a)
 #pragma unroll
             for (int b = 0; b < FN; ++b) {
-                if (a % KS != kw || mrow[a] >= p.M || nval[b] != 4) continue;
+                if (a % KS != kw || mrow[a] >= Mi || nval[b] != 4) continue;
                 const f32x4 v = acc[a][b];
                 const float c = sigmoidf_(v[1]) * cprev[a][b] + sigmoidf_(v[0]) * tanhf(v[2]);
                 const int u = ncol[b] >> 2;
-                p.cstate[mrow[a] * (p.N >> 2) + u] = c;
-                static_cast<T*>(p.C)[mrow[a] * p.ldc + u] = static_cast<T>(sigmoidf_(v[3]) * tanhf(c));
+                p.cstate[static_cast<int64_t>(mrow[a]) * (p.N >> 2) + u] = c;
+                static_cast<T*>(p.C)[static_cast<int64_t>(mrow[a]) * p.ldc + u] = static_cast<T>(sigmoidf_(v[3]) * tanhf(c));
             }
         return;
     }
@@ -745,8 +730,8 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
             for (int a = 0; a < FM; ++a)
 #pragma unroll
                 for (int b = 0; b < FN; ++b) {
-                    if (mrow[a] >= p.M || nval[b] == 0) continue;
-                    const int64_t idx = mrow[a] * p.ldc + ncol[b];
+                    if (mrow[a] >= Mi || nval[b] == 0) continue;
+                    const int64_t idx = static_cast<int64_t>(mrow[a]) * p.ldc + ncol[b];
                     float v[4], rv[4] = {0.f, 0.f, 0.f, 0.f};
                     if (resp) ld4<T>(resp, idx, nval[b], rv);
 #pragma unroll
@@ -771,11 +756,11 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
 #pragma unroll
         for (int i = 0; i < NCH; ++i) {
             const int r = cr + i * RPP;
-            const int64_t m = m0 + r;
-            if (r >= BM || m >= p.M || cval == 0) continue;
+            const int m = m0 + r;
+            if (r >= BM || m >= Mi || cval == 0) continue;
             float v[8], rsd[8];
             tile8(r, v);
-            const int64_t idx = m * p.ldc + c0;
+            const int64_t idx = static_cast<int64_t>(m) * p.ldc + c0;
             load8<T>(resp, idx, resp ? cval : 0, rsd);
 #pragma unroll
             for (int e = 0; e < 8; ++e) v[e] = act_f(v[e] + rsd[e], p.act);
@@ -792,11 +777,11 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
         const int r = cr + i * RPP;
-        const int64_t m = m0 + r;
-        if (r >= BM || m >= p.M || cval == 0) continue;
+        const int m = m0 + r;
+        if (r >= BM || m >= Mi || cval == 0) continue;
         float v[8];
         tile8(r, v);
-        store8<float>(part, m * p.N + c0, v, cval);
+        store8<float>(part, static_cast<int64_t>(m) * p.N + c0, v, cval);
     }
 }
 
@@ -804,12 +789,19 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
 template <typename T>
 __global__ void splitk_reduce_kernel(const GemmParams p) {
     touch_kernargs<sizeof(GemmParams)>();
-    const int groups = (p.N + 3) / 4;
-    const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (t >= p.M * groups) return;
-    const int64_t m = t / groups;
-    const int n = static_cast<int>(t - m * groups) * 4;
+    // one thread per 4 columns of a row; M * ceil(N / 4) < 2^31 (checked at launch)
+    const unsigned groups = static_cast<unsigned>(p.N + 3) / 4;
+    const unsigned t = blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= static_cast<unsigned>(p.M) * groups) return;
+    const unsigned mu = p.r_div_groups.div(t);
+    const int64_t m = mu;
+    const int n = static_cast<int>(t - mu * groups) * 4;
     const int nvalid = min(4, p.N - n);
+    // bias, second bias and residual go out first, so their latency overlaps the partials'
+    float bias[4] = {0.f, 0.f, 0.f, 0.f}, bias2[4] = {0.f, 0.f, 0.f, 0.f}, rsd[4] = {0.f, 0.f, 0.f, 0.f};
+    if (p.bias) ld4(static_cast<const T*>(p.bias), n, nvalid, bias);
+    if (p.bias2) ld4(static_cast<const T*>(p.bias2), n, nvalid, bias2);
+    if (p.res) ld4(static_cast<const T*>(p.res), m * p.ldc + n, nvalid, rsd);
     float v[4] = {0.f, 0.f, 0.f, 0.f};
     const int64_t plane = p.M * static_cast<int64_t>(p.N);
     const float* src = p.partial + m * p.N + n;
@@ -826,7 +818,12 @@ __global__ void splitk_reduce_kernel(const GemmParams p) {
         for (int s = 0; s < p.splits; ++s)
             for (int e = 0; e < nvalid; ++e) v[e] += src[s * plane + e];
     }
-    epilogue4<T>(p, m, n, nvalid, v);
+    for (int q = 0; q < 4; ++q) v[q] = act_f((v[q] + (bias[q] + bias2[q])) + rsd[q], p.act);
+    const int64_t idx = m * p.ldc + n;
+    if (p.out_f32)
+        store4<float>(static_cast<float*>(p.C), idx, v, nvalid);
+    else
+        store4<T>(static_cast<T*>(p.C), idx, v, nvalid);
 }
 
 // ---------------------------------------------------------------------------
@@ -837,7 +834,7 @@ __global__ void splitk_reduce_kernel(const GemmParams p) {
 constexpr int kCUs = 256;
 
 int gemm_splits(int64_t M, int N, int K, int dtype, int epi) {
-    if (epi != EPI_STD) return 1;
+    if (epi != EPI_STD || M * ((N + 3) / 4) >= (int64_t(1) << 31)) return 1;
     const int bk = dtype == MOPAR_BF16 ? 64 : 32;
     const int64_t nk = (K + bk - 1) / bk;
     const int64_t tiles = ((M + 63) / 64) * ((N + 63) / 64);   // reference tiling, independent of k
@@ -920,6 +917,7 @@ hipError_t launch_gemm(const GemmParams& params, int dtype, hipStream_t stream) 
         p.div_w = FastDiv(static_cast<unsigned>(p.out_w));
     }
     if (p.M <= 0 || p.N <= 0) return hipSuccess;
+    if (p.M > (int64_t(1) << 31) - 256) return hipErrorInvalidValue;   // rows are 32-bit in the kernel
     // operands are read through buffer resources with 32-bit byte offsets, and offset 2^31
     // must lie past both of them
     const int64_t esz = dtype == MOPAR_BF16 ? 2 : 4;
@@ -933,6 +931,8 @@ hipError_t launch_gemm(const GemmParams& params, int dtype, hipStream_t stream) 
     hipError_t e = dtype == MOPAR_BF16 ? dispatch<__bf16>(p, stream) : dispatch<float>(p, stream);
     if (e != hipSuccess || p.splits == 1) return e;
     const int64_t n = p.M * ((p.N + 3) / 4);
+    if (n >= (int64_t(1) << 31)) return hipErrorInvalidValue;
+    p.r_div_groups = FastDiv(static_cast<unsigned>((p.N + 3) / 4));
     const unsigned blocks = static_cast<unsigned>((n + 255) / 256);
     if (dtype == MOPAR_BF16)
         launch_kernel(splitk_reduce_kernel<__bf16>, dim3(blocks), dim3(256), 0, stream, p);

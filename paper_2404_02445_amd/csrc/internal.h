@@ -114,6 +114,7 @@ struct GemmParams {
     // remainder rr, and divisors for the block-index decode
     int g_mt, g_nt, g_total, g_per_xcd, g_cols, g_nk, g_q, g_rr;
     FastDiv g_div_group, g_div_last, g_div_nt, g_div_ksub, g_div_splits;
+    FastDiv r_div_groups;   // split-K reduce: divide by ceil(N / 4) (set by launch_gemm)
 };
 
 // Split-K factor used for an (M, N, K) product.  A function of the shape
