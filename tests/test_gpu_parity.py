@@ -219,7 +219,7 @@ def test_embed_gather_bitwise():
     np.testing.assert_array_equal(_np(y1), oracle.forward(m, ids))
 
 
-@pytest.mark.parametrize("b,t,e,h", [(3, 7, 64, 64), (64, 4, 128, 256), (2, 3, 24, 40)])
+@pytest.mark.parametrize("b,t,e,h", [(3, 7, 64, 64), (64, 4, 128, 256), (2, 3, 24, 40), (37, 5, 32, 72)])
 def test_lstm(b, t, e, h):
     bld, x = seq_input_model("bf16", b, t, e)
     y = bld.lstm(x, h, "lstm", -0.3, 0.3)
