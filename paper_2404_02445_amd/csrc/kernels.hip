@@ -222,18 +222,28 @@ __device__ __forceinline__ int ln_col(int lane, int i) {
     return VEC ? (lane + 64 * (i / V)) * V + i % V : lane + 64 * i;
 }
 
-template <typename T, bool VEC>
-__device__ __forceinline__ void ln_row(float (&v)[LN_MAXV], int f, int lane, const T* g, const T* b, float eps,
+template <typename T, bool VEC, int MV>
+__device__ __forceinline__ void ln_row(float (&v)[MV], int f, int lane, const T* g, const T* b, float eps,
                                        T* out) {
     constexpr int V = Vec<T>::N;
+    // gamma and beta go out before the reductions, so their latency overlaps the row's
+    uint4 gr[VEC ? MV / V : 1], br[VEC ? MV / V : 1];
+    if constexpr (VEC) {
+#pragma unroll
+        for (int j = 0; j < MV / V; ++j) {
+            const int c0 = min((lane + 64 * j) * V, f - V);   // in range; unused past f
+            gr[j] = *reinterpret_cast<const uint4*>(g + c0);
+            br[j] = *reinterpret_cast<const uint4*>(b + c0);
+        }
+    }
     float s = 0.0f;
 #pragma unroll
-    for (int i = 0; i < LN_MAXV; ++i)
+    for (int i = 0; i < MV; ++i)
         if (ln_col<T, VEC>(lane, i) < f) s += v[i];
     const float mean = wave_sum(s) / static_cast<float>(f);
     float q = 0.0f;
 #pragma unroll
-    for (int i = 0; i < LN_MAXV; ++i)
+    for (int i = 0; i < MV; ++i)
         if (ln_col<T, VEC>(lane, i) < f) {
             const float d = v[i] - mean;
             q += d * d;
@@ -242,12 +252,11 @@ __device__ __forceinline__ void ln_row(float (&v)[LN_MAXV], int f, int lane, con
     const float inv = 1.0f / sqrtf(var + eps);
     if constexpr (VEC) {
 #pragma unroll
-        for (int j = 0; j < LN_MAXV / V; ++j) {
+        for (int j = 0; j < MV / V; ++j) {
             const int c0 = (lane + 64 * j) * V;
             if (c0 >= f) continue;
-            const uint4 gr = *reinterpret_cast<const uint4*>(g + c0), br = *reinterpret_cast<const uint4*>(b + c0);
-            const T* ge = reinterpret_cast<const T*>(&gr);
-            const T* be = reinterpret_cast<const T*>(&br);
+            const T* ge = reinterpret_cast<const T*>(&gr[j]);
+            const T* be = reinterpret_cast<const T*>(&br[j]);
             uint4 o;
             T* oe = reinterpret_cast<T*>(&o);
 #pragma unroll
@@ -256,7 +265,7 @@ __device__ __forceinline__ void ln_row(float (&v)[LN_MAXV], int f, int lane, con
         }
     } else {
 #pragma unroll
-        for (int i = 0; i < LN_MAXV; ++i) {
+        for (int i = 0; i < MV; ++i) {
             const int col = lane + i * 64;
             if (col < f) out[col] = from_f<T>((v[i] - mean) * inv * to_f(g[col]) + to_f(b[col]));
         }
@@ -264,54 +273,74 @@ __device__ __forceinline__ void ln_row(float (&v)[LN_MAXV], int f, int lane, con
 }
 
 // v[i] = a[col] (+ c[col]) for this lane's columns (zeros past f)
-template <typename T, bool VEC>
-__device__ __forceinline__ void ln_load(const T* a, const T* c, int f, int lane, float (&v)[LN_MAXV]) {
+template <typename T, bool VEC, int MV>
+__device__ __forceinline__ void ln_load(const T* a, const T* c, int f, int lane, float (&v)[MV]) {
     constexpr int V = Vec<T>::N;
     if constexpr (VEC) {
+        // Every lane loads (a lane past f re-reads the last chunk and keeps zeros): per-lane
+        // branches around the loads would make each chunk wait for the previous one.
+        uint4 ar[MV / V], cr[MV / V];
 #pragma unroll
-        for (int j = 0; j < LN_MAXV / V; ++j) {
-            const int c0 = (lane + 64 * j) * V;
-            uint4 ar = make_uint4(0, 0, 0, 0), cr = make_uint4(0, 0, 0, 0);
-            if (c0 < f) {
-                ar = *reinterpret_cast<const uint4*>(a + c0);
-                if (c) cr = *reinterpret_cast<const uint4*>(c + c0);
-            }
-            const T* ae = reinterpret_cast<const T*>(&ar);
-            const T* ce = reinterpret_cast<const T*>(&cr);
+        for (int j = 0; j < MV / V; ++j) {
+            const int cc = min((lane + 64 * j) * V, f - V);
+            ar[j] = *reinterpret_cast<const uint4*>(a + cc);
+            cr[j] = c ? *reinterpret_cast<const uint4*>(c + cc) : make_uint4(0, 0, 0, 0);
+        }
 #pragma unroll
-            for (int e = 0; e < V; ++e) v[j * V + e] = to_f(ae[e]) + (c ? to_f(ce[e]) : 0.0f);
+        for (int j = 0; j < MV / V; ++j) {
+            const bool ok = (lane + 64 * j) * V < f;
+            const T* ae = reinterpret_cast<const T*>(&ar[j]);
+            const T* ce = reinterpret_cast<const T*>(&cr[j]);
+#pragma unroll
+            for (int e = 0; e < V; ++e) v[j * V + e] = ok ? to_f(ae[e]) + (c ? to_f(ce[e]) : 0.0f) : 0.0f;
         }
     } else {
 #pragma unroll
-        for (int i = 0; i < LN_MAXV; ++i) {
+        for (int i = 0; i < MV; ++i) {
             const int col = lane + i * 64;
             v[i] = col < f ? to_f(a[col]) + (c ? to_f(c[col]) : 0.0f) : 0.0f;
         }
     }
 }
 
-template <typename T, bool VEC>
+template <typename T, bool VEC, int MV>
 __global__ void layernorm_kernel(const T* __restrict__ x, const T* __restrict__ res, const T* __restrict__ g,
                                  const T* __restrict__ b, T* __restrict__ y, int64_t rows, int f, float eps) {
     const int lane = threadIdx.x & 63;
     const int64_t row = static_cast<int64_t>(blockIdx.x) * (blockDim.x / 64) + (threadIdx.x >> 6);
     if (row >= rows) return;
-    float v[LN_MAXV];
-    ln_load<T, VEC>(x + row * f, res ? res + row * f : nullptr, f, lane, v);
-    ln_row<T, VEC>(v, f, lane, g, b, eps, y + row * f);
+    float v[MV];
+    ln_load<T, VEC, MV>(x + row * f, res ? res + row * f : nullptr, f, lane, v);
+    ln_row<T, VEC, MV>(v, f, lane, g, b, eps, y + row * f);
 }
+
+// go(kernel) with the row kernel instance for f columns: 16-byte chunks when f allows, with as
+// many per lane as the row needs (fewer registers, more resident waves), else one element
+// per lane and step
+template <typename T, template <typename, bool, int> class K, typename Go>
+static void ln_instance(int f, Go&& go) {
+    constexpr int V = Vec<T>::N;
+    if (f % V != 0) return go(K<T, false, LN_MAXV>::fn);
+    switch ((f + 64 * V - 1) / (64 * V)) {
+        case 1: return go(K<T, true, V>::fn);
+        case 2: return go(K<T, true, 2 * V>::fn);
+        case 3: return go(K<T, true, 3 * V>::fn);
+        case 4: return go(K<T, true, 4 * V>::fn);
+        default: return go(K<T, true, LN_MAXV>::fn);
+    }
+}
+template <typename T, bool VEC, int MV>
+struct LnK { static constexpr auto fn = layernorm_kernel<T, VEC, MV>; };
 
 template <typename T>
 static void layernorm_launch(const void* x, const void* res, const void* g, const void* b, void* y, int64_t rows,
                              int f, float eps, hipStream_t s) {
     const T *xp = static_cast<const T*>(x), *rp = static_cast<const T*>(res);
     const T *gp = static_cast<const T*>(g), *bp = static_cast<const T*>(b);
-    if (f % Vec<T>::N == 0)
-        launch_kernel(layernorm_kernel<T, true>, dim3(blocks_for(rows, 4)), dim3(256), 0, s, xp, rp, gp, bp,
-                      static_cast<T*>(y), rows, f, eps);
-    else
-        launch_kernel(layernorm_kernel<T, false>, dim3(blocks_for(rows, 4)), dim3(256), 0, s, xp, rp, gp, bp,
-                      static_cast<T*>(y), rows, f, eps);
+    ln_instance<T, LnK>(f, [&](auto kern) {
+        launch_kernel(kern, dim3(blocks_for(rows, 4)), dim3(256), 0, s, xp, rp, gp, bp, static_cast<T*>(y), rows, f,
+                      eps);
+    });
 }
 
 hipError_t launch_layernorm(const void* x, const void* res, const void* g, const void* b, void* y, int64_t rows,
@@ -327,7 +356,7 @@ hipError_t launch_layernorm(const void* x, const void* res, const void* g, const
 // BERT embedding: v = tok[id] + pos[s] + type[0], then layer norm (one wave
 // per token).
 // ---------------------------------------------------------------------------
-template <typename T, bool VEC>
+template <typename T, bool VEC, int MV>
 __global__ void embed_bert_kernel(const int32_t* __restrict__ ids, const T* __restrict__ tok,
                                   const T* __restrict__ pos, const T* __restrict__ type, const T* __restrict__ g,
                                   const T* __restrict__ b, T* __restrict__ y, int64_t rows, int seq, int f,
@@ -338,26 +367,27 @@ __global__ void embed_bert_kernel(const int32_t* __restrict__ ids, const T* __re
     const int sidx = static_cast<int>(row % seq);
     const T* tr = tok + static_cast<int64_t>(ids[row]) * f;
     const T* pr = pos + static_cast<int64_t>(sidx) * f;
-    float v[LN_MAXV];
-    ln_load<T, VEC>(tr, pr, f, lane, v);
-    float t[LN_MAXV];
-    ln_load<T, VEC>(type, nullptr, f, lane, t);
+    float v[MV];
+    ln_load<T, VEC, MV>(tr, pr, f, lane, v);
+    float t[MV];
+    ln_load<T, VEC, MV>(type, nullptr, f, lane, t);
 #pragma unroll
-    for (int i = 0; i < LN_MAXV; ++i) v[i] += t[i];
-    ln_row<T, VEC>(v, f, lane, g, b, eps, y + row * f);
+    for (int i = 0; i < MV; ++i) v[i] += t[i];
+    ln_row<T, VEC, MV>(v, f, lane, g, b, eps, y + row * f);
 }
+
+template <typename T, bool VEC, int MV>
+struct EmbK { static constexpr auto fn = embed_bert_kernel<T, VEC, MV>; };
 
 template <typename T>
 static void embed_bert_launch(const int32_t* ids, const void* tok, const void* pos, const void* type, const void* g,
                               const void* b, void* y, int64_t rows, int seq, int f, float eps, hipStream_t s) {
     const T *tp = static_cast<const T*>(tok), *pp = static_cast<const T*>(pos), *yp = static_cast<const T*>(type);
     const T *gp = static_cast<const T*>(g), *bp = static_cast<const T*>(b);
-    if (f % Vec<T>::N == 0)
-        launch_kernel(embed_bert_kernel<T, true>, dim3(blocks_for(rows, 4)), dim3(256), 0, s, ids, tp, pp, yp, gp,
-                      bp, static_cast<T*>(y), rows, seq, f, eps);
-    else
-        launch_kernel(embed_bert_kernel<T, false>, dim3(blocks_for(rows, 4)), dim3(256), 0, s, ids, tp, pp, yp, gp,
-                      bp, static_cast<T*>(y), rows, seq, f, eps);
+    ln_instance<T, EmbK>(f, [&](auto kern) {
+        launch_kernel(kern, dim3(blocks_for(rows, 4)), dim3(256), 0, s, ids, tp, pp, yp, gp, bp, static_cast<T*>(y),
+                      rows, seq, f, eps);
+    });
 }
 
 hipError_t launch_embed_bert(const int32_t* ids, const void* tok, const void* pos, const void* type, const void* g,
