@@ -18,8 +18,9 @@
 // the unsplit output bit for bit.
 //
 // Data path.  Operands stream from HBM straight into LDS with buffer_load_dwordx4
-// ... lds (16 bytes per lane, no VGPR staging), NS stages deep; a stage holds KH
-// sub-stages and costs one barrier.  A sub-stage holds 64 bf16 (32 float) of k for
+// ... lds (16 bytes per lane, no VGPR staging), NS stages deep; a stage holds one
+// sub-stage (one per wave on the K-split tiles) and costs one barrier.  A
+// sub-stage holds 64 bf16 (32 float) of k for
 // every row: 128 bytes, one cache line.  Each load instruction fetches 8 whole rows
 // (the DMA writes lane l's 16 bytes to slot l of a 1 KB LDS block); lanes take the
 // chunks of a row in XOR-swizzled order (chunk (l % 8) ^ row), so the ds_read_b128
@@ -30,10 +31,12 @@
 // a memory access -- every lane issues the same loads, so the wait counts are
 // exact.  The waves run v_mfma_f32_16x16x32_bf16 (bf16) or v_mfma_f32_16x16x4_f32
 // (fp32) on their wave tile, with the weight fragment as the first operand: each
-// lane ends up holding four consecutive output columns of one row.  The epilogue
+// lane ends up holding four consecutive output columns of one row.  The
+// accumulators start at the bias (loaded before the operand stages); the epilogue
 // stages the fp32 tile through LDS so that each thread finishes whole 8-column
-// chunks (bias, residual, activation, one 16-byte store); the LSTM cell works on
-// the MFMA layout directly.
+// chunks (residual, activation, one 16-byte store), except that tiles of 32
+// columns or fewer store straight from the MFMA layout; the LSTM cell works on the
+// MFMA layout directly.
 //
 // Blocks are numbered so that the eight XCDs (which take blocks round-robin)
 // each receive a contiguous run of tiles, grouped eight m-tiles at a time so
@@ -357,7 +360,7 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
     const int nk = p.g_nk;
     const int u0 = static_cast<int>(p.g_div_splits.div(static_cast<unsigned>(nk * split)));
     const int u1 = static_cast<int>(p.g_div_splits.div(static_cast<unsigned>(nk * (split + 1))));
-    const int nst = (u1 - u0 + KH - 1) / KH;    // stages; sub-stages past u1 load zeros, run no MFMA
+    const int nst = (u1 - u0 + KH - 1) / KH;    // stages; sub-stages past u1 re-read u0, run no MFMA
 
     // --- operand loads ----------------------------------------------------------------------
     // Each operand is read through a raw buffer resource: a lane's chunk address is a fixed
