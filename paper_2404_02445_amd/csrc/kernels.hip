@@ -45,10 +45,15 @@ __global__ void nchw_to_nhwc_kernel(const float* __restrict__ x, T* __restrict__
     const float* src = x + static_cast<int64_t>(img) * c * hw + r;
     T* dst = y + static_cast<int64_t>(pix) * cs;
     for (int c0 = 0; c0 < cs; c0 += V) {           // cs is a multiple of V
+        // every channel slot loads (padding slots re-read channel c - 1), so the loads go out
+        // together instead of one branch and one wait per channel
+        float f[V];
+#pragma unroll
+        for (int i = 0; i < V; ++i) f[i] = src[static_cast<int64_t>(min(c0 + i, c - 1)) * hw];
         uint4 out;
         T* o = reinterpret_cast<T*>(&out);
 #pragma unroll
-        for (int i = 0; i < V; ++i) o[i] = from_f<T>(c0 + i < c ? src[static_cast<int64_t>(c0 + i) * hw] : 0.0f);
+        for (int i = 0; i < V; ++i) o[i] = from_f<T>(c0 + i < c ? f[i] : 0.0f);
         *reinterpret_cast<uint4*>(dst + c0) = out;
     }
 }
@@ -68,8 +73,9 @@ hipError_t launch_nchw_to_nhwc(const float* x, void* y, int n, int c, int h, int
 
 // ---------------------------------------------------------------------------
 // Max pool, NHWC: one thread per (output pixel, 16-byte channel group).
-// Window positions outside the image are skipped (they count as -inf).  KW > 0
-// fixes the window size at compile time so all its loads issue together.
+// Window positions outside the image count as -inf.  KW > 0 fixes the window
+// size at compile time; every position then loads (an outside one re-reads a
+// clamped pixel and is ignored), so all the window's loads issue together.
 // Sizes below 2^31 elements (host-checked): 32-bit index math.
 // ---------------------------------------------------------------------------
 template <typename T, int KW>
@@ -86,16 +92,40 @@ __global__ void maxpool_kernel(const T* __restrict__ x, T* __restrict__ y, int n
     float m[V];
 #pragma unroll
     for (int i = 0; i < V; ++i) m[i] = -INFINITY;
-    for (int r = 0; r < k; ++r) {          // fully unrolled when KW > 0
-        const int iy = oy * stride - pad + r;
-        for (int q = 0; q < k; ++q) {
-            const int ix = ox * stride - pad + q;
-            if (static_cast<unsigned>(iy) >= static_cast<unsigned>(h) || static_cast<unsigned>(ix) >= static_cast<unsigned>(w))
-                continue;
-            const uint4 raw = *reinterpret_cast<const uint4*>(x + ((img * h + iy) * w + ix) * c + g * V);
-            const T* e = reinterpret_cast<const T*>(&raw);
+    if constexpr (KW > 0) {
+        uint4 raw[KW * KW];
 #pragma unroll
-            for (int i = 0; i < V; ++i) m[i] = fmaxf(m[i], to_f(e[i]));
+        for (int r = 0; r < KW; ++r)
+#pragma unroll
+            for (int q = 0; q < KW; ++q) {
+                const int iy = min(max(oy * stride - pad + r, 0), h - 1);
+                const int ix = min(max(ox * stride - pad + q, 0), w - 1);
+                raw[r * KW + q] = *reinterpret_cast<const uint4*>(x + ((img * h + iy) * w + ix) * c + g * V);
+            }
+#pragma unroll
+        for (int r = 0; r < KW; ++r)
+#pragma unroll
+            for (int q = 0; q < KW; ++q) {
+                const int iy = oy * stride - pad + r, ix = ox * stride - pad + q;
+                const bool in = static_cast<unsigned>(iy) < static_cast<unsigned>(h) &&
+                                static_cast<unsigned>(ix) < static_cast<unsigned>(w);
+                const T* e = reinterpret_cast<const T*>(&raw[r * KW + q]);
+#pragma unroll
+                for (int i = 0; i < V; ++i) m[i] = fmaxf(m[i], in ? to_f(e[i]) : -INFINITY);
+            }
+    } else {
+        for (int r = 0; r < k; ++r) {
+            const int iy = oy * stride - pad + r;
+            for (int q = 0; q < k; ++q) {
+                const int ix = ox * stride - pad + q;
+                if (static_cast<unsigned>(iy) >= static_cast<unsigned>(h) ||
+                    static_cast<unsigned>(ix) >= static_cast<unsigned>(w))
+                    continue;
+                const uint4 raw = *reinterpret_cast<const uint4*>(x + ((img * h + iy) * w + ix) * c + g * V);
+                const T* e = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+                for (int i = 0; i < V; ++i) m[i] = fmaxf(m[i], to_f(e[i]));
+            }
         }
     }
     uint4 out;
