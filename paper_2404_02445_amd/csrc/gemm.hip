@@ -224,7 +224,16 @@ __device__ __forceinline__ void ld4_or_zero(const T* p, int64_t i, int nvalid, f
 // unconditional load either way
 template <typename T>
 __device__ __forceinline__ Raw8<T> load_raw8(const T* q, const void* zero_page) {
-    return *reinterpret_cast<const Raw8<T>*>(q ? static_cast<const void*>(q) : zero_page);
+    // through a global-address-space pointer, so it is a global (not flat) load
+    typedef unsigned w4_t __attribute__((ext_vector_type(4)));
+    const auto* src = (const __attribute__((address_space(1))) w4_t*)(q ? static_cast<const void*>(q) : zero_page);
+    Raw8<T> r;
+#pragma unroll
+    for (int h = 0; h < static_cast<int>(sizeof(T)) / 2; ++h) {
+        const w4_t v = src[h];
+        r.w[h] = make_uint4(v[0], v[1], v[2], v[3]);
+    }
+    return r;
 }
 
 template <typename T>
@@ -755,7 +764,22 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
         for (int e = 0; e < 4; ++e) v[e] = lo[e], v[4 + e] = hi[e];
     };
     if (direct) {
-        // bias is already in the sums: residual, activation, store
+        // bias is already in the sums: residual, activation, store.  The residual chunks of
+        // all this thread's rows go out together before any is used (a load under each row's
+        // own conditions would wait for the one before it); partial or unaligned chunks are
+        // read element by element when used.
+        Raw8<T> rraw[NCH];
+        bool rfast[NCH];
+        if (resp) {
+#pragma unroll
+            for (int i = 0; i < NCH; ++i) {
+                const int r = cr + i * RPP;
+                const int m = m0 + r;
+                const int64_t idx = static_cast<int64_t>(m) * p.ldc + c0;
+                rfast[i] = r < BM && m < Mi && cval == 8 && aligned16(resp + idx);
+                rraw[i] = load_raw8<T>(rfast[i] ? resp + idx : nullptr, kZeroChunk);
+            }
+        }
 #pragma unroll
         for (int i = 0; i < NCH; ++i) {
             const int r = cr + i * RPP;
@@ -764,7 +788,10 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
             float v[8], rsd[8];
             tile8(r, v);
             const int64_t idx = static_cast<int64_t>(m) * p.ldc + c0;
-            load8<T>(resp, idx, resp ? cval : 0, rsd);
+            if (resp && rfast[i])
+                unpack8<T>(rraw[i], rsd);
+            else
+                load8<T>(resp, idx, resp ? cval : 0, rsd);
 #pragma unroll
             for (int e = 0; e < 8; ++e) v[e] = act_f(v[e] + rsd[e], p.act);
             if (p.out_f32)
