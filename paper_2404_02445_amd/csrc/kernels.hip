@@ -240,8 +240,9 @@ hipError_t launch_avgpool(const void* x, void* y, int n, int hw, int c, int dtyp
 // Layer norm over rows of F <= 64 * LN_MAXV elements: one wave per row, the
 // row held in registers, mean then centred variance by wave butterflies.
 // When F is a whole number of 16-byte chunks each lane holds whole chunks
-// (chunk lane + 64 j), read and written as vectors; otherwise element
-// lane + 64 i.
+// (chunk lane + 64 j), read and written as vectors, and the kernel instance
+// keeps MV floats per lane -- just the row's chunks, so fewer registers and
+// more resident waves; otherwise element lane + 64 i, MV = LN_MAXV.
 // ---------------------------------------------------------------------------
 constexpr int LN_MAXV = 32;
 
