@@ -857,6 +857,191 @@ __global__ void splitk_reduce_kernel(const GemmParams p) {
 }
 
 // ---------------------------------------------------------------------------
+// 3x3 convolutions (stride 1, padding 1) over 64- or 128-channel bf16 images,
+// patch-staged.  The implicit GEMM above fetches every input pixel once per
+// tap (nine times); here a block owns an 8 x 8 tile of output pixels of one
+// image and BN output channels of one sub-slice, and for each 64-channel chunk
+// it stages the 10 x 10 input patch around its tile (one pixel of halo each
+// way, zeros outside the image) once, with the nine taps' weight rows, then
+// forms all nine taps' A fragments from that patch in LDS (about a sixth of the
+// A bytes; the win is largest on narrow sub-slices, whose A traffic dominates).  Loads use the same
+// whole-line, XOR-swizzled layout as above (patch pixels and weight rows in
+// place of tile rows).  The k order is chunk, then tap, then the two 32-wide
+// steps; it depends only on the op, not on BN or the sub-slice, so sub-sliced
+// and unsplit launches agree bit for bit.  Four waves each take two tile rows
+// (16 pixels) by BN columns; the accumulators start at the bias and the
+// epilogue stores from the MFMA layout (residual, activation).
+// ---------------------------------------------------------------------------
+constexpr int HT = 8;                        // output tile side (64 pixels = 64 GEMM rows)
+constexpr int HP = HT + 2;                   // patch side
+constexpr int HPIX = HP * HP;                // 100 patch pixels
+constexpr int HPBLK = (HPIX + 7) / 8;        // 13 load blocks of 8 pixels
+
+bool conv_halo_ok(int dtype, int kh, int kw, int stride, int pad, int cs, int n_out, int out_h, int out_w) {
+    // (convs with more than 128 outputs, or over images above 56 x 56 -- VGG-16's first three
+    // blocks -- ran slower here than on the implicit GEMM's larger tiles, measured: the patch is
+    // re-read for every 16 output channels, and small tiles multiply the per-block costs)
+    return dtype == MOPAR_BF16 && kh == 3 && kw == 3 && stride == 1 && pad == 1 && cs % 64 == 0 && cs <= 128 &&
+           n_out <= 128 && out_h >= 16 && out_w >= 16 && out_h * out_w <= 56 * 56;
+}
+
+template <int BN>
+__global__ __launch_bounds__(256) void conv3_halo_kernel(const GemmParams p) {
+    using T = __bf16;
+    constexpr int FN = BN / 16;
+    constexpr int BPT = BN / 8;                 // weight load blocks per tap
+    constexpr int NBB = 9 * BPT;                // weight load blocks per chunk
+    constexpr int LP = (HPBLK + 3) / 4, LB = (NBB + 3) / 4;   // load slots per wave
+    __shared__ uint4 lds[(HPBLK + NBB) * 64];   // one chunk: patch blocks, then weight blocks
+    touch_kernargs<sizeof(GemmParams)>();
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+
+    // block -> (image, spatial tile, sub-slice, n tile); the blocks that share a patch are
+    // consecutive, and each XCD runs a contiguous range of them
+    const unsigned t = (blockIdx.x % 8) * static_cast<unsigned>(p.g_per_xcd) + blockIdx.x / 8;
+    if (t >= static_cast<unsigned>(p.g_total)) return;
+    const unsigned tile = p.g_div_group.div(t);
+    const unsigned col = t - tile * static_cast<unsigned>(p.g_cols);
+    const unsigned j = p.g_div_nt.div(col);
+    const int nti = static_cast<int>(col - j * static_cast<unsigned>(p.g_nt));
+    const unsigned img = p.h_div_tiles.div(tile);
+    const unsigned tin = tile - img * static_cast<unsigned>(p.h_tiles);
+    const unsigned tyi = p.h_div_tx.div(tin);
+    const int oh0 = static_cast<int>(tyi) * HT, ow0 = static_cast<int>(tin - tyi * static_cast<unsigned>(p.h_tx)) * HT;
+    const int jj = static_cast<int>(j);
+    const int n_lo = jj * p.g_q + min(jj, p.g_rr), n_hi = (jj + 1) * p.g_q + min(jj + 1, p.g_rr);
+    const int n0 = n_lo + nti * BN;
+    if (n0 >= n_hi) return;                     // block-uniform, before any barrier
+
+    // loads of chunk q: patch block b covers pixels 8b .. 8b + 7 (pixel pp at patch row pp / 10,
+    // column pp % 10), weight block b covers rows 8 (b % BPT) .. +7 of tap b / BPT; lane l takes
+    // entity 8b + l / 8, chunk cl = (l % 8) ^ (l / 8); a chunk's byte offset adds 128 q
+    const int cl = (lane & 7) ^ (lane >> 3);
+    const unsigned pix_bytes = static_cast<unsigned>(p.cs) * 2u;
+    unsigned voffP[LP], voffB[LB];
+#pragma unroll
+    for (int i = 0; i < LP; ++i) {
+        const int pp = 8 * min(wave + 4 * i, HPBLK - 1) + (lane >> 3);
+        const int ih = oh0 - 1 + pp / HP, iw = ow0 - 1 + pp % HP;
+        const bool in = pp < HPIX && static_cast<unsigned>(ih) < static_cast<unsigned>(p.img_h) &&
+                        static_cast<unsigned>(iw) < static_cast<unsigned>(p.img_w);
+        voffP[i] = in ? (static_cast<unsigned>((static_cast<int>(img) * p.img_h + ih) * p.img_w + iw)) * pix_bytes +
+                            static_cast<unsigned>(cl * 16)
+                      : kOOB;
+    }
+#pragma unroll
+    for (int i = 0; i < LB; ++i) {
+        const int b = min(wave + 4 * i, NBB - 1);
+        const int tap = b / BPT, n = min(n0 + (b % BPT) * 8 + (lane >> 3), n_hi - 1);
+        voffB[i] = static_cast<unsigned>(n) * static_cast<unsigned>(p.K * 2) + static_cast<unsigned>(tap) * pix_bytes +
+                   static_cast<unsigned>(cl * 16);
+    }
+
+    // epilogue set-up (MFMA layout): this lane's tile pixel and four columns per n fragment
+    const int pix = wave * 16 + (lane & 15);
+    const int oh = oh0 + (pix >> 3), ow = ow0 + (pix & 7);
+    const bool row_ok = oh < p.out_h && ow < p.out_w;
+    const int64_t row = (static_cast<int64_t>(img) * p.out_h + oh) * p.out_w + ow;
+    int ncol[FN], nval[FN];
+    f32x4 acc[FN];
+#pragma unroll
+    for (int b = 0; b < FN; ++b) {
+        ncol[b] = n0 + b * 16 + (lane >> 4) * 4;
+        nval[b] = max(0, min(4, n_hi - ncol[b]));
+        float bv[4], b2v[4];
+        ld4_or_zero<T>(static_cast<const T*>(p.bias), ncol[b], nval[b], bv);
+        ld4_or_zero<T>(static_cast<const T*>(p.bias2), ncol[b], nval[b], b2v);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[b][e] = bv[e] + b2v[e];
+    }
+
+    const unsigned lds0 = static_cast<unsigned>(reinterpret_cast<size_t>((lds_ptr_t)(&lds[0])));
+    const int nq = p.cs / 64;
+    for (int qc = 0; qc < nq; ++qc) {
+        if (qc > 0) __syncthreads();            // the previous chunk's fragments have been read
+        const unsigned soff = static_cast<unsigned>(qc) * 128u;
+#pragma unroll
+        for (int i = 0; i < LP; ++i) {
+            if (HPBLK % 4 != 0 && i == LP - 1 && wave + 4 * i >= HPBLK) break;   // wave-uniform
+            buffer_load_lds(p.A, p.a_bytes, (lds_ptr_t)(&lds[(wave + 4 * i) * 64]), voffP[i], soff);
+        }
+#pragma unroll
+        for (int i = 0; i < LB; ++i) {
+            if (NBB % 4 != 0 && i == LB - 1 && wave + 4 * i >= NBB) break;
+            buffer_load_lds(p.B, p.b_bytes, (lds_ptr_t)(&lds[(HPBLK + wave + 4 * i) * 64]), voffB[i], soff);
+        }
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+#pragma unroll
+        for (int tap = 0; tap < 9; ++tap) {
+            const int pp = ((pix >> 3) + tap / 3) * HP + (pix & 7) + tap % 3;
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                const int ch = 4 * ks + (lane >> 4);
+                u32x4 af = lds_read16(lds0 + static_cast<unsigned>(pp * 128 + ((ch ^ (pp & 7)) << 4)));
+                u32x4 bf[FN];
+#pragma unroll
+                for (int b = 0; b < FN; ++b) {
+                    const int nb = b * 16 + (lane & 15);
+                    bf[b] = lds_read16(lds0 + static_cast<unsigned>((HPBLK * 64 + (tap * BN + nb) * 8 + (ch ^ (nb & 7))) * 16));
+                }
+                lds_wait();
+                pin(af);
+#pragma unroll
+                for (int b = 0; b < FN; ++b) {
+                    pin(bf[b]);
+                    acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, bf[b]),
+                                                                   __builtin_bit_cast(bf16x8, af), acc[b], 0, 0, 0);
+                }
+            }
+        }
+    }
+
+    if (!row_ok) return;
+    const T* resp = static_cast<const T*>(p.res);
+#pragma unroll
+    for (int b = 0; b < FN; ++b) {
+        if (nval[b] == 0) continue;
+        const int64_t idx = row * p.ldc + ncol[b];
+        float v[4], rv[4] = {0.f, 0.f, 0.f, 0.f};
+        if (resp) ld4<T>(resp, idx, nval[b], rv);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = act_f(acc[b][e] + rv[e], p.act);
+        if (p.out_f32)
+            store4<float>(static_cast<float*>(p.C), idx, v, nval[b]);
+        else
+            store4<T>(static_cast<T*>(p.C), idx, v, nval[b]);
+    }
+}
+
+template <int BN>
+static hipError_t launch_halo(const GemmParams& params, int width, hipStream_t st) {
+    GemmParams p = params;
+    const int64_t nt = (width + BN - 1) / BN;
+    const int ty = (p.out_h + HT - 1) / HT, tx = (p.out_w + HT - 1) / HT;
+    const int64_t imgs = p.M / (static_cast<int64_t>(p.out_h) * p.out_w);
+    const int64_t total = imgs * ty * tx * p.ksub * nt;
+    if (total >= (int64_t(1) << 31) / 8 || static_cast<int64_t>(ty) * tx * p.ksub * nt >= (int64_t(1) << 31))
+        return hipErrorInvalidValue;
+    p.g_total = static_cast<int>(total);
+    p.g_per_xcd = static_cast<int>((total + 7) / 8);
+    p.g_nt = static_cast<int>(nt);
+    p.g_cols = static_cast<int>(nt * p.ksub);
+    p.g_q = p.N / p.ksub;
+    p.g_rr = p.N % p.ksub;
+    p.g_div_group = FastDiv(static_cast<unsigned>(p.g_cols));
+    p.g_div_nt = FastDiv(static_cast<unsigned>(nt));
+    p.h_tiles = ty * tx;
+    p.h_tx = tx;
+    p.h_div_tiles = FastDiv(static_cast<unsigned>(ty * tx));
+    p.h_div_tx = FastDiv(static_cast<unsigned>(tx));
+    const int64_t grid = (total + 7) / 8 * 8;
+    launch_kernel(conv3_halo_kernel<BN>, dim3(static_cast<unsigned>(grid)), dim3(256), 0, st, p);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Tile selection.  All shapes share the K loop, so the choice only affects
 // speed, never the bits of a result.
 // ---------------------------------------------------------------------------
@@ -961,6 +1146,11 @@ hipError_t launch_gemm(const GemmParams& params, int dtype, hipStream_t stream) 
     p.a_bytes = static_cast<uint32_t>(a_bytes);
     p.b_bytes = static_cast<uint32_t>(b_bytes);
     if (p.splits < 1 || (p.splits > 1 && (!p.partial || p.epi != EPI_STD))) return hipErrorInvalidValue;
+    if (p.conv && conv_halo_ok(dtype, p.kh, p.kw, p.stride, p.pad, p.cs, p.N, p.out_h, p.out_w)) {
+        if (p.splits != 1 || p.epi != EPI_STD) return hipErrorInvalidValue;
+        // 16-column tiles at every width (measured at least as fast as 32 on 32-wide sub-slices)
+        return launch_halo<16>(p, (p.N + p.ksub - 1) / p.ksub, stream);
+    }
     hipError_t e = dtype == MOPAR_BF16 ? dispatch<__bf16>(p, stream) : dispatch<float>(p, stream);
     if (e != hipSuccess || p.splits == 1) return e;
     const int64_t n = p.M * ((p.N + 3) / 4);

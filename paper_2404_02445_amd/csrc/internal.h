@@ -115,6 +115,9 @@ struct GemmParams {
     int g_mt, g_nt, g_total, g_per_xcd, g_cols, g_nk, g_q, g_rr;
     FastDiv g_div_group, g_div_last, g_div_nt, g_div_ksub, g_div_splits;
     FastDiv r_div_groups;   // split-K reduce: divide by ceil(N / 4) (set by launch_gemm)
+    // patch-staged 3x3 conv: spatial tiles per image and per tile row, and their divisors
+    int h_tiles, h_tx;
+    FastDiv h_div_tiles, h_div_tx;
 };
 
 // Split-K factor used for an (M, N, K) product.  A function of the shape
@@ -126,6 +129,12 @@ inline size_t gemm_partial_bytes(int64_t M, int N, int splits) {
 }
 
 enum { EPI_STD = 0, EPI_LSTM = 1 };
+
+// Whether a conv runs on the patch-staged 3x3 kernel (bf16, 3x3, stride 1, padding 1, 64 or 128
+// input channels, at most 128 outputs, output from 16 x 16 up to 56 x 56 pixels).  A function of
+// the op's geometry only -- never of the sub-slice count -- so sub-sliced and unsplit launches of
+// one op take the same path; such convs never split K.
+bool conv_halo_ok(int dtype, int kh, int kw, int stride, int pad, int cs, int n_out, int out_h, int out_w);
 
 hipError_t launch_gemm(const GemmParams& p, int dtype, hipStream_t stream);
 

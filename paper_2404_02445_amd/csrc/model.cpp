@@ -337,7 +337,10 @@ static int validate_and_build(mopar_model_s& m) {
                 if (!wcheck(op.w, op.n_out * inf.K, "w") || !wcheck(op.b, op.n_out, "b"))
                     return set_error(MOPAR_E_ARG, nm + ": weight offsets out of range or not 16-byte aligned");
                 if (xin) inf.temps.push_back(static_cast<size_t>(x.dims[0] * x.dims[2] * x.dims[3] * inf.cs) * es);
-                inf.splits = gemm_splits(inf.M, op.n_out, static_cast<int>(inf.K), m.dtype, EPI_STD);
+                inf.splits = conv_halo_ok(m.dtype, op.kh, op.kw, op.stride, op.pad, inf.cs, op.n_out,
+                                          static_cast<int>(ho), static_cast<int>(wo))
+                                 ? 1
+                                 : gemm_splits(inf.M, op.n_out, static_cast<int>(inf.K), m.dtype, EPI_STD);
                 if (inf.splits > 1) {
                     inf.partial_temp = static_cast<int>(inf.temps.size());
                     inf.temps.push_back(gemm_partial_bytes(inf.M, op.n_out, inf.splits));

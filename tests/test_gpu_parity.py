@@ -68,7 +68,9 @@ def conv_model(dtype, n, c, hw, cout, k, stride, pad, act="relu", residual=False
 CONV_CASES = [
     # dtype, n, c, hw, cout, k, stride, pad, residual, pre
     ("bf16", 2, 3, 37, 64, 7, 2, 3, False, False),    # stem-like, padded channels, ragged M
-    ("bf16", 1, 64, 19, 48, 3, 1, 1, True, True),     # 3x3, residual, ragged N tile
+    ("bf16", 1, 64, 19, 48, 3, 1, 1, True, True),     # 3x3, residual, ragged N tile (patch-staged)
+    ("bf16", 2, 128, 20, 64, 3, 1, 1, False, True),   # patch-staged 3x3: two channel chunks, ragged tiles
+    ("bf16", 1, 64, 16, 120, 3, 1, 1, True, True),    # patch-staged 3x3: whole tiles, ragged sub-slices
     ("bf16", 2, 32, 14, 96, 3, 2, 1, True, True),     # strided 3x3
     ("bf16", 1, 128, 9, 256, 1, 1, 0, True, True),    # 1x1 wide
     ("bf16", 3, 16, 11, 20, 1, 2, 0, False, True),    # strided 1x1, N=20
