@@ -872,10 +872,7 @@ __global__ void splitk_reduce_kernel(const GemmParams p) {
 // (16 pixels) by BN columns; the accumulators start at the bias and the
 // epilogue stores from the MFMA layout (residual, activation).
 // ---------------------------------------------------------------------------
-constexpr int HT = 8;                        // output tile side (64 pixels = 64 GEMM rows)
-constexpr int HP = HT + 2;                   // patch side
-constexpr int HPIX = HP * HP;                // 100 patch pixels
-constexpr int HPBLK = (HPIX + 7) / 8;        // 13 load blocks of 8 pixels
+constexpr int HTW = 8;                       // output tile width; its height TH is a parameter
 
 bool conv_halo_ok(int dtype, int kh, int kw, int stride, int pad, int cs, int n_out, int out_h, int out_w) {
     // (convs with more than 128 outputs, or over images above 56 x 56 -- VGG-16's first three
@@ -885,13 +882,16 @@ bool conv_halo_ok(int dtype, int kh, int kw, int stride, int pad, int cs, int n_
            n_out <= 128 && out_h >= 16 && out_w >= 16 && out_h * out_w <= 56 * 56;
 }
 
-template <int BN>
-__global__ __launch_bounds__(256) void conv3_halo_kernel(const GemmParams p) {
+template <int BN, int TH>
+__global__ __launch_bounds__(TH * HTW / 16 * 64) void conv3_halo_kernel(const GemmParams p) {
     using T = __bf16;
+    constexpr int NW = TH * HTW / 16;           // waves: 16 tile pixels (two tile rows) each
+    constexpr int PW = HTW + 2, PIX = (TH + 2) * PW;   // patch width, pixels
+    constexpr int HPBLK = (PIX + 7) / 8;        // patch load blocks of 8 pixels
     constexpr int FN = BN / 16;
     constexpr int BPT = BN / 8;                 // weight load blocks per tap
     constexpr int NBB = 9 * BPT;                // weight load blocks per chunk
-    constexpr int LP = (HPBLK + 3) / 4, LB = (NBB + 3) / 4;   // load slots per wave
+    constexpr int LP = (HPBLK + NW - 1) / NW, LB = (NBB + NW - 1) / NW;   // load slots per wave
     __shared__ uint4 lds[(HPBLK + NBB) * 64];   // one chunk: patch blocks, then weight blocks
     touch_kernargs<sizeof(GemmParams)>();
     const int lane = threadIdx.x & 63;
@@ -908,7 +908,7 @@ __global__ __launch_bounds__(256) void conv3_halo_kernel(const GemmParams p) {
     const unsigned img = p.h_div_tiles.div(tile);
     const unsigned tin = tile - img * static_cast<unsigned>(p.h_tiles);
     const unsigned tyi = p.h_div_tx.div(tin);
-    const int oh0 = static_cast<int>(tyi) * HT, ow0 = static_cast<int>(tin - tyi * static_cast<unsigned>(p.h_tx)) * HT;
+    const int oh0 = static_cast<int>(tyi) * TH, ow0 = static_cast<int>(tin - tyi * static_cast<unsigned>(p.h_tx)) * HTW;
     const int jj = static_cast<int>(j);
     const int n_lo = jj * p.g_q + min(jj, p.g_rr), n_hi = (jj + 1) * p.g_q + min(jj + 1, p.g_rr);
     const int n0 = n_lo + nti * BN;
@@ -922,9 +922,9 @@ __global__ __launch_bounds__(256) void conv3_halo_kernel(const GemmParams p) {
     unsigned voffP[LP], voffB[LB];
 #pragma unroll
     for (int i = 0; i < LP; ++i) {
-        const int pp = 8 * min(wave + 4 * i, HPBLK - 1) + (lane >> 3);
-        const int ih = oh0 - 1 + pp / HP, iw = ow0 - 1 + pp % HP;
-        const bool in = pp < HPIX && static_cast<unsigned>(ih) < static_cast<unsigned>(p.img_h) &&
+        const int pp = 8 * min(wave + NW * i, HPBLK - 1) + (lane >> 3);
+        const int ih = oh0 - 1 + pp / PW, iw = ow0 - 1 + pp % PW;
+        const bool in = pp < PIX && static_cast<unsigned>(ih) < static_cast<unsigned>(p.img_h) &&
                         static_cast<unsigned>(iw) < static_cast<unsigned>(p.img_w);
         voffP[i] = in ? (static_cast<unsigned>((static_cast<int>(img) * p.img_h + ih) * p.img_w + iw)) * pix_bytes +
                             static_cast<unsigned>(cl * 16)
@@ -932,7 +932,7 @@ __global__ __launch_bounds__(256) void conv3_halo_kernel(const GemmParams p) {
     }
 #pragma unroll
     for (int i = 0; i < LB; ++i) {
-        const int b = min(wave + 4 * i, NBB - 1);
+        const int b = min(wave + NW * i, NBB - 1);
         const int tap = b / BPT, n = min(n0 + (b % BPT) * 8 + (lane >> 3), n_hi - 1);
         voffB[i] = static_cast<unsigned>(n) * static_cast<unsigned>(p.K * 2) + static_cast<unsigned>(tap) * pix_bytes +
                    static_cast<unsigned>(cl * 16);
@@ -963,19 +963,19 @@ __global__ __launch_bounds__(256) void conv3_halo_kernel(const GemmParams p) {
         const unsigned soff = static_cast<unsigned>(qc) * 128u;
 #pragma unroll
         for (int i = 0; i < LP; ++i) {
-            if (HPBLK % 4 != 0 && i == LP - 1 && wave + 4 * i >= HPBLK) break;   // wave-uniform
-            buffer_load_lds(p.A, p.a_bytes, (lds_ptr_t)(&lds[(wave + 4 * i) * 64]), voffP[i], soff);
+            if (HPBLK % NW != 0 && i == LP - 1 && wave + NW * i >= HPBLK) break;   // wave-uniform
+            buffer_load_lds(p.A, p.a_bytes, (lds_ptr_t)(&lds[(wave + NW * i) * 64]), voffP[i], soff);
         }
 #pragma unroll
         for (int i = 0; i < LB; ++i) {
-            if (NBB % 4 != 0 && i == LB - 1 && wave + 4 * i >= NBB) break;
-            buffer_load_lds(p.B, p.b_bytes, (lds_ptr_t)(&lds[(HPBLK + wave + 4 * i) * 64]), voffB[i], soff);
+            if (NBB % NW != 0 && i == LB - 1 && wave + NW * i >= NBB) break;
+            buffer_load_lds(p.B, p.b_bytes, (lds_ptr_t)(&lds[(HPBLK + wave + NW * i) * 64]), voffB[i], soff);
         }
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __builtin_amdgcn_s_barrier();
 #pragma unroll
         for (int tap = 0; tap < 9; ++tap) {
-            const int pp = ((pix >> 3) + tap / 3) * HP + (pix & 7) + tap % 3;
+            const int pp = ((pix >> 3) + tap / 3) * PW + (pix & 7) + tap % 3;
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
                 const int ch = 4 * ks + (lane >> 4);
@@ -1015,11 +1015,11 @@ __global__ __launch_bounds__(256) void conv3_halo_kernel(const GemmParams p) {
     }
 }
 
-template <int BN>
+template <int BN, int TH>
 static hipError_t launch_halo(const GemmParams& params, int width, hipStream_t st) {
     GemmParams p = params;
     const int64_t nt = (width + BN - 1) / BN;
-    const int ty = (p.out_h + HT - 1) / HT, tx = (p.out_w + HT - 1) / HT;
+    const int ty = (p.out_h + TH - 1) / TH, tx = (p.out_w + HTW - 1) / HTW;
     const int64_t imgs = p.M / (static_cast<int64_t>(p.out_h) * p.out_w);
     const int64_t total = imgs * ty * tx * p.ksub * nt;
     if (total >= (int64_t(1) << 31) / 8 || static_cast<int64_t>(ty) * tx * p.ksub * nt >= (int64_t(1) << 31))
@@ -1037,7 +1037,7 @@ static hipError_t launch_halo(const GemmParams& params, int width, hipStream_t s
     p.h_div_tiles = FastDiv(static_cast<unsigned>(ty * tx));
     p.h_div_tx = FastDiv(static_cast<unsigned>(tx));
     const int64_t grid = (total + 7) / 8 * 8;
-    launch_kernel(conv3_halo_kernel<BN>, dim3(static_cast<unsigned>(grid)), dim3(256), 0, st, p);
+    launch_kernel(conv3_halo_kernel<BN, TH>, dim3(static_cast<unsigned>(grid)), dim3(TH * HTW / 16 * 64), 0, st, p);
     return hipGetLastError();
 }
 
@@ -1149,7 +1149,7 @@ hipError_t launch_gemm(const GemmParams& params, int dtype, hipStream_t stream) 
     if (p.conv && conv_halo_ok(dtype, p.kh, p.kw, p.stride, p.pad, p.cs, p.N, p.out_h, p.out_w)) {
         if (p.splits != 1 || p.epi != EPI_STD) return hipErrorInvalidValue;
         // 16-column tiles at every width (measured at least as fast as 32 on 32-wide sub-slices)
-        return launch_halo<16>(p, (p.N + p.ksub - 1) / p.ksub, stream);
+        return launch_halo<16, 8>(p, (p.N + p.ksub - 1) / p.ksub, stream);
     }
     hipError_t e = dtype == MOPAR_BF16 ? dispatch<__bf16>(p, stream) : dispatch<float>(p, stream);
     if (e != hipSuccess || p.splits == 1) return e;
