@@ -79,25 +79,33 @@ def read_counters(path):
     return out
 
 
+# the kernels that run the GEMM ops (conv / linear / AE codec): the implicit-GEMM kernel and the
+# patch-staged 3x3 conv
+GEMM_KERNELS = ("gemm_kernel", "conv3_halo_kernel")
+
+
 def summarize_pmc(fetch_csv, write_csv, copy_mib):
-    """Markdown summary of per-dispatch HBM-side traffic of gemm_kernel, scaled by the
+    """Markdown summary of per-dispatch HBM-side traffic of the GEMM-op kernels, scaled by the
     counters of a raw copy of known size (copy_mib MiB read and written)."""
     fetch, write = read_counters(fetch_csv), read_counters(write_csv)
     def avg(rows, key):
-        v = [val for name, val in rows.values() if key in name]
+        keys = key if isinstance(key, tuple) else (key,)
+        v = [val for name, val in rows.values() if any(k in name for k in keys)]
         return (sum(v) / len(v), len(v)) if v else (0.0, 0)
     # calibration: the largest copy_kernel dispatch is the known-size copy
     cf = max((val for name, val in fetch.values() if "copy_kernel" in name), default=0.0)
     cw = max((val for name, val in write.values() if "copy_kernel" in name), default=0.0)
     kib = copy_mib * 1024.0
     sf, sw = (kib / cf if cf else float("nan")), (kib / cw if cw else float("nan"))
-    gf, n_f = avg(fetch, "gemm_kernel")
-    gw, n_w = avg(write, "gemm_kernel")
+    gf, n_f = avg(fetch, GEMM_KERNELS)
+    gw, n_w = avg(write, GEMM_KERNELS)
+    hf, n_h = avg(fetch, "conv3_halo_kernel")
+    hw, _ = avg(write, "conv3_halo_kernel")
     rf, n_r = avg(fetch, "splitk_reduce_kernel")
     rw, _ = avg(write, "splitk_reduce_kernel")
     traffic = (gf * sf + gw * sw) * 1024.0
     lines = [
-        "# gemm_kernel HBM-side traffic, ResNet-50 bf16 batch 8 (sequential sliced forward)",
+        "# GEMM-op kernels' HBM-side traffic, ResNet-50 bf16 batch 8 (sequential sliced forward)",
         "",
         "Counters: rocprofv3 `FETCH_SIZE` and `WRITE_SIZE` (KiB per dispatch), one pass each,",
         f"scaled by the same counters read for a raw copy of {copy_mib} MiB in the same run.",
@@ -106,10 +114,11 @@ def summarize_pmc(fetch_csv, write_csv, copy_mib):
         "|---|---|",
         f"| copy calibration: FETCH_SIZE / WRITE_SIZE of the {copy_mib} MiB copy (KiB) | {cf:.1f} / {cw:.1f} |",
         f"| scale factors (read, write) | {sf:.4f} / {sw:.4f} |",
-        f"| gemm_kernel dispatches (fetch pass / write pass) | {n_f} / {n_w} |",
-        f"| gemm_kernel mean FETCH_SIZE / WRITE_SIZE per dispatch (KiB) | {gf:.1f} / {gw:.1f} |",
+        f"| GEMM-op dispatches, gemm_kernel and conv3_halo_kernel (fetch pass / write pass) | {n_f} / {n_w} |",
+        f"| their mean FETCH_SIZE / WRITE_SIZE per dispatch (KiB) | {gf:.1f} / {gw:.1f} |",
+        f"| of which conv3_halo_kernel: dispatches, mean FETCH / WRITE (KiB) | {n_h}, {hf:.1f} / {hw:.1f} |",
         f"| splitk_reduce_kernel dispatches, mean FETCH / WRITE (KiB) | {n_r}, {rf:.1f} / {rw:.1f} |",
-        f"| traffic per gemm_kernel launch (scaled read + write, bytes) | {traffic:.0f} |",
+        f"| traffic per GEMM-op launch (scaled read + write, bytes) | {traffic:.0f} |",
         "",
         "```",
         f"gemm_hip_sha256: {gemm_source_hash()}",
@@ -436,9 +445,10 @@ def main():
         traffic = committed_traffic() if m.name.startswith("resnet50") else None
         res["roofline"] = {
             "bound": "mfma",
-            "kernel": "gemm_kernel: every conv / linear op and AE codec GEMM of a step (device time of "
-                      "each launch from its own HIP event pair; an op's time also holds the stem's layout "
-                      "conversion and the split-K reduce of split ops)",
+            "kernel": "gemm_kernel (conv3_halo_kernel for the patch-staged 3x3 convs): every conv / linear "
+                      "op and AE codec GEMM of a step (device time of each launch from its own HIP event "
+                      "pair; an op's time also holds the stem's layout conversion and the split-K reduce "
+                      "of split ops)",
             "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4),
             "traffic": round(traffic) if traffic is not None else None,
