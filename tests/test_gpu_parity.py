@@ -68,6 +68,7 @@ def conv_model(dtype, n, c, hw, cout, k, stride, pad, act="relu", residual=False
 CONV_CASES = [
     # dtype, n, c, hw, cout, k, stride, pad, residual, pre
     ("bf16", 2, 3, 37, 64, 7, 2, 3, False, False),    # stem-like, padded channels, ragged M
+    ("bf16", 2, 3, 30, 40, 3, 1, 1, False, False),    # first layer 3x3: ragged tiles and columns
     ("bf16", 1, 64, 19, 48, 3, 1, 1, True, True),     # 3x3, residual, ragged N tile (patch-staged)
     ("bf16", 2, 128, 20, 64, 3, 1, 1, False, True),   # patch-staged 3x3: two channel chunks, ragged tiles
     ("bf16", 1, 64, 16, 120, 3, 1, 1, True, True),    # patch-staged 3x3: whole tiles, ragged sub-slices
