@@ -527,10 +527,13 @@ __device__ __forceinline__ bf16x8_t lds8(const __bf16* p) { return *reinterpret_
 
 __global__ __launch_bounds__(256) void attention_mfma_kernel(const __bf16* __restrict__ qkv, __bf16* __restrict__ y,
                                                              int seq, int heads, float scale, int n_tiles) {
-    __shared__ __attribute__((aligned(16))) __bf16 sq[AM_Q * AM_LD];
-    __shared__ __attribute__((aligned(16))) __bf16 sk[AM_K * AM_LD];
+    // P reuses the Q and K space once S = Q K^T is done (45 KB in all: three blocks per CU)
+    static_assert(4 * 16 * AM_LP <= (AM_Q + AM_K) * AM_LD, "P fits where Q and K were");
+    __shared__ __attribute__((aligned(16))) __bf16 sqk[(AM_Q + AM_K) * AM_LD];
     __shared__ __attribute__((aligned(16))) __bf16 svt[AM_D * AM_LP];
-    __shared__ __attribute__((aligned(16))) __bf16 sp[4 * 16 * AM_LP];
+    __bf16* const sq = sqk;
+    __bf16* const sk = sqk + AM_Q * AM_LD;
+    __bf16* const sp = sqk;
     // The XCDs take blocks round-robin: number the tiles so that each XCD runs a contiguous
     // range, and the query tiles of one (batch, head) -- which read the same K and V -- run
     // on the same XCD at about the same time, K and V coming from its L2 after the first.
@@ -598,6 +601,7 @@ __global__ __launch_bounds__(256) void attention_mfma_kernel(const __bf16* __res
         }
     mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    __syncthreads();                                   // every wave is done with Q and K: P goes there
     float sum = 0.0f;
     __bf16* prow = &sp[(wave * 16 + lr) * AM_LP];
 #pragma unroll
