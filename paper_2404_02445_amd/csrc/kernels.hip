@@ -435,20 +435,22 @@ hipError_t launch_embed_bert(const int32_t* ids, const void* tok, const void* po
 // ---------------------------------------------------------------------------
 // Plain embedding gather: one thread per 16-byte chunk of an output row.
 // ---------------------------------------------------------------------------
-__global__ void embed_kernel(const int32_t* __restrict__ ids, const uint4* __restrict__ table,
-                             uint4* __restrict__ y, int64_t rows, int chunks) {
-    const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (t >= rows * chunks) return;
-    const int64_t row = t / chunks;
-    const int c = static_cast<int>(t - row * chunks);
-    y[t] = table[static_cast<int64_t>(ids[row]) * chunks + c];
+// one block per token: the id is one (scalar) load per block, then the row's 16-byte chunks
+__global__ __launch_bounds__(128) void embed_kernel(const int32_t* __restrict__ ids, const uint4* __restrict__ table,
+                                                    uint4* __restrict__ y, int chunks) {
+    const int64_t row = blockIdx.x;
+    const uint4* src = table + static_cast<int64_t>(ids[row]) * chunks;
+    uint4* dst = y + row * chunks;
+    for (int c = threadIdx.x; c < chunks; c += 128) dst[c] = src[c];
 }
 
 hipError_t launch_embed(const int32_t* ids, const void* table, void* y, int64_t n, int f, int dtype,
                         hipStream_t s) {
     const int chunks = static_cast<int>(f * dtype_size(dtype) / 16);
-    launch_kernel(embed_kernel, dim3(blocks_for(n * chunks, 256)), dim3(256), 0, s, ids,
-                       static_cast<const uint4*>(table), static_cast<uint4*>(y), n, chunks);
+    if (n >= (int64_t(1) << 31)) return hipErrorInvalidValue;
+    if (n == 0) return hipSuccess;
+    launch_kernel(embed_kernel, dim3(static_cast<unsigned>(n)), dim3(128), 0, s, ids, static_cast<const uint4*>(table),
+                  static_cast<uint4*>(y), chunks);
     return hipGetLastError();
 }
 
