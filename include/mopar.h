@@ -154,7 +154,9 @@ typedef enum {
     MOPAR_OP_ATTENTION = 6,  /* in0 (B,S,3F) = [Q|K|V] -> out (B,S,F); heads; scale; head dim 64  */
     MOPAR_OP_EMBED_BERT = 7, /* ids (B,S) -> LN(tok[id] + pos[s] + type[0]); w: tok [V][F];
                                 w2: pos [P][F]; w3: type [T][F]; w4: gamma; w5: beta; eps        */
-    MOPAR_OP_EMBED = 8,      /* ids (B,S) -> table[id]; w: table [V][F]                           */
+    MOPAR_OP_EMBED = 8,      /* ids (B,S) -> table[id]; w: table [V][F].  For both embeddings an
+                                id outside [0, V) is clamped to the nearest row (no error, no
+                                access past the table); V < 2^31                                 */
     MOPAR_OP_LSTM = 9        /* in0 (B,T,E) -> out (B,T,H) hidden sequence, h0 = c0 = 0;
                                 w: W_ih [4H][E], w2: W_hh [4H][H], b: b_ih [4H], w3: b_hh [4H];
                                 rows interleaved by unit: row 4u+g holds gate g (i,f,g,o) of

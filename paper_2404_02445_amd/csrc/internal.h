@@ -152,10 +152,12 @@ hipError_t launch_maxpool(const void* x, void* y, int n, int h, int w, int c, in
 hipError_t launch_avgpool(const void* x, void* y, int n, int hw, int c, int dtype, hipStream_t s);
 hipError_t launch_layernorm(const void* x, const void* res, const void* g, const void* b, void* y,
                             int64_t rows, int f, float eps, int dtype, hipStream_t s);
+// (embeddings clamp ids to [0, vocab): an out-of-range id reads the nearest row, never memory
+// past the table)
 hipError_t launch_embed_bert(const int32_t* ids, const void* tok, const void* pos, const void* type,
-                             const void* g, const void* b, void* y, int batch, int seq, int f, float eps,
-                             int dtype, hipStream_t s);
-hipError_t launch_embed(const int32_t* ids, const void* table, void* y, int64_t n, int f, int dtype,
+                             const void* g, const void* b, void* y, int batch, int seq, int vocab, int f,
+                             float eps, int dtype, hipStream_t s);
+hipError_t launch_embed(const int32_t* ids, const void* table, void* y, int64_t n, int f, int vocab, int dtype,
                         hipStream_t s);
 hipError_t launch_attention(const void* qkv, void* y, int batch, int seq, int heads, float scale, int dtype,
                             hipStream_t s);

@@ -390,13 +390,13 @@ hipError_t launch_layernorm(const void* x, const void* res, const void* g, const
 template <typename T, bool VEC, int MV>
 __global__ void embed_bert_kernel(const int32_t* __restrict__ ids, const T* __restrict__ tok,
                                   const T* __restrict__ pos, const T* __restrict__ type, const T* __restrict__ g,
-                                  const T* __restrict__ b, T* __restrict__ y, int64_t rows, int seq, int f,
+                                  const T* __restrict__ b, T* __restrict__ y, int64_t rows, int seq, int vocab, int f,
                                   float eps) {
     const int lane = threadIdx.x & 63;
     const int64_t row = static_cast<int64_t>(blockIdx.x) * (blockDim.x / 64) + (threadIdx.x >> 6);
     if (row >= rows) return;
     const int sidx = static_cast<int>(row % seq);
-    const T* tr = tok + static_cast<int64_t>(ids[row]) * f;
+    const T* tr = tok + static_cast<int64_t>(min(max(ids[row], 0), vocab - 1)) * f;   // ids clamped to the table
     const T* pr = pos + static_cast<int64_t>(sidx) * f;
     float v[MV];
     ln_load<T, VEC, MV>(tr, pr, f, lane, v);
@@ -412,23 +412,25 @@ struct EmbK { static constexpr auto fn = embed_bert_kernel<T, VEC, MV>; };
 
 template <typename T>
 static void embed_bert_launch(const int32_t* ids, const void* tok, const void* pos, const void* type, const void* g,
-                              const void* b, void* y, int64_t rows, int seq, int f, float eps, hipStream_t s) {
+                              const void* b, void* y, int64_t rows, int seq, int vocab, int f, float eps,
+                              hipStream_t s) {
     const T *tp = static_cast<const T*>(tok), *pp = static_cast<const T*>(pos), *yp = static_cast<const T*>(type);
     const T *gp = static_cast<const T*>(g), *bp = static_cast<const T*>(b);
     ln_instance<T, EmbK>(f, [&](auto kern) {
         launch_kernel(kern, dim3(blocks_for(rows, 4)), dim3(256), 0, s, ids, tp, pp, yp, gp, bp, static_cast<T*>(y),
-                      rows, seq, f, eps);
+                      rows, seq, vocab, f, eps);
     });
 }
 
 hipError_t launch_embed_bert(const int32_t* ids, const void* tok, const void* pos, const void* type, const void* g,
-                             const void* b, void* y, int batch, int seq, int f, float eps, int dtype,
+                             const void* b, void* y, int batch, int seq, int vocab, int f, float eps, int dtype,
                              hipStream_t s) {
     const int64_t rows = static_cast<int64_t>(batch) * seq;
+    if (vocab < 1) return hipErrorInvalidValue;
     if (dtype == MOPAR_BF16)
-        embed_bert_launch<__bf16>(ids, tok, pos, type, g, b, y, rows, seq, f, eps, s);
+        embed_bert_launch<__bf16>(ids, tok, pos, type, g, b, y, rows, seq, vocab, f, eps, s);
     else
-        embed_bert_launch<float>(ids, tok, pos, type, g, b, y, rows, seq, f, eps, s);
+        embed_bert_launch<float>(ids, tok, pos, type, g, b, y, rows, seq, vocab, f, eps, s);
     return hipGetLastError();
 }
 
@@ -436,21 +438,22 @@ hipError_t launch_embed_bert(const int32_t* ids, const void* tok, const void* po
 // Plain embedding gather: one thread per 16-byte chunk of an output row.
 // ---------------------------------------------------------------------------
 // one block per token: the id is one (scalar) load per block, then the row's 16-byte chunks
+// (an id outside [0, vocab) reads the nearest valid row instead of memory past the table)
 __global__ __launch_bounds__(128) void embed_kernel(const int32_t* __restrict__ ids, const uint4* __restrict__ table,
-                                                    uint4* __restrict__ y, int chunks) {
+                                                    uint4* __restrict__ y, int chunks, int vocab) {
     const int64_t row = blockIdx.x;
-    const uint4* src = table + static_cast<int64_t>(ids[row]) * chunks;
+    const uint4* src = table + static_cast<int64_t>(min(max(ids[row], 0), vocab - 1)) * chunks;
     uint4* dst = y + row * chunks;
     for (int c = threadIdx.x; c < chunks; c += 128) dst[c] = src[c];
 }
 
-hipError_t launch_embed(const int32_t* ids, const void* table, void* y, int64_t n, int f, int dtype,
+hipError_t launch_embed(const int32_t* ids, const void* table, void* y, int64_t n, int f, int vocab, int dtype,
                         hipStream_t s) {
     const int chunks = static_cast<int>(f * dtype_size(dtype) / 16);
-    if (n >= (int64_t(1) << 31)) return hipErrorInvalidValue;
+    if (n >= (int64_t(1) << 31) || vocab < 1) return hipErrorInvalidValue;
     if (n == 0) return hipSuccess;
     launch_kernel(embed_kernel, dim3(static_cast<unsigned>(n)), dim3(128), 0, s, ids, static_cast<const uint4*>(table),
-                  static_cast<uint4*>(y), chunks);
+                  static_cast<uint4*>(y), chunks, vocab);
     return hipGetLastError();
 }
 

@@ -407,6 +407,7 @@ static int validate_and_build(mopar_model_s& m) {
                 const int64_t f = y.dims[2];
                 if (op.rows[0] < 1 || op.rows[1] < x.dims[1] || op.rows[2] < 1 || f > 2048)
                     return set_error(MOPAR_E_SHAPE, nm + ": table rows (positions must cover seq)");
+                if (op.rows[0] >= (int64_t(1) << 31)) return set_error(MOPAR_E_UNSUPPORTED, nm + ": vocabulary >= 2^31");
                 if (!wcheck(op.w, op.rows[0] * f, "tok") || !wcheck(op.w2, op.rows[1] * f, "pos") ||
                     !wcheck(op.w3, op.rows[2] * f, "type") || !wcheck(op.w4, f, "g") || !wcheck(op.w5, f, "b"))
                     return set_error(MOPAR_E_ARG, nm + ": weight offsets out of range or not 16-byte aligned");
@@ -417,6 +418,7 @@ static int validate_and_build(mopar_model_s& m) {
                     return set_error(MOPAR_E_SHAPE, nm + ": embedding needs ids -> (..., F)");
                 const int64_t f = y.dims[y.rank - 1];
                 if ((f * static_cast<int64_t>(es)) % 16 != 0) return set_error(MOPAR_E_UNSUPPORTED, nm + ": row bytes % 16");
+                if (op.rows[0] >= (int64_t(1) << 31)) return set_error(MOPAR_E_UNSUPPORTED, nm + ": vocabulary >= 2^31");
                 if (op.rows[0] < 1 || !wcheck(op.w, op.rows[0] * f, "table"))
                     return set_error(MOPAR_E_ARG, nm + ": weight offsets out of range or not 16-byte aligned");
                 break;
@@ -667,10 +669,11 @@ static hipError_t run_op(const mopar_model_s& m, int i, const Ptrs& P, int ksub,
         case MOPAR_OP_EMBED_BERT:
             return launch_embed_bert(static_cast<const int32_t*>(P.get(op.in0)), W(m, op.w), W(m, op.w2), W(m, op.w3),
                                      W(m, op.w4), W(m, op.w5), P.get(op.out), static_cast<int>(x.dims[0]),
-                                     static_cast<int>(x.dims[1]), static_cast<int>(y.dims[2]), op.eps, dt, s);
+                                     static_cast<int>(x.dims[1]), static_cast<int>(op.rows[0]),
+                                     static_cast<int>(y.dims[2]), op.eps, dt, s);
         case MOPAR_OP_EMBED:
             return launch_embed(static_cast<const int32_t*>(P.get(op.in0)), W(m, op.w), P.get(op.out), numel(x),
-                                static_cast<int>(y.dims[y.rank - 1]), dt, s);
+                                static_cast<int>(y.dims[y.rank - 1]), static_cast<int>(op.rows[0]), dt, s);
         case MOPAR_OP_LSTM: {
             const int B = static_cast<int>(x.dims[0]), T = static_cast<int>(x.dims[1]), E = static_cast<int>(x.dims[2]);
             const int H = op.n_out;

@@ -222,6 +222,18 @@ def test_embed_gather_bitwise():
     np.testing.assert_array_equal(_np(y1), oracle.forward(m, ids))
 
 
+def test_embed_ids_out_of_range_clamped():
+    """Ids outside [0, V) read the nearest table row (documented in the header), never past it."""
+    bld, x = seq_input_model("bf16", 2, 5, 64)
+    m = bld.finish(x, 1)
+    v = 2 * 5
+    ids = np.array([[0, -3, 4, v, v + 1000], [-(1 << 30), 9, 1, 2, (1 << 31) - 1]], dtype=np.int32)
+    y1, _, _ = run_gpu(m, ids, P.make_plan(1, [0], [1]))
+    table = np.asarray(m.weights["src.table"])
+    want = table[np.clip(ids, 0, v - 1)]
+    np.testing.assert_array_equal(_np(y1), want.astype(np.float32))
+
+
 @pytest.mark.parametrize("b,t,e,h", [(3, 7, 64, 64), (64, 4, 128, 256), (2, 3, 24, 40), (37, 5, 32, 72)])
 def test_lstm(b, t, e, h):
     bld, x = seq_input_model("bf16", b, t, e)
