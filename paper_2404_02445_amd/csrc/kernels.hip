@@ -560,21 +560,27 @@ __global__ __launch_bounds__(256) void attention_mfma_kernel(const __bf16* __res
         *reinterpret_cast<uint4*>(&sq[r * AM_LD + c * 8]) = v;
     }
     // every key row of the tile is staged (zeros past seq), so the products below run over all
-    // AM_K keys with no data-dependent branches; the softmax masks keys >= seq
-    unsigned short* svt16 = reinterpret_cast<unsigned short*>(svt);
-    for (int i = threadIdx.x; i < AM_K * 8; i += 256) {
-        const int r = i >> 3, c = i & 7;
-        uint4 kv = zero4, vv = zero4;
-        if (r < seq) {
-            kv = *reinterpret_cast<const uint4*>(base + r * row3 + f + c * 8);
-            vv = *reinterpret_cast<const uint4*>(base + r * row3 + 2 * f + c * 8);
+    // AM_K keys with no data-dependent branches; the softmax masks keys >= seq.  A thread takes
+    // two adjacent keys, so each V^T word it writes holds both (keys 2p, 2p + 1 of one dim).
+    unsigned* svt32 = reinterpret_cast<unsigned*>(svt);
+    for (int i = threadIdx.x; i < AM_K / 2 * 8; i += 256) {
+        const int kp = i >> 3, c = i & 7, r0 = 2 * kp;
+        uint4 k0 = zero4, k1 = zero4, v0 = zero4, v1 = zero4;
+        if (r0 < seq) {
+            k0 = *reinterpret_cast<const uint4*>(base + r0 * row3 + f + c * 8);
+            v0 = *reinterpret_cast<const uint4*>(base + r0 * row3 + 2 * f + c * 8);
         }
-        *reinterpret_cast<uint4*>(&sk[r * AM_LD + c * 8]) = kv;
-        const unsigned w[4] = {vv.x, vv.y, vv.z, vv.w};
+        if (r0 + 1 < seq) {
+            k1 = *reinterpret_cast<const uint4*>(base + (r0 + 1) * row3 + f + c * 8);
+            v1 = *reinterpret_cast<const uint4*>(base + (r0 + 1) * row3 + 2 * f + c * 8);
+        }
+        *reinterpret_cast<uint4*>(&sk[r0 * AM_LD + c * 8]) = k0;
+        *reinterpret_cast<uint4*>(&sk[(r0 + 1) * AM_LD + c * 8]) = k1;
+        const unsigned a[4] = {v0.x, v0.y, v0.z, v0.w}, b[4] = {v1.x, v1.y, v1.z, v1.w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            svt16[(c * 8 + 2 * e) * AM_LP + r] = static_cast<unsigned short>(w[e] & 0xffffu);
-            svt16[(c * 8 + 2 * e + 1) * AM_LP + r] = static_cast<unsigned short>(w[e] >> 16);
+            svt32[((c * 8 + 2 * e) * AM_LP) / 2 + kp] = (a[e] & 0xffffu) | (b[e] << 16);
+            svt32[((c * 8 + 2 * e + 1) * AM_LP) / 2 + kp] = (a[e] >> 16) | (b[e] & 0xffff0000u);
         }
     }
     __syncthreads();
