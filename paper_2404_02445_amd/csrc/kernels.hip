@@ -18,10 +18,30 @@ __device__ __forceinline__ float to_f(float v) { return v; }
 
 template <typename T> __device__ __forceinline__ T from_f(float v) { return static_cast<T>(v); }
 
+// Sum over the wave, the same value in every lane: within each row of 16 lanes a butterfly of
+// DPP moves (partners 1 and 2 apart, then the mirrored half, then the mirrored row: each step
+// adds a lane's partial to its partner's, so all lanes of a row agree), then the four row sums
+// are read out and added in row order.
+__device__ __forceinline__ float dpp_add(float v, int ctrl_sel) {
+    int m = 0;
+    switch (ctrl_sel) {   // DPP controls must be compile-time constants
+        case 0: m = __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false); break;   // quad [1,0,3,2]
+        case 1: m = __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false); break;   // quad [2,3,0,1]
+        case 2: m = __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false); break;  // row half mirror
+        default: m = __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false); break; // row mirror
+    }
+    return v + __int_as_float(m);
+}
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
+    v = dpp_add(v, 0);
+    v = dpp_add(v, 1);
+    v = dpp_add(v, 2);
+    v = dpp_add(v, 3);
+    const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+    return (r0 + r1) + (r2 + r3);
 }
 
 static inline unsigned blocks_for(int64_t n, int per_block) {
