@@ -859,18 +859,19 @@ __global__ void splitk_reduce_kernel(const GemmParams p) {
 // ---------------------------------------------------------------------------
 // 3x3 convolutions (stride 1, padding 1) over 64- or 128-channel bf16 images,
 // patch-staged.  The implicit GEMM above fetches every input pixel once per
-// tap (nine times); here a block owns an 8 x 8 tile of output pixels of one
-// image and BN output channels of one sub-slice, and for each 64-channel chunk
-// it stages the 10 x 10 input patch around its tile (one pixel of halo each
-// way, zeros outside the image) once, with the nine taps' weight rows, then
-// forms all nine taps' A fragments from that patch in LDS (about a sixth of the
-// A bytes; the win is largest on narrow sub-slices, whose A traffic dominates).  Loads use the same
-// whole-line, XOR-swizzled layout as above (patch pixels and weight rows in
-// place of tile rows).  The k order is chunk, then tap, then the two 32-wide
-// steps; it depends only on the op, not on BN or the sub-slice, so sub-sliced
-// and unsplit launches agree bit for bit.  Four waves each take two tile rows
-// (16 pixels) by BN columns; the accumulators start at the bias and the
-// epilogue stores from the MFMA layout (residual, activation).
+// tap (nine times); here a block owns a TH x 8 tile of output pixels of one
+// image (8 x 8 in use) and BN output channels of one sub-slice, and for each
+// 64-channel chunk it stages the (TH + 2) x 10 input patch around its tile (one
+// pixel of halo each way, zeros outside the image) once, with the nine taps'
+// weight rows, then forms all nine taps' A fragments from that patch in LDS
+// (about a sixth of the A bytes; the win is largest on narrow sub-slices, whose
+// A traffic dominates).  Loads use the same whole-line, XOR-swizzled layout as
+// above (patch pixels and weight rows in place of tile rows).  The k order is
+// chunk, then tap, then the two 32-wide steps; it depends only on the op, not
+// on BN, TH or the sub-slice, so sub-sliced and unsplit launches agree bit for
+// bit.  TH / 2 waves each take two tile rows (16 pixels) by BN columns; the
+// accumulators start at the bias and the epilogue stores from the MFMA layout
+// (residual, activation).
 // ---------------------------------------------------------------------------
 constexpr int HTW = 8;                       // output tile width; its height TH is a parameter
 
