@@ -93,11 +93,15 @@ __device__ __forceinline__ float ld_f(const __bf16* p, int64_t i) {
 }
 __device__ __forceinline__ float ld_f(const float* p, int64_t i) { return p[i]; }
 
-// four consecutive elements (vector load when aligned)
+// whether q is aligned to a whole vector of four elements (8 bytes for bf16, 16 for float)
+template <typename T>
+__device__ __forceinline__ bool aligned4(const T* q) { return (reinterpret_cast<uintptr_t>(q) & (4 * sizeof(T) - 1)) == 0; }
+
+// four consecutive elements (vector load when the address is aligned)
 template <typename T>
 __device__ __forceinline__ void ld4(const T* p, int64_t i, int nvalid, float* v) {
     if constexpr (sizeof(T) == 2) {
-        if (nvalid == 4 && (i & 3) == 0) {
+        if (nvalid == 4 && aligned4(p + i)) {
             const uint2 r = *reinterpret_cast<const uint2*>(p + i);
             v[0] = __uint_as_float(r.x << 16);
             v[1] = __uint_as_float(r.x & 0xffff0000u);
@@ -106,7 +110,7 @@ __device__ __forceinline__ void ld4(const T* p, int64_t i, int nvalid, float* v)
             return;
         }
     } else {
-        if (nvalid == 4 && (i & 3) == 0) {
+        if (nvalid == 4 && aligned4(p + i)) {
             const f32x4 r = *reinterpret_cast<const f32x4*>(p + i);
             v[0] = r[0], v[1] = r[1], v[2] = r[2], v[3] = r[3];
             return;
@@ -123,16 +127,18 @@ __device__ __forceinline__ float act_f(float v, int act) {
     return v;
 }
 
+// four consecutive elements to c + idx (vector store when the address is aligned: a branch
+// written into a concatenated tensor may start at any channel)
 template <typename T>
 __device__ __forceinline__ void store4(T* c, int64_t idx, const float* v, int nvalid) {
     if constexpr (sizeof(T) == 2) {
-        if (nvalid == 4 && (idx & 3) == 0) {
+        if (nvalid == 4 && aligned4(c + idx)) {
             const bf16x4 o = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
             *reinterpret_cast<bf16x4*>(c + idx) = o;
             return;
         }
     } else {
-        if (nvalid == 4 && (idx & 3) == 0) {
+        if (nvalid == 4 && aligned4(c + idx)) {
             *reinterpret_cast<f32x4*>(c + idx) = f32x4{v[0], v[1], v[2], v[3]};
             return;
         }

@@ -96,6 +96,38 @@ def test_conv_parity_and_subslice_bitwise(case):
         assert torch.equal(yk, y1), f"k={ks} differs from the unsplit kernel"
 
 
+def concat_model(dtype, n, hw, seed=6):
+    """A stem conv to 64 channels, then one parallel node whose three branches write side by
+    side into an 80-channel tensor at channel offsets 0, 13 and 64: a 1x1 conv (13 outputs),
+    the RD 3x3 conv (51 outputs, stride 1, padding 1, 64 input channels -- the patch-staged
+    kernel in bf16) and a 1x1 conv (16 outputs).  Offset 13 leaves the 3x3 branch's rows
+    unaligned to a vector of four elements.  A 1x1 head conv reads the concatenation."""
+    b = synth._Builder("concat", dtype, n, seed)
+    x = b.tensor((n, 3, hw, hw), "f32")
+    b.new_layer("stem")
+    x = b.conv(x, 64, 3, 1, 1, "relu", "stem", bn_fold=True)
+    b.new_layer("cat")
+    out = b.tensor((n, 80, hw, hw))
+    b.conv(x, 13, 1, 1, 0, "relu", "b1", bn_fold=True, branch=1, pos=1, into=(out, 0))
+    b.conv(x, 51, 3, 1, 1, "relu", "b2", bn_fold=True, branch=2, pos=1, rd=True, into=(out, 13))
+    b.conv(x, 16, 1, 1, 0, "none", "b3", bn_fold=True, branch=3, pos=1, into=(out, 64))
+    b.new_layer("head")
+    y = b.conv(out, 24, 1, 1, 0, "none", "head", bn_fold=True)
+    return b.finish(y, n_slices=1, k_by_layer={})
+
+
+@pytest.mark.parametrize("dt,n,hw", [("bf16", 2, 18), ("bf16", 1, 16), ("f32", 2, 9)])
+def test_concat_at_unaligned_channel_offsets(dt, n, hw):
+    m = concat_model(dt, n, hw)
+    x = synth.random_tensor((n, 3, hw, hw), "f32", seed=12)
+    ref = oracle.forward(m, x)
+    y1, _, _ = run_gpu(m, x, P.make_plan(3, [2], [1, 1, 1]))
+    assert rel_err(_np(y1), ref) <= TOL[dt]
+    for ks in (2, 3, 4):
+        yk, _, _ = run_gpu(m, x, P.make_plan(3, [2], [1, ks, 1]))
+        assert torch.equal(yk, y1), f"k={ks} differs from the unsplit kernel"
+
+
 def seq_input_model(dtype, b, s, f, seed=3, scale=1.0):
     """Model whose first op produces an arbitrary [B,S,F] activation: an embedding of ids
     0..B*S-1 into a table of random rows."""
