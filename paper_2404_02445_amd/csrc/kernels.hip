@@ -175,6 +175,8 @@ static void maxpool_launch(const void* x, void* y, int n, int h, int w, int c, i
 hipError_t launch_maxpool(const void* x, void* y, int n, int h, int w, int c, int k, int stride, int pad, int ho,
                           int wo, int dtype, hipStream_t s) {
     if (static_cast<int64_t>(n) * h * w * c >= (int64_t(1) << 31)) return hipErrorInvalidValue;
+    // the kernel moves whole 16-byte channel groups: a channel count off the granule is refused
+    if (c % (dtype == MOPAR_BF16 ? 8 : 4) != 0) return hipErrorInvalidValue;
     if (dtype == MOPAR_BF16)
         maxpool_launch<__bf16>(x, y, n, h, w, c, k, stride, pad, ho, wo, s);
     else
