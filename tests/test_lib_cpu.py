@@ -284,3 +284,61 @@ def test_concatenating_writers_validated():
     bad[first].out_off = 0
     bad[first].n_out += 8                         # writes past the next branch's channels
     assert create(bad) != 0
+
+
+def _create_error(build):
+    """Status of model creation for the model `build` makes (None when accepted)."""
+    b = synth._Builder("v", "bf16", 2, 9)
+    y = build(b)
+    m = b.finish(y, n_slices=1, k_by_layer={})
+    try:
+        P.SlicedModel(m, device="cpu")
+    except P.MoparError as e:
+        return e.status
+    return None
+
+
+def test_model_create_checks_what_the_kernels_assume():
+    def stem(b, c):
+        x = b.tensor((2, 3, 12, 12), "f32")
+        b.new_layer("stem")
+        return b.conv(x, c, 3, 1, 1, "relu", "stem", bn_fold=True)
+
+    def pool(c):
+        def f(b):
+            x = stem(b, c)
+            b.new_layer("pool")
+            return b.maxpool(x, 3, 2, 1, "pool")
+        return f
+
+    def conv_after(c):
+        def f(b):
+            x = stem(b, c)
+            b.new_layer("c1")
+            return b.conv(x, 16, 3, 1, 1, "relu", "c1", bn_fold=True)
+        return f
+
+    def concat(offsets, head=True):
+        def f(b):
+            x = stem(b, 16)
+            b.new_layer("cat")
+            out = b.tensor((2, 32, 12, 12))
+            for i, (c, off) in enumerate(offsets):
+                b.conv(x, c, 1, 1, 0, "relu", f"b{i}", bn_fold=True, branch=i + 1, pos=1, into=(out, off))
+            if not head:
+                return out
+            b.new_layer("head")
+            return b.conv(out, 8, 1, 1, 0, "none", "head", bn_fold=True)
+        return f
+
+    # 16-byte channel groups (8 bf16): pools and conv inputs off the granule are refused
+    assert _create_error(pool(16)) is None
+    assert _create_error(pool(12)) == L.MOPAR_E_UNSUPPORTED
+    assert _create_error(conv_after(24)) is None
+    assert _create_error(conv_after(20)) == L.MOPAR_E_UNSUPPORTED
+    # concatenation writers: any offset, but in channel order and covering every channel
+    assert _create_error(concat([(13, 0), (19, 13)])) is None
+    assert _create_error(concat([(19, 13), (13, 0)])) == L.MOPAR_E_ARG
+    assert _create_error(concat([(13, 0), (16, 16)])) == L.MOPAR_E_ARG
+    # the output must come from the last op, not from a concatenation's first writer
+    assert _create_error(concat([(13, 0), (19, 13)], head=False)) == L.MOPAR_E_ARG
