@@ -398,6 +398,7 @@ static void layernorm_launch(const void* x, const void* res, const void* g, cons
 
 hipError_t launch_layernorm(const void* x, const void* res, const void* g, const void* b, void* y, int64_t rows,
                             int f, float eps, int dtype, hipStream_t s) {
+    if (f < 1 || f > 64 * LN_MAXV) return hipErrorInvalidValue;   // a row lives in one wave's registers
     if (dtype == MOPAR_BF16)
         layernorm_launch<__bf16>(x, res, g, b, y, rows, f, eps, s);
     else
@@ -448,7 +449,7 @@ hipError_t launch_embed_bert(const int32_t* ids, const void* tok, const void* po
                              const void* b, void* y, int batch, int seq, int vocab, int f, float eps, int dtype,
                              hipStream_t s) {
     const int64_t rows = static_cast<int64_t>(batch) * seq;
-    if (vocab < 1) return hipErrorInvalidValue;
+    if (vocab < 1 || f < 1 || f > 64 * LN_MAXV) return hipErrorInvalidValue;
     if (dtype == MOPAR_BF16)
         embed_bert_launch<__bf16>(ids, tok, pos, type, g, b, y, rows, seq, vocab, f, eps, s);
     else
