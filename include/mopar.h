@@ -17,7 +17,9 @@
  *            buffers and the workspace are device pointers the caller
  *            allocated; descriptors and plans are host memory the caller
  *            owns.  The library never allocates device memory, never frees
- *            caller memory and never synchronises the host.
+ *            caller memory and never synchronises the host -- except
+ *            mopar_model_measure and mopar_model_op_times, which wait for
+ *            their timing events, as documented there.
  * Streams.   `stream` is a hipStream_t passed as void* (NULL = the default
  *            stream).  Work is enqueued asynchronously in call order.
  * Alignment. Device pointers must be 16-byte aligned.
@@ -202,9 +204,16 @@ typedef struct {
 
 typedef struct mopar_model_s* mopar_model_t;
 
-/* Validate the description and build host metadata (op dispatch, workspace
- * layout).  `weights_dev` (device) must stay valid for the model's life;
- * `weights_bytes` bounds every weight offset.  No device calls. */
+/* Validate the description and build host metadata: the graph G = <V, E> of
+ * operators grouped into planning nodes (layers) with single-input topology,
+ * each node's ops in the chain / parallel-branch structure that Eq. 1-3
+ * aggregate, the resource-dominant ops that the hybrid strategy pi_P may split
+ * (Sec. III-B service profile, Sec. III-C problem statement), and the
+ * workspace layout.  `weights_dev` (device) must stay valid for the model's
+ * life; `weights_bytes` bounds every weight offset.  No device calls.
+ * Errors: MOPAR_E_ARG (null pointers, bad ids or offsets, a graph the planner
+ * cannot chain), MOPAR_E_SHAPE, MOPAR_E_DTYPE, MOPAR_E_UNSUPPORTED (a valid
+ * model outside what the kernels implement); *out is NULL then. */
 int mopar_model_create(const mopar_model_desc* desc, const void* weights_dev, size_t weights_bytes,
                        mopar_model_t* out);
 void mopar_model_destroy(mopar_model_t model);
@@ -226,16 +235,26 @@ int mopar_model_profile(mopar_model_t model, mopar_layer_profile* out);
 int mopar_model_profile_dominant(mopar_model_t model, double frac, mopar_layer_profile* out);
 
 /* Bytes of device workspace mopar_slice_forward / mopar_model_forward need
- * under `plan` (activations inside slices, boundary tensors, scratch). */
+ * under `plan`: the tensors that live inside slices, the boundary tensors
+ * before encode and after decode (the hand-off of Sec. III-D goes through the
+ * caller's code buffers, not this workspace) and op scratch (split-K partial
+ * sums, the LSTM gate pre-activations and cell state).  The caller allocates it
+ * (Memory convention); one workspace serves one forward at a time.  Errors:
+ * MOPAR_E_ARG (null pointers, a plan for another model or with an invalid k). */
 int mopar_model_workspace_bytes(mopar_model_t model, const mopar_plan* plan, size_t* bytes);
 
-/* Run slice s of `plan`: the layers after the previous cut up to
- * slice_end[s].  `in_dev` holds the slice input (the model input for s = 0,
- * otherwise the output of node slice_end[s-1], in its physical layout);
- * `out_dev` receives the output of node slice_end[s].  Any other tensor
- * crossing the cut before slice s (a skip edge, see mopar_model_cut_tensors)
- * is read from its slot in `ws`, where the earlier slices, run with the same
- * workspace, left it.  RD ops of node l run as k[l] sub-slices of one launch. */
+/* Run slice s of `plan`: one slice of the vertical partition pi_S (Sec.
+ * III-C; the paper deploys each slice as its own function), i.e. the layers
+ * after the previous split point up to slice_end[s].  `in_dev` holds the slice
+ * input (the model input for s = 0, otherwise the output of node
+ * slice_end[s-1], in its physical layout); `out_dev` receives the output of
+ * node slice_end[s].  Any other tensor crossing the cut before slice s (a skip
+ * edge, see mopar_model_cut_tensors) is read from its slot in `ws`, where the
+ * earlier slices, run with the same workspace, left it.  RD ops of node l run
+ * as the k[l] equal-size sub-slices of pi_P, all in one launch, each writing
+ * its own output columns (the aggregation t_a of Eq. 5 costs nothing).
+ * Errors: MOPAR_E_ARG (bad plan, s out of range, null pointers),
+ * MOPAR_E_WORKSPACE (ws smaller than mopar_model_workspace_bytes), MOPAR_E_HIP. */
 int mopar_slice_forward(mopar_model_t model, const mopar_plan* plan, int32_t s, const void* in_dev,
                         void* out_dev, void* ws, size_t ws_bytes, void* stream);
 
@@ -332,9 +351,13 @@ int mopar_pipeline_create(mopar_model_t model, const mopar_plan* plan, const mop
                           int32_t depth, void* const* streams, void* ws, size_t ws_bytes, void* const* code_bufs,
                           mopar_pipeline_t* out);
 
-/* Enqueue one batch: read `in_dev` (the model input), write `out_dev`.  Both
- * must stay untouched by the caller until the last slice's stream has
- * finished this batch (e.g. synchronise that stream).  Never blocks. */
+/* Enqueue one batch: read `in_dev` (the model input), write `out_dev`.  The
+ * batch runs on the pipeline's own streams and does not wait for any other
+ * stream: `in_dev` must already hold the input when the first slice's stream
+ * reaches this batch (e.g. make that stream wait for an event recorded after
+ * the input was written).  Both buffers must stay untouched by the caller
+ * until the last slice's stream has finished this batch (e.g. synchronise
+ * that stream).  Never blocks. */
 int mopar_pipeline_submit(mopar_pipeline_t pipe, const void* in_dev, void* out_dev);
 
 /* Graph replay (HIP graphs; off by default).  With `enable` set, each later

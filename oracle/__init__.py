@@ -217,15 +217,17 @@ def _ae(x, w, b, rnd):
 # Operators, sub-slicing and the sliced model forward
 # ---------------------------------------------------------------------------
 
-def run_op(model, op, env, w_rows=None):
+def run_op(model, op, env, w_rows=None, rnd=None):
     """Evaluate one op of ``model`` (a ``synth.Model``) on tensors in ``env``.
 
     ``w_rows = (lo, hi)`` restricts the op to output channels / features
     lo..hi-1 using only those rows of its weight and bias: one horizontal
     sub-slice holding its share of the parameters (Sec. III-C, pi_P).
+    ``rnd``: storage rounding of the op's output ('none' keeps every value in
+    double); None rounds to the model dtype, as the library stores it.
     """
     W = model.weights
-    rnd = model.dtype
+    rnd = model.dtype if rnd is None else rnd
     k = op["kind"]
     ins = [env[t] for t in op["inputs"]]
     lo, hi = w_rows if w_rows is not None else (None, None)
@@ -269,16 +271,16 @@ def out_width(model, op):
     return op["cout"] if op["kind"] == "conv" else op["nout"]
 
 
-def run_op_sliced(model, op, env, k):
+def run_op_sliced(model, op, env, k, rnd=None):
     """The k-way sub-sliced operator: sub-slice j computes its own output range with its own
     rows of the parameters; the k partial outputs are concatenated (the aggregation of Eq. 5)."""
     n = out_width(model, op)
-    parts = [run_op(model, op, env, subslice_range(n, k, j)) for j in range(k)]
+    parts = [run_op(model, op, env, subslice_range(n, k, j), rnd) for j in range(k)]
     axis = 1 if parts[0].ndim == 4 else -1
     return np.concatenate(parts, axis=axis)
 
 
-def forward(model, x, k=None, cuts=(), codecs=None, sample=None, keep=False):
+def forward(model, x, k=None, cuts=(), codecs=None, sample=None, keep=False, rnd=None):
     """Sliced forward pass of ``model`` on input ``x`` (canonical layout).
 
     k       -- per planning node, the sub-slice count of its RD ops (None: all 1)
@@ -287,6 +289,9 @@ def forward(model, x, k=None, cuts=(), codecs=None, sample=None, keep=False):
     sample  -- optional batch indices; every op is independent across the batch,
                so the result is exactly those rows of the full-batch result
     keep    -- also return every tensor, every code and every boundary tensor before encoding
+    rnd     -- storage rounding of every stored tensor: None (the model dtype, as the library
+               stores them) or 'none' (exact double arithmetic throughout, for pinning the
+               op dispatch against library routines without rounding noise)
 
     The boundary tensor of a cut is encoded at the end of the slice and
     decoded at the start of the next (Sec. III-D); raw hand-off returns the
@@ -294,11 +299,12 @@ def forward(model, x, k=None, cuts=(), codecs=None, sample=None, keep=False):
     """
     if sample is not None:
         x = x[np.asarray(sample)]
+    rnd = model.dtype if rnd is None else rnd
     t_in = model.tensors[model.input_tid]
     if t_in["dtype"] == "i32":
         env = {model.input_tid: np.ascontiguousarray(x, dtype=np.int32)}
     else:
-        env = {model.input_tid: round_to(x, model.dtype)}
+        env = {model.input_tid: round_to(x, rnd)}
     cuts = list(cuts)
     if codecs is None:
         codecs = [None] * sum(len(crossing_tensors(model, c)) for c in cuts)
@@ -307,9 +313,9 @@ def forward(model, x, k=None, cuts=(), codecs=None, sample=None, keep=False):
         for op in [o for o in model.ops if o["layer"] == li]:
             kk = 1 if k is None else int(k[li])
             if op.get("rd") and kk > 1:
-                res = run_op_sliced(model, op, env, kk)
+                res = run_op_sliced(model, op, env, kk, rnd)
             else:
-                res = run_op(model, op, env)
+                res = run_op(model, op, env, None, rnd)
             if "out_off" in op:
                 # a branch of a parallel node: its channels of the concatenated node output
                 full = env.get(op["out"])
@@ -330,8 +336,8 @@ def forward(model, x, k=None, cuts=(), codecs=None, sample=None, keep=False):
                     code = env[tid].copy()
                     env[tid] = code.copy()
                 else:
-                    code = ae_encode(env[tid], cd["w_enc"], cd["b_enc"], model.dtype)
-                    env[tid] = ae_decode(code, cd["w_dec"], cd["b_dec"], model.dtype)
+                    code = ae_encode(env[tid], cd["w_enc"], cd["b_enc"], rnd)
+                    env[tid] = ae_decode(code, cd["w_dec"], cd["b_dec"], rnd)
                 codes[(li, tid)] = code
                 if tid == model.layer_output_tid(li):
                     bounds[li], codes[li] = bounds[(li, tid)], code

@@ -421,6 +421,8 @@ class SlicePipeline:
 
     def __init__(self, sm, plan, codec, codec_weights, depth, replicas=1, stream_per_slice=True):
         self.sm, self.plan = sm, plan
+        self.replicas = replicas
+        self._submitted = 0
         S = plan.n_slices
         self.streams = []
         for _ in range(replicas):
@@ -445,7 +447,18 @@ class SlicePipeline:
         self.handle = h
 
     def submit(self, x, out):
+        """Enqueue one batch.  Batch i runs on instance i mod replicas (the library's rule):
+        that instance's first stream waits for the work torch's current stream has queued so
+        far (which produced ``x``), and both tensors are marked in use by the instance's streams
+        so the caching allocator does not hand their memory out before the batch has run."""
+        rep = self._submitted % self.replicas
+        S = self.plan.n_slices
+        first, last = self.streams[rep * S], self.streams[rep * S + S - 1]
+        first.wait_stream(torch.cuda.current_stream(first.device))
         check(lib().mopar_pipeline_submit(self.handle, _ptr(x), _ptr(out)))
+        self._submitted += 1
+        x.record_stream(first)
+        out.record_stream(last)
         return out
 
     def use_graphs(self, enable=True):

@@ -1152,7 +1152,9 @@ hipError_t launch_gemm(const GemmParams& params, int dtype, hipStream_t stream) 
     if (a_bytes >= (int64_t(1) << 31) || b_bytes >= (int64_t(1) << 31)) return hipErrorInvalidValue;
     p.a_bytes = static_cast<uint32_t>(a_bytes);
     p.b_bytes = static_cast<uint32_t>(b_bytes);
-    if (p.splits < 1 || (p.splits > 1 && (!p.partial || p.epi != EPI_STD))) return hipErrorInvalidValue;
+    // the reduce keeps every split's partial in flight at once, for at most 16 splits
+    if (p.splits < 1 || p.splits > 16 || (p.splits > 1 && (!p.partial || p.epi != EPI_STD)))
+        return hipErrorInvalidValue;
     if (p.conv && conv_halo_ok(dtype, p.kh, p.kw, p.stride, p.pad, p.cs, p.N, p.out_h, p.out_w)) {
         if (p.splits != 1 || p.epi != EPI_STD) return hipErrorInvalidValue;
         // 16-column tiles at every width (measured at least as fast as 32 on 32-wide sub-slices)

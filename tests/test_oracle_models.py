@@ -19,6 +19,8 @@ import synth
 
 
 def _round(t, dtype):
+    if dtype == "none":
+        return t
     if dtype == "bf16":
         return t.to(torch.bfloat16).double()
     if dtype == "f32":
@@ -26,9 +28,11 @@ def _round(t, dtype):
     return t
 
 
-def torch_forward(m, x):
+def torch_forward(m, x, rnd=None):
+    """The model evaluated with torch library routines in float64; every stored tensor rounded
+    to ``rnd`` (None: the model dtype; 'none': no rounding, the LSTM cell state included)."""
     W = {k: torch.from_numpy(v.astype(np.float64)) for k, v in m.weights.items()}
-    dt = m.dtype
+    dt = m.dtype if rnd is None else rnd
     if m.tensors[m.input_tid]["dtype"] == "i32":
         env = {m.input_tid: torch.from_numpy(x.astype(np.int64))}
     else:
@@ -83,7 +87,7 @@ def torch_forward(m, x):
             for s in range(t):
                 g = F.linear(xx[:, s], W[op["w_ih"]], W[op["b_ih"]]) + F.linear(h, W[op["w_hh"]], W[op["b_hh"]])
                 i, f, gg, o = g.split(hd, dim=1)
-                c = _round(torch.sigmoid(f) * c + torch.sigmoid(i) * torch.tanh(gg), "f32")
+                c = _round(torch.sigmoid(f) * c + torch.sigmoid(i) * torch.tanh(gg), "none" if dt == "none" else "f32")
                 h = _round(torch.sigmoid(o) * torch.tanh(c), dt)
                 outs.append(h)
             y = torch.stack(outs, 1)
@@ -121,6 +125,19 @@ def test_oracle_model_matches_torch_library_forward(cfg):
     assert np.abs(y - ref).max() <= tol * scale
 
 
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6, 7])
+def test_oracle_model_matches_torch_library_forward_unrounded(cfg):
+    """Without storage rounding both evaluators compute the same real-valued function in double,
+    so they agree to double-precision summation-order noise: any op-dispatch mistake in the oracle
+    (a weight in the wrong place, a missing residual, a wrong flatten order) shows up far above
+    1e-12, which the bf16-rounded comparison above, held to bf16 noise, cannot resolve."""
+    m = synth.build(cfg, **SMALL[cfg])
+    x = synth.make_input(m)
+    y = oracle.forward(m, x, rnd="none")
+    ref = torch_forward(m, x, rnd="none")
+    assert np.abs(y - ref).max() <= 1e-12 * np.abs(ref).max()
+
+
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
 def test_sample_rows_equal_full_batch(cfg):
     m = synth.build(cfg, **SMALL[cfg])
@@ -150,3 +167,37 @@ def test_codec_hand_off_changes_only_through_codec():
         np.testing.assert_array_equal(env[m.layer_output_tid(li)],
                                       oracle.ae_decode(code, c["w_dec"], c["b_dec"], "bf16"))
     assert math.isfinite(float(np.abs(y).max()))
+
+
+def _planted(monkeypatch, name):
+    """Plant one plausible mistake in the oracle's op dispatch (CPU only, undone after the test)."""
+    real = oracle.run_op
+
+    def wrong(model, op, env, w_rows=None, rnd=None):
+        k = op["kind"]
+        if name == "linear_residual_dropped" and k == "linear" and len(op["inputs"]) > 1:
+            op = dict(op, inputs=op["inputs"][:1])
+        elif name == "attention_scale_over_hidden" and k == "attention":
+            op = dict(op, scale=op["scale"] / np.sqrt(op["heads"]))     # 1/sqrt(F) in place of 1/sqrt(d)
+        elif name == "lstm_gates_swapped" and k == "lstm":
+            W = dict(model.weights)
+            h = op["hidden"]
+            for key in ("w_ih", "w_hh", "b_ih", "b_hh"):
+                a = W[op[key]]
+                W[op[key]] = np.concatenate([a[h:2 * h], a[:h], a[2 * h:]])   # i <-> f
+            model = type(model)(**{**model.__dict__, "weights": W})
+        elif name == "conv_residual_dropped" and k == "conv" and len(op["inputs"]) > 1:
+            op = dict(op, inputs=op["inputs"][:1])
+        return real(model, op, env, w_rows, rnd)
+    monkeypatch.setattr(oracle, "run_op", wrong)
+
+
+@pytest.mark.parametrize("cfg,mistake", [(4, "linear_residual_dropped"), (4, "attention_scale_over_hidden"),
+                                         (5, "lstm_gates_swapped"), (2, "conv_residual_dropped")])
+def test_unrounded_pin_catches_planted_mistakes(monkeypatch, cfg, mistake):
+    m = synth.build(cfg, **SMALL[cfg])
+    x = synth.make_input(m)
+    ref = torch_forward(m, x, rnd="none")
+    _planted(monkeypatch, mistake)
+    y = oracle.forward(m, x, rnd="none")
+    assert np.abs(y - ref).max() > 1e-9 * np.abs(ref).max()
