@@ -270,7 +270,10 @@ typedef enum { MOPAR_CODEC_RAW = 0, MOPAR_CODEC_AE = 1 } mopar_codec_kind;
  *      y[p][c] = b_dec[c] + sum_e w_dec[c][e] code[p][e], stored in the
  *      tensor's dtype; R = c / c_code.  Weights are device pointers in the
  *      tensor dtype: w_enc [c_code][c], b_enc [c_code], w_dec [c][c_code],
- *      b_dec [c].  c and c_code must be multiples of 8 (bf16) or 4 (f32). */
+ *      b_dec [c].  Any c, c_code >= 1: a layer whose input width (c for the
+ *      encoder, c_code for the decoder) is a multiple of 8 (bf16) or 4 (f32)
+ *      runs on the matrix cores, any other on the vector ALUs (such layers are
+ *      a few channels wide).  positions * max(c, c_code) < 2^31. */
 typedef struct {
     int32_t kind;
     int32_t c, c_code;

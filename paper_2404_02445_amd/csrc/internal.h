@@ -162,6 +162,10 @@ hipError_t launch_embed(const int32_t* ids, const void* table, void* y, int64_t 
 hipError_t launch_attention(const void* qkv, void* y, int batch, int seq, int heads, float scale, int dtype,
                             hipStream_t s);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+// One codec layer y[p][o] = b[o] + sum_c w[o][c] x[p][c] on the vector ALUs, for input widths off
+// the GEMM's 16-byte granule; positions * cout < 2^31.
+hipError_t launch_codec_narrow(const void* x, const void* w, const void* b, void* y, int64_t positions, int cin,
+                               int cout, int dtype, hipStream_t s);
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s);
 
 size_t dtype_size(int dtype);

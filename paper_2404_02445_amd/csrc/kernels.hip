@@ -744,6 +744,45 @@ hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// One autoencoder codec layer whose input width is not a whole number of 16-byte
+// chunks (the matrix-core GEMM streams 16-byte chunks of every row, so it needs
+// that width on the granule): y[p][o] = b[o] + sum_c w[o][c] x[p][c], one thread
+// per (position, output channel), the sum over c in ascending order in float32.
+// Such layers are tiny (a few channels per position), so the vector ALUs serve.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void codec_narrow_kernel(const T* __restrict__ x, const T* __restrict__ w,
+                                                           const T* __restrict__ b, T* __restrict__ y,
+                                                           unsigned total, int cin, int cout) {
+    const unsigned i = blockIdx.x * 256u + threadIdx.x;
+    if (i >= total) return;
+    const unsigned p = i / static_cast<unsigned>(cout);
+    const int o = static_cast<int>(i - p * static_cast<unsigned>(cout));
+    const T* xr = x + static_cast<int64_t>(p) * cin;
+    const T* wr = w + static_cast<int64_t>(o) * cin;
+    float acc = b ? to_f(b[o]) : 0.0f;
+    for (int c = 0; c < cin; ++c) acc += to_f(wr[c]) * to_f(xr[c]);
+    y[i] = from_f<T>(acc);
+}
+
+hipError_t launch_codec_narrow(const void* x, const void* w, const void* b, void* y, int64_t positions, int cin,
+                               int cout, int dtype, hipStream_t s) {
+    const int64_t total = positions * cout;
+    if (total <= 0) return hipSuccess;
+    if (total >= (int64_t(1) << 31)) return hipErrorInvalidValue;   // 32-bit thread index
+    const dim3 grid(blocks_for(total, 256));
+    if (dtype == MOPAR_BF16)
+        launch_kernel(codec_narrow_kernel<__bf16>, grid, dim3(256), 0, s, static_cast<const __bf16*>(x),
+                      static_cast<const __bf16*>(w), static_cast<const __bf16*>(b), static_cast<__bf16*>(y),
+                      static_cast<unsigned>(total), cin, cout);
+    else
+        launch_kernel(codec_narrow_kernel<float>, grid, dim3(256), 0, s, static_cast<const float*>(x),
+                      static_cast<const float*>(w), static_cast<const float*>(b), static_cast<float*>(y),
+                      static_cast<unsigned>(total), cin, cout);
+    return hipGetLastError();
+}
+
 size_t dtype_size(int dtype) { return dtype == MOPAR_BF16 ? 2 : 4; }
 
 }  // namespace mopar

@@ -877,10 +877,7 @@ static int codec_geometry(const mopar_codec* c, const mopar_tensor_desc* x, int6
     if (c->kind == MOPAR_CODEC_RAW) return MOPAR_OK;
     if (c->kind != MOPAR_CODEC_AE) return set_error(MOPAR_E_ARG, std::string(who) + ": codec kind");
     if (c->c != ch) return set_error(MOPAR_E_SHAPE, std::string(who) + ": codec channels differ from the tensor's");
-    const int g = x->dtype == MOPAR_BF16 ? 8 : 4;   // 16-byte granule of the GEMM loads
-    if (c->c_code < 1 || c->c % g != 0 || c->c_code % g != 0)
-        return set_error(MOPAR_E_UNSUPPORTED, std::string(who) + ": c and c_code must be multiples of " +
-                                                  std::to_string(g));
+    if (c->c_code < 1) return set_error(MOPAR_E_ARG, std::string(who) + ": c_code must be >= 1");
     if (!c->w_enc || !c->w_dec) return set_error(MOPAR_E_ARG, std::string(who) + ": null codec weights");
     const int64_t es = elt_bytes(x->dtype);
     if (!gemm_operands_fit(*positions * std::max<int64_t>(ch, c->c_code) * es, int64_t(c->c_code) * ch * es))
@@ -902,6 +899,11 @@ int code_bytes_impl(const mopar_codec* c, const mopar_tensor_desc* x, size_t* by
 static hipError_t codec_apply(const mopar_codec& c, int dtype, int64_t pos, int ch, const void* src, void* dst,
                               bool encode, hipStream_t s) {
     if (c.kind == MOPAR_CODEC_RAW) return launch_copy(src, dst, static_cast<size_t>(pos * ch) * elt_bytes(dtype), s);
+    // the layer's input width must sit on the GEMM's 16-byte granule; otherwise the vector-ALU kernel
+    const int cin = encode ? c.c : c.c_code, cout = encode ? c.c_code : c.c;
+    if (cin % (dtype == MOPAR_BF16 ? 8 : 4) != 0)
+        return launch_codec_narrow(src, encode ? c.w_enc : c.w_dec, encode ? c.b_enc : c.b_dec, dst, pos, cin, cout,
+                                   dtype, s);
     GemmParams g{};
     g.A = src;
     g.lda = encode ? c.c : c.c_code;

@@ -5,7 +5,7 @@ import synth
 
 # Shrunken variants of the five workloads: every kernel path of the full-size
 # model, several tiles and a ragged tail, and a CPU oracle that finishes in
-# seconds.  Channel counts at the cuts keep C / 8 a multiple of the codec granule.
+# seconds.
 SMALL = {
     1: dict(hw=16),
     2: dict(batch=2, hw=64, blocks=(1, 2, 2, 1), widths=(16, 32, 32, 64), n_cls=37),
@@ -29,27 +29,24 @@ def rel_err(got, ref):
 TOL = {"f32": 1e-4, "bf16": 2e-2}
 
 
+def codec_ratio(c):
+    """Compression ratio of a boundary of C channels: R = 8, the smallest ratio the paper
+    studies, when it divides C (the code then has C / 8 channels), else the largest of 4 and
+    2 that does, else 1."""
+    return next((r for r in (8, 4, 2) if c % r == 0), 1)
+
+
 def codec_ratios(model, cuts):
-    """Compression ratio per cut: the largest R in 8, 4, 2, 1 that divides the boundary's
-    channel count C and leaves C / R a multiple of the 16-byte granule (8 bf16 / 4 fp32)."""
-    g = 8 if model.dtype == "bf16" else 4
-    out = []
-    for li in cuts:
-        c = synth.boundary_channels(model, li)
-        out.append(next((r for r in (8, 4, 2) if c % r == 0 and (c // r) % g == 0), 1))
-    return out
+    """Compression ratio per cut (the boundary tensor leaving each cut node)."""
+    return [codec_ratio(synth.boundary_channels(model, li)) for li in cuts]
 
 
 def boundary_codecs(model, cuts, kind="ae"):
     """Boundary tensors of the cuts (every tensor crossing each cut, cut-major, ascending id)
-    and AE codec weights for each, at the largest ratio the granule allows."""
+    and AE codec weights for each, at codec_ratio of its channel count."""
     import oracle
     tids = [t for c in cuts for t in oracle.crossing_tensors(model, c)]
-    g = 8 if model.dtype == "bf16" else 4
-    ratios = []
-    for t in tids:
-        c = synth.tensor_channels(model, t)
-        ratios.append(next((r for r in (8, 4, 2) if c % r == 0 and (c // r) % g == 0), 1))
+    ratios = [codec_ratio(synth.tensor_channels(model, t)) for t in tids]
     if kind != "ae" or not tids:
         return tids, None
     return tids, synth.make_codec_weights(model, cuts, ratio=ratios, tensors=tids)

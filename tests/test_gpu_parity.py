@@ -296,7 +296,11 @@ def test_codec_raw_roundtrip_bitwise(dt, shape):
 
 
 @pytest.mark.parametrize("dt,shape,ratio", [("bf16", (2, 256, 7, 9), 8), ("bf16", (3, 13, 768), 8),
-                                            ("bf16", (1, 1024, 3, 5), 8), ("f32", (2, 32, 5, 6), 4)])
+                                            ("bf16", (1, 1024, 3, 5), 8), ("f32", (2, 32, 5, 6), 4),
+                                            # code widths off the 16-byte granule (vector-ALU layers):
+                                            # the tiny VGG's 16-channel boundary at R = 8
+                                            ("f32", (1, 16, 16, 16), 8), ("bf16", (2, 9, 24), 8),
+                                            ("bf16", (1, 12, 5, 3), 4)])
 def test_codec_ae_parity(dt, shape, ratio):
     c = shape[1] if len(shape) == 4 else shape[-1]
     w = synth.random_codec_weights(c, c // ratio, dt, seed=7)

@@ -191,6 +191,14 @@ def test_codec_code_bytes_host_only():
     ae.c = 128
     with pytest.raises(P.MoparError):
         P.mopar_boundary_code_bytes(ae, (8, 256, 56, 56), "bf16")
+    # widths off the 16-byte granule run on the vector-ALU codec kernel: accepted
+    ae.c, ae.c_code = 16, 2
+    assert P.mopar_boundary_code_bytes(ae, (1, 16, 32, 32), "f32") == 32 * 32 * 2 * 4
+    ae.c, ae.c_code = 12, 3
+    assert P.mopar_boundary_code_bytes(ae, (2, 7, 12), "bf16") == 2 * 7 * 3 * 2
+    ae.c_code = 0
+    with pytest.raises(P.MoparError):
+        P.mopar_boundary_code_bytes(ae, (2, 7, 12), "bf16")
 
 
 def test_pipeline_workspace_and_validation_host_only():
