@@ -314,6 +314,24 @@ int mopar_model_forward(mopar_model_t model, const mopar_plan* plan, const mopar
                         const void* in_dev, void* out_dev, void* const* code_bufs, void* ws,
                         size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory -- code under HIP graph
+ * capture, serving loops or harnesses that forbid hipMalloc: mopar_model_forward
+ * with the workspace taken from a static device array the library owns
+ * (MOPAR_STATIC_WORKSPACE_BYTES per GPU, held until the process ends) instead of
+ * a caller buffer.  Inputs, outputs and code buffers are still the caller's.
+ * The call allocates nothing (its first call on a GPU looks the array's device
+ * address up once).  Same kernels, hence the same output bits, as
+ * mopar_model_forward.  Every call on one GPU shares that GPU's array: calls
+ * that overlap on one GPU (other streams, other threads) race and must be
+ * ordered by the caller.  The forward writes every workspace byte it reads, so
+ * the array's contents from an earlier call do not matter.
+ * Errors: as mopar_model_forward; MOPAR_E_WORKSPACE when the plan needs more
+ * than MOPAR_STATIC_WORKSPACE_BYTES (mopar_model_workspace_bytes tells), before
+ * any device call; MOPAR_E_ARG while per-op timing is on (it creates events). */
+#define MOPAR_STATIC_WORKSPACE_BYTES ((size_t)64 << 20)
+int mopar_model_forward_static(mopar_model_t model, const mopar_plan* plan, const mopar_codec* codecs,
+                               const void* in_dev, void* out_dev, void* const* code_bufs, void* stream);
+
 /* The tensors a cut after node `node` (0 <= node < n_layers - 1) carries: the
  * outputs of nodes <= node that nodes > node read (Sec. III-C: after node
  * elimination, the parallel edges between the two sides are one merged edge

@@ -21,6 +21,8 @@ OP_CONV, OP_LINEAR, OP_MAXPOOL, OP_AVGPOOL, OP_LAYERNORM = 1, 2, 3, 4, 5
 OP_ATTENTION, OP_EMBED_BERT, OP_EMBED, OP_LSTM = 6, 7, 8, 9
 ACT = {"none": 0, "relu": 1, "gelu": 2}
 CODEC_RAW, CODEC_AE = 0, 1
+# MOPAR_STATIC_WORKSPACE_BYTES of include/mopar.h: the static workspace of mopar_model_forward_static
+STATIC_WORKSPACE_BYTES = 64 << 20
 STATUS_NAMES = {0: "OK", 1: "E_ARG", 2: "E_SHAPE", 3: "E_DTYPE", 4: "E_UNSUPPORTED", 5: "E_INFEASIBLE",
                 6: "E_WORKSPACE", 7: "E_HIP"}
 
@@ -82,6 +84,8 @@ SIGNATURES = {
     "mopar_boundary_decode": (c_i32, [ctypes.POINTER(Codec), ctypes.POINTER(TensorDesc), c_vp, c_vp, c_vp]),
     "mopar_model_forward": (c_i32, [c_vp, ctypes.POINTER(Plan), ctypes.POINTER(Codec), c_vp, c_vp,
                                     ctypes.POINTER(c_vp), c_vp, ctypes.c_size_t, c_vp]),
+    "mopar_model_forward_static": (c_i32, [c_vp, ctypes.POINTER(Plan), ctypes.POINTER(Codec), c_vp, c_vp,
+                                           ctypes.POINTER(c_vp), c_vp]),
     "mopar_pipeline_workspace_bytes": (c_i32, [c_vp, ctypes.POINTER(Plan), c_i32, ctypes.POINTER(ctypes.c_size_t)]),
     "mopar_pipeline_create": (c_i32, [c_vp, ctypes.POINTER(Plan), ctypes.POINTER(Codec), c_i32, c_i32,
                                       ctypes.POINTER(c_vp), c_vp, ctypes.c_size_t, ctypes.POINTER(c_vp),

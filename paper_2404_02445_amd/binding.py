@@ -367,6 +367,16 @@ class SlicedModel:
                                         _ptr(ws), 0 if ws is None else ws.numel(), _stream_ptr(stream)))
         return out
 
+    def forward_static(self, plan, x, out, codecs=None, code_bufs=None, stream=None):
+        """mopar_model_forward_static: the same forward with the library's static workspace (for
+        callers that cannot allocate; see include/mopar.h)."""
+        bufs = list(code_bufs or [])
+        cb = (ctypes.c_void_p * max(len(bufs), 1))(*[b.data_ptr() for b in bufs])
+        cod = codecs if codecs is not None else (L.Codec * 1)()
+        check(lib().mopar_model_forward_static(self.handle, ctypes.byref(plan.raw), cod, _ptr(x), _ptr(out), cb,
+                                               _stream_ptr(stream)))
+        return out
+
     # -- cross-request slice pipeline ---------------------------------------------
     def pipeline(self, plan, codec="ae", codec_weights=None, depth=2, replicas=1, stream_per_slice=True):
         """A ``SlicePipeline``: ``replicas`` instances of the sliced model; each instance runs

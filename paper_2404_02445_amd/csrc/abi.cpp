@@ -19,6 +19,8 @@ int encode_impl(const mopar_codec*, const mopar_tensor_desc*, const void*, void*
 int decode_impl(const mopar_codec*, const mopar_tensor_desc*, const void*, void*, void*);
 int model_forward_impl(const mopar_model_s*, const mopar_plan*, const mopar_codec*, const void*, void*, void* const*,
                        void*, size_t, void*);
+int model_forward_static_impl(const mopar_model_s*, const mopar_plan*, const mopar_codec*, const void*, void*,
+                              void* const*, void*);
 
 int pipeline_ws_bytes_impl(const mopar_model_s*, const mopar_plan*, int32_t, size_t*);
 int pipeline_create_impl(const mopar_model_s*, const mopar_plan*, const mopar_codec*, int32_t, int32_t, void* const*,
@@ -113,6 +115,13 @@ int mopar_model_forward(mopar_model_t model, const mopar_plan* plan, const mopar
                         void* out_dev, void* const* code_bufs, void* ws, size_t ws_bytes, void* stream) {
     return guarded("mopar_model_forward", [&] {
         return model_forward_impl(model, plan, codecs, in_dev, out_dev, code_bufs, ws, ws_bytes, stream);
+    });
+}
+
+int mopar_model_forward_static(mopar_model_t model, const mopar_plan* plan, const mopar_codec* codecs,
+                               const void* in_dev, void* out_dev, void* const* code_bufs, void* stream) {
+    return guarded("mopar_model_forward_static", [&] {
+        return model_forward_static_impl(model, plan, codecs, in_dev, out_dev, code_bufs, stream);
     });
 }
 

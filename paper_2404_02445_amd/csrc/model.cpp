@@ -560,6 +560,8 @@ static int check_plan(const mopar_model_s* m, const mopar_plan* p, const char* w
     return MOPAR_OK;
 }
 
+bool model_timing_enabled(const mopar_model_s* m) { return m && m->timing; }
+
 int workspace_bytes_impl(const mopar_model_s* m, const mopar_plan* p, size_t* bytes) {
     if (!bytes) return set_error(MOPAR_E_ARG, "mopar_model_workspace_bytes: null output");
     const int rc = check_plan(m, p, "mopar_model_workspace_bytes");
