@@ -102,8 +102,48 @@ def source_hash():
     return h.hexdigest()[:16]
 
 
+_DEMANGLED = {}
+
+
+def _demangle(name):
+    """Readable kernel name.  This library's kernels (namespace mopar, integer / bool / type template
+    arguments) are decoded here; other names go through c++filt."""
+    import re
+    mm = re.match(r"_ZN5mopar(\d+)", name)
+    if mm:
+        n = int(mm.group(1))
+        base = name[len(mm.group(0)):len(mm.group(0)) + n]
+        rest = name[len(mm.group(0)) + n:]
+        args = []
+        if rest.startswith("I"):
+            body = rest[1:]
+            while body and not body.startswith("E"):
+                if body.startswith("DF16b"):
+                    args.append("bf16"); body = body[5:]
+                elif body.startswith("f"):
+                    args.append("float"); body = body[1:]
+                else:
+                    t = re.match(r"L([ib])(\d+)E", body)
+                    if not t:
+                        break
+                    args.append(("true" if t.group(2) == "1" else "false") if t.group(1) == "b" else t.group(2))
+                    body = body[t.end():]
+        return base + (f"<{', '.join(args)}>" if args else "")
+    if not name.startswith("_Z"):
+        return name
+    if name not in _DEMANGLED:
+        import subprocess
+        try:
+            _DEMANGLED[name] = subprocess.run(["c++filt", name], capture_output=True, text=True,
+                                              timeout=10).stdout.strip() or name
+        except (OSError, subprocess.SubprocessError):
+            _DEMANGLED[name] = name
+    return _DEMANGLED[name]
+
+
 def _short(name):
     """Kernel name without its argument list (template arguments kept)."""
+    name = _demangle(name)
     depth, out = 0, []
     for i, ch in enumerate(name):
         if ch == "(" and depth == 0 and out:
