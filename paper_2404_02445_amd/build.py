@@ -13,7 +13,7 @@ LIB = os.path.join(HERE, "libmopar.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["abi.cpp", "plan.cpp", "model.cpp", "gemm.hip", "kernels.hip", "noalloc.hip"]
+SOURCES = ["abi.cpp", "plan.cpp", "model.cpp", "gemm.hip", "kernels.hip", "noalloc.hip", "lstm.hip"]
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall", "-Wno-unused-result",
          # packed fp32 ALU ops are kept out of the generated code
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

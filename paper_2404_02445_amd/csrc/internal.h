@@ -162,6 +162,15 @@ hipError_t launch_embed(const int32_t* ids, const void* table, void* y, int64_t 
 hipError_t launch_attention(const void* qkv, void* y, int batch, int seq, int heads, float scale, int dtype,
                             hipStream_t s);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+// LSTM recurrence of one layer in a single launch (bf16, hidden a multiple of 16 and at most 1024,
+// hidden states and cell state under 2 GiB): hseq[b][t] = h_t from gx = x W_ih^T + b_ih + b_hh
+// (float32 [B*T][4H], rows interleaved by unit as the weights).  `sync` holds
+// lstm_recurrence_sync_bytes of step counters and tile claims, zeroed by the launcher; cst is
+// scratch for the cell state.
+bool lstm_recurrence_ok(int dtype, int64_t batch, int64_t steps, int64_t hidden);
+size_t lstm_recurrence_sync_bytes(int64_t batch, int64_t steps, int64_t hidden);
+hipError_t launch_lstm_recurrence(const float* gx, const void* whh, void* hseq, float* cst, void* sync, int batch,
+                                  int steps, int hidden, hipStream_t s);
 // One codec layer y[p][o] = b[o] + sum_c w[o][c] x[p][c] on the vector ALUs, for input widths off
 // the GEMM's 16-byte granule; positions * cout < 2^31.
 hipError_t launch_codec_narrow(const void* x, const void* w, const void* b, void* y, int64_t positions, int cin,

@@ -436,7 +436,10 @@ static int validate_and_build(mopar_model_s& m) {
                     return set_error(MOPAR_E_UNSUPPORTED, nm + ": a GEMM operand reaches 2 GiB");
                 inf.temps.push_back(static_cast<size_t>(bt * 4 * h) * 4);       // input projection, f32
                 inf.temps.push_back(static_cast<size_t>(x.dims[0] * h) * 4);    // cell state, f32
-                inf.temps.push_back(static_cast<size_t>(x.dims[0] * h) * es);   // h_0 = 0
+                if (lstm_recurrence_ok(m.dtype, x.dims[0], x.dims[1], h))       // one-launch recurrence:
+                    inf.temps.push_back(lstm_recurrence_sync_bytes(x.dims[0], x.dims[1], h));   // step sync
+                else
+                    inf.temps.push_back(static_cast<size_t>(x.dims[0] * h) * es);   // h_0 = 0
                 break;
             }
             default: return set_error(MOPAR_E_ARG, nm + ": unknown op kind");
@@ -682,9 +685,13 @@ static hipError_t run_op(const mopar_model_s& m, int i, const Ptrs& P, int ksub,
             float* gx = reinterpret_cast<float*>(P.ws + inf.temp_off[0]);
             float* cst = reinterpret_cast<float*>(P.ws + inf.temp_off[1]);
             void* h0 = P.ws + inf.temp_off[2];
-            hipError_t e = launch_fill_zero(cst, static_cast<size_t>(B) * H * 4, s);
-            if (e == hipSuccess) e = launch_fill_zero(h0, static_cast<size_t>(B) * H * dtype_size(dt), s);
-            if (e != hipSuccess) return e;
+            const bool one_launch = lstm_recurrence_ok(dt, B, T, H);
+            hipError_t e = hipSuccess;
+            if (!one_launch) {
+                e = launch_fill_zero(cst, static_cast<size_t>(B) * H * 4, s);
+                if (e == hipSuccess) e = launch_fill_zero(h0, static_cast<size_t>(B) * H * dtype_size(dt), s);
+                if (e != hipSuccess) return e;
+            }
             // input projection for all steps: gx = x W_ih^T + b_ih + b_hh (float32)
             GemmParams g{};
             g.A = P.get(op.in0);
@@ -701,7 +708,8 @@ static hipError_t run_op(const mopar_model_s& m, int i, const Ptrs& P, int ksub,
             g.out_f32 = 1;
             e = launch_gemm(g, dt, s);
             if (e != hipSuccess) return e;
-            // recurrence: one GEMM per step with the cell update fused in its epilogue
+            if (one_launch) return launch_lstm_recurrence(gx, W(m, op.w2), P.get(op.out), cst, h0, B, T, H, s);
+            // otherwise one GEMM per step with the cell update fused in its epilogue
             unsigned char* hseq = static_cast<unsigned char*>(P.get(op.out));
             const size_t es = dtype_size(dt);
             for (int t = 0; t < T; ++t) {

@@ -1,0 +1,93 @@
+"""The LSTM recurrence on the GPU.
+
+bf16 layers whose hidden size is a multiple of 16 (up to 1024) run the whole
+recurrence in one launch; others run one GEMM per step.  Both are checked
+against the oracle.  The one-launch kernel lets any resident block compute a
+tile whose owner is not running; the tests force that from the host (a hook
+makes some blocks exit at once) and require the same output bits, and run two
+layers concurrently on two streams.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests.helpers import TOL, rel_err
+
+pytestmark = pytest.mark.gpu
+P = pytest.importorskip("paper_2404_02445_amd")
+
+
+def lstm_model(b, t, e, h, seed=3, layers=1):
+    bld = synth._Builder("lstm", "bf16", b, seed)
+    ids = bld.tensor((b, t), "i32")
+    bld.new_layer("L0")
+    x = bld.embed(ids, b * t, e, "src", -1.0, 1.0)
+    for i in range(layers):
+        x = bld.lstm(x, h, f"lstm{i}", -0.3, 0.3)
+    return bld.finish(x, 1), np.arange(b * t, dtype=np.int32).reshape(b, t)
+
+
+def forward(m, ids, stream=None):
+    sm = P.SlicedModel(m)
+    plan = P.make_plan(1, [0], [1])
+    ws = sm.alloc_workspace(plan)
+    out = sm.alloc_output()
+    x = torch.from_numpy(ids).cuda()
+    if stream is not None:                  # weights and ids were uploaded on torch's stream
+        stream.wait_stream(torch.cuda.current_stream())
+    sm.forward(plan, x, out, None, None, ws, stream=stream)
+    return out, (sm, ws, x)
+
+
+def canon(t):
+    return t.float().cpu().numpy()
+
+
+@pytest.mark.parametrize("b,t,e,h", [
+    (37, 6, 64, 48),       # ragged batch group (37 = 2 x 16 + 5), K padded to a whole MFMA step
+    (17, 1, 16, 32),       # a single step
+    (64, 5, 128, 256),
+    (5, 9, 1024, 1024),    # the LSTM LM's hidden size: 32 weight fragments per lane
+    (3, 4, 24, 40),        # hidden size off the 16-unit tile: one GEMM per step
+])
+def test_lstm_recurrence_parity(b, t, e, h):
+    m, ids = lstm_model(b, t, e, h)
+    y, _ = forward(m, ids)
+    torch.cuda.synchronize()
+    assert rel_err(canon(y), oracle.forward(m, ids)) <= TOL["bf16"]
+
+
+@pytest.mark.parametrize("absent", [2, 3, 7])
+def test_tiles_of_blocks_that_never_run_are_computed_by_others(absent):
+    m, ids = lstm_model(40, 12, 64, 256, layers=2)
+    ref, _ = forward(m, ids)
+    torch.cuda.synchronize()
+    os.environ["MOPAR_TEST_LSTM_ABSENT"] = str(absent)
+    try:
+        got, _ = forward(m, ids)
+        torch.cuda.synchronize()
+    finally:
+        del os.environ["MOPAR_TEST_LSTM_ABSENT"]
+    assert torch.equal(got, ref)
+    assert rel_err(canon(got), oracle.forward(m, ids)) <= TOL["bf16"]
+
+
+def test_two_layers_running_concurrently_on_two_streams():
+    m, ids = lstm_model(64, 24, 256, 512, layers=2)
+    ref, _ = forward(m, ids)
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    keep = []
+    outs = []
+    for rep in range(3):
+        for s in (s1, s2):
+            o, k = forward(m, ids, stream=s)
+            outs.append(o)
+            keep.append(k)
+    torch.cuda.synchronize()
+    for o in outs:
+        assert torch.equal(o, ref)
