@@ -101,7 +101,8 @@ typedef struct {
     double lambda_bytes;        /* eta <= floor(M_g / lambda) when > 0 (Eq. 6 constraint)         */
     const double* tp_table;     /* [n][k_max] measured t_p(l, eta); NULL: t_p = t_l               */
     const double* ta_table;     /* [n][k_max] measured t_a(l, eta); NULL: 0                       */
-    const int32_t* k_override;  /* n entries; > 0 forces k for that node; NULL: none              */
+    const int32_t* k_override;  /* n entries; > 0 forces k for that node (at most the node's RD
+                                   width, and at most k_max when measured tables are given); NULL: none */
     int32_t uniform;            /* 1: the Uniform partitioning of the evaluation (Sec. IV): exactly
                                    n_slices (> 0) slices with equal node counts (the first
                                    n mod n_slices one node longer); allowed_cut and elimination do

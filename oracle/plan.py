@@ -379,6 +379,8 @@ def plan_slices(prof, opts: PlanOpts) -> Plan:
             if opts.k_override[l] > 0:
                 if prof[l].rd_width == 0 or opts.k_override[l] > prof[l].rd_width:
                     raise ValueError("k_override on a node without a wide enough RD op")
+                if opts.k_override[l] > max(1, opts.k_max) and (opts.tp_table is not None or opts.ta_table is not None):
+                    raise ValueError("k_override beyond k_max: the measured tables stop at k_max")
                 k[l] = int(opts.k_override[l])
 
     t_tau = 0.0

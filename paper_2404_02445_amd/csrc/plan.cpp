@@ -75,6 +75,10 @@ int plan_slices_impl(const mopar_layer_profile* L, int32_t n, const mopar_plan_o
             if (k < 0 || (k > 0 && (L[l].rd_width == 0 ? k > 1 : k > L[l].rd_width)))
                 return set_error(MOPAR_E_ARG, "mopar_plan_slices: k_override[" + std::to_string(l) +
                                                   "] needs an RD op at least that wide");
+            // measured tables hold t_p / t_a for eta = 1 .. k_max only
+            if (k > kmax && (o->tp_table || o->ta_table))
+                return set_error(MOPAR_E_ARG, "mopar_plan_slices: k_override[" + std::to_string(l) +
+                                                  "] exceeds k_max, beyond the measured tables");
         }
 
     // step 1: graph simplification

@@ -151,6 +151,9 @@ def seq_ids(b, s):
     ("f32", 2, 7, 36, 44, "relu", True, 2),
     # few rows: K split across the waves of a block, with split-K and a K tail (2000 = 31*64 + 16)
     ("bf16", 16, 1, 2000, 96, "relu", False, 3),
+    # split-K summed in the GEMM launch (k = 1) against the separate reduce launch (k = 100 sub-slices
+    # need more arrival counters than the op's slot holds): bitwise equal
+    ("bf16", 16, 1, 2000, 200, "relu", False, 100),
     # M = 40: the 64x64 and 64x16 K-split tiles (k = 1 vs k = 4) must agree bit for bit
     ("bf16", 5, 8, 1504, 70, "gelu", True, 4),
     ("f32", 4, 4, 700, 33, "none", True, 2),

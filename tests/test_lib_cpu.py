@@ -350,3 +350,17 @@ def test_model_create_checks_what_the_kernels_assume():
     assert _create_error(concat([(13, 0), (16, 16)])) == L.MOPAR_E_ARG
     # the output must come from the last op, not from a concatenation's first writer
     assert _create_error(concat([(13, 0), (19, 13)], head=False)) == L.MOPAR_E_ARG
+
+
+def test_k_override_beyond_measured_tables_refused_by_both_planners():
+    """A forced sub-slice count above k_max has no measured t_p / t_a: both planners refuse it
+    (the library used to read past the tables; found by the sanitizer run)."""
+    prof = [(1e6, 1e-4, 1e3, 64)] * 3
+    tp = [[1e-4, 2e-4]] * 3
+    with pytest.raises(P.MoparError, match="ARG"):
+        P.mopar_plan_slices(prof, k_max=2, tp_table=tp, k_override=[0, 4, 0])
+    with pytest.raises(ValueError):
+        OP.plan_slices([OP.LayerProfile(*p) for p in prof],
+                       OP.PlanOpts(k_max=2, tp_table=tp, k_override=[0, 4, 0]))
+    # without tables the analytic t_p applies to any k
+    assert P.mopar_plan_slices(prof, k_max=2, k_override=[0, 4, 0]).k[1] == 4
