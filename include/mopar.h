@@ -36,9 +36,12 @@
  *            dtype; rank-2/3 tensors are row-major.  Weight layouts are
  *            given at mopar_op.
  * Determinism. Plans and sub-slice ranges are pure functions of their
- *            inputs; kernels use no atomics, so a forward pass is bitwise
- *            reproducible, and the k-way sub-sliced RD kernels produce the
- *            same bits as the unsplit kernel.
+ *            inputs, and a forward pass is bitwise reproducible: no kernel
+ *            accumulates through atomics, and the one-launch LSTM recurrence,
+ *            whose blocks claim (step, tile) work with atomics, computes a
+ *            tile with the same operands and operation order whichever block
+ *            claims it.  The k-way sub-sliced RD kernels produce the same bits
+ *            as the unsplit kernel.
  */
 #ifndef MOPAR_H
 #define MOPAR_H

@@ -162,11 +162,13 @@ hipError_t launch_embed(const int32_t* ids, const void* table, void* y, int64_t 
 hipError_t launch_attention(const void* qkv, void* y, int batch, int seq, int heads, float scale, int dtype,
                             hipStream_t s);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+// every byte of [p, p + bytes) set to `value` (a fill kernel: safe to record in a graph)
+hipError_t launch_fill_bytes(void* p, size_t bytes, unsigned char value, hipStream_t s);
 // LSTM recurrence of one layer in a single launch (bf16, hidden a multiple of 16 and at most 1024,
 // hidden states and cell state under 2 GiB): hseq[b][t] = h_t from gx = x W_ih^T + b_ih + b_hh
 // (float32 [B*T][4H], rows interleaved by unit as the weights).  `sync` holds
-// lstm_recurrence_sync_bytes of step counters and tile claims, zeroed by the launcher; cst is
-// scratch for the cell state.
+// lstm_recurrence_sync_bytes of tile claims, zeroed by the launcher, which also fills hseq
+// with 0xFF bytes (the kernel's "not yet stored" mark); cst is scratch for the cell state.
 bool lstm_recurrence_ok(int dtype, int64_t batch, int64_t steps, int64_t hidden);
 size_t lstm_recurrence_sync_bytes(int64_t batch, int64_t steps, int64_t hidden);
 hipError_t launch_lstm_recurrence(const float* gx, const void* whh, void* hseq, float* cst, void* sync, int batch,

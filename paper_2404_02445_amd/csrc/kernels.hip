@@ -704,14 +704,14 @@ __global__ void copy_tail_kernel(const unsigned char* src, unsigned char* dst, i
     const int64_t i = threadIdx.x;
     if (i < n) dst[i] = src[i];
 }
-__global__ void fill_zero_kernel(uint4* __restrict__ dst, int64_t n16) {
+__global__ void fill_kernel(uint4* __restrict__ dst, int64_t n16, unsigned v) {
     for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n16;
          i += static_cast<int64_t>(gridDim.x) * blockDim.x)
-        dst[i] = make_uint4(0, 0, 0, 0);
+        dst[i] = make_uint4(v, v, v, v);
 }
-__global__ void fill_zero_tail_kernel(unsigned char* dst, int64_t n) {
+__global__ void fill_tail_kernel(unsigned char* dst, int64_t n, unsigned char v) {
     const int64_t i = threadIdx.x;
-    if (i < n) dst[i] = 0;
+    if (i < n) dst[i] = v;
 }
 
 static unsigned stream_blocks(int64_t n16) {
@@ -733,16 +733,19 @@ hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s) 
     return hipGetLastError();
 }
 
-hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
+hipError_t launch_fill_bytes(void* p, size_t bytes, unsigned char value, hipStream_t s) {
     const int64_t n16 = static_cast<int64_t>(bytes / 16);
     if (n16 > 0)
-        launch_kernel(fill_zero_kernel, dim3(stream_blocks(n16)), dim3(256), 0, s, static_cast<uint4*>(p), n16);
+        launch_kernel(fill_kernel, dim3(stream_blocks(n16)), dim3(256), 0, s, static_cast<uint4*>(p), n16,
+                      0x01010101u * value);
     const int64_t tail = static_cast<int64_t>(bytes % 16);
     if (tail)
-        launch_kernel(fill_zero_tail_kernel, dim3(1), dim3(16), 0, s,
-                           static_cast<unsigned char*>(p) + n16 * 16, tail);
+        launch_kernel(fill_tail_kernel, dim3(1), dim3(16), 0, s, static_cast<unsigned char*>(p) + n16 * 16, tail,
+                      value);
     return hipGetLastError();
 }
+
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) { return launch_fill_bytes(p, bytes, 0, s); }
 
 // ---------------------------------------------------------------------------
 // One autoencoder codec layer whose input width is not a whole number of 16-byte

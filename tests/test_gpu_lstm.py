@@ -3,9 +3,9 @@
 bf16 layers whose hidden size is a multiple of 16 (up to 1024) run the whole
 recurrence in one launch; others run one GEMM per step.  Both are checked
 against the oracle.  The one-launch kernel lets any resident block compute a
-tile whose owner is not running; the tests force that from the host (a hook
-makes some blocks exit at once) and require the same output bits, and run two
-layers concurrently on two streams.
+tile whose owner is not running; the tests force that from the host (hooks make
+some blocks exit at once, or start late) and require the same output bits, and
+run two layers concurrently on two streams.
 """
 import os
 
@@ -72,6 +72,23 @@ def test_tiles_of_blocks_that_never_run_are_computed_by_others(absent):
         torch.cuda.synchronize()
     finally:
         del os.environ["MOPAR_TEST_LSTM_ABSENT"]
+    assert torch.equal(got, ref)
+    assert rel_err(canon(got), oracle.forward(m, ids)) <= TOL["bf16"]
+
+
+@pytest.mark.parametrize("late_us", [1000, 5000])
+def test_owners_that_start_late_take_over_from_helpers(late_us):
+    # the owners of every third gate slice start late: others compute those tiles' first steps
+    # (their cell state left in memory), then each owner claims the steps still free and goes on
+    m, ids = lstm_model(40, 40, 64, 256, layers=2)
+    ref, _ = forward(m, ids)
+    torch.cuda.synchronize()
+    os.environ["MOPAR_TEST_LSTM_LATE_US"] = str(late_us)
+    try:
+        got, _ = forward(m, ids)
+        torch.cuda.synchronize()
+    finally:
+        del os.environ["MOPAR_TEST_LSTM_LATE_US"]
     assert torch.equal(got, ref)
     assert rel_err(canon(got), oracle.forward(m, ids)) <= TOL["bf16"]
 
