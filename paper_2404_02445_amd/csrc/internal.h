@@ -102,6 +102,7 @@ struct GemmParams {
     const void* bias2;      // optional second bias [N]
     int out_f32;            // store C as float32 instead of the model dtype
     int epi;                // EPI_STD or EPI_LSTM
+    int thin;               // a boundary codec layer: few output columns or a short K, bandwidth-bound
     // EPI_LSTM: columns 4u..4u+3 are gates i, f, g, o of hidden unit u.
     const float* gx;        // [M][ldgx] float32 gate pre-activations added to the product
     int64_t ldgx;

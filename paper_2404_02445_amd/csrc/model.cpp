@@ -925,6 +925,7 @@ static hipError_t codec_apply(const mopar_codec& c, int dtype, int64_t pos, int 
     g.N = encode ? c.c_code : c.c;
     g.K = encode ? c.c : c.c_code;
     g.ksub = 1;
+    g.thin = 1;
     return launch_gemm(g, dtype, s);
 }
 
