@@ -142,8 +142,9 @@ def _demangle(name):
 
 
 def _short(name):
-    """Kernel name without its argument list (template arguments kept)."""
-    name = _demangle(name)
+    """Kernel name without its argument list (template arguments kept).  rocprofv3's csv names
+    spell bf16 template arguments as "bool _Accum"; they are written back as bf16."""
+    name = _demangle(name).replace("(anonymous namespace)::", "").replace("bool _Accum", "bf16")
     depth, out = 0, []
     for i, ch in enumerate(name):
         if ch == "(" and depth == 0 and out:
@@ -159,22 +160,30 @@ def _rows(path):
         return list(csv.DictReader(f))
 
 
-def summarize_trace(path, title, cmd):
-    """Markdown: per (kernel, grid) dispatch count and mean / median duration from a rocprofv3
-    kernel-trace csv."""
+def summarize_trace(path, title, cmd, min_share=0.002):
+    """Markdown: per (kernel, grid, stream) dispatch count and mean / median duration from a
+    rocprofv3 kernel-trace csv (groups below `min_share` of all kernel time folded into one row)."""
     groups = {}
     for r in _rows(path):
         key = (_short(r["Kernel_Name"]), int(r.get("Grid_Size", r.get("Grid_Size_X", 0)) or 0),
-               int(r.get("Workgroup_Size", r.get("Workgroup_Size_X", 0)) or 0))
+               int(r.get("Workgroup_Size", r.get("Workgroup_Size_X", 0)) or 0), int(r.get("Stream_Id", 0) or 0))
         groups.setdefault(key, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
     total = sum(sum(v) for v in groups.values())
     lines = [f"# {title}", "", "Command (from the repository root, on the GPU box):", "", "```", cmd, "```", "",
-             f"Source hash of `csrc/`: `{source_hash()}`.  Durations in microseconds, grouped by kernel and "
-             f"grid size (threads); share = the group's fraction of all kernel time.", "",
-             "| kernel | grid | block | dispatches | mean us | median us | share |", "|---|---|---|---|---|---|---|"]
+             f"Source hash of `csrc/`: `{source_hash()}`.  Durations in microseconds, grouped by kernel, "
+             f"grid size (threads) and HIP stream; share = the group's fraction of all kernel time.", "",
+             "| kernel | grid | block | stream | dispatches | mean us | median us | share |",
+             "|---|---|---|---|---|---|---|---|"]
+    rest_n, rest_t = 0, 0.0
     for key, v in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
-        lines.append(f"| `{key[0]}` | {key[1]} | {key[2]} | {len(v)} | {statistics.fmean(v):.2f} | "
+        if sum(v) / total < min_share:
+            rest_n += len(v)
+            rest_t += sum(v)
+            continue
+        lines.append(f"| `{key[0]}` | {key[1]} | {key[2]} | {key[3]} | {len(v)} | {statistics.fmean(v):.2f} | "
                      f"{statistics.median(v):.2f} | {sum(v) / total:.3f} |")
+    if rest_n:
+        lines.append(f"| (other groups) | | | | {rest_n} | | | {rest_t / total:.3f} |")
     return "\n".join(lines)
 
 
@@ -206,34 +215,63 @@ def summarize_pmc(paths, title, cmd, copy_mib, grid_of_interest=None):
         lines += ["", f"Copy calibration: a raw copy of {copy_mib} MiB reads FETCH_SIZE {cf:.1f} KiB and "
                       f"WRITE_SIZE {cw:.1f} KiB: scale factors {sf:.4f} (read), {sw:.4f} (write)."]
         if grid_of_interest:
-            for key, d in vals.items():
-                if key[1] == grid_of_interest and "FETCH_SIZE" in d:
-                    t = (statistics.fmean(d["FETCH_SIZE"]) * sf + statistics.fmean(d["WRITE_SIZE"]) * sw) * 1024.0
-                    out = {"kernel": key[0], "grid": key[1], "traffic_bytes_per_launch": round(t)}
+            # the dispatches of interest: comma-separated grid sizes and / or kernel-name substrings;
+            # the traffic per launch is their dispatch-weighted mean
+            # Each selector is [name][@grid][#mfma]: a kernel-name part, a grid size, and an exact
+            # SQ_INSTS_MFMA count that keeps only the dispatches of one op when several ops share a
+            # kernel and grid (the passes are separate runs of one deterministic sequence, so the
+            # i-th dispatch of a group is the same op in every pass).  Selectors are separated by
+            # "|"; the traffic is the mean over every selected dispatch.
+            sel = [x.strip() for x in str(grid_of_interest).split("|") if x.strip()]
+
+            def parse(x):
+                x, _, mf = x.partition("#")
+                name, at, grid = x.rpartition("@")
+                if not at:
+                    name, grid = (x, "") if not x.isdigit() else ("", x)
+                return name, (int(grid) if grid else None), (float(mf) if mf else None)
+            tot, cnt = 0.0, 0
+            for x in sel:
+                name, grid, mf = parse(x)
+                for key, d in vals.items():
+                    if (name and name not in key[0]) or (grid is not None and key[1] != grid):
+                        continue
+                    if "FETCH_SIZE" not in d or "WRITE_SIZE" not in d:
+                        continue
+                    idx = range(min(len(d["FETCH_SIZE"]), len(d["WRITE_SIZE"])))
+                    if mf is not None:
+                        idx = [i for i in idx if i < len(d.get("SQ_INSTS_MFMA", [])) and d["SQ_INSTS_MFMA"][i] == mf]
+                    for i in idx:
+                        tot += (d["FETCH_SIZE"][i] * sf + d["WRITE_SIZE"][i] * sw) * 1024.0
+                        cnt += 1
+            if cnt:
+                out = {"traffic_bytes_per_launch": round(tot / cnt), "dispatches": cnt}
             lines += ["", "```", f"source_hash: {source_hash()}",
                       f"grid: {grid_of_interest}",
+                      f"dispatches: {out.get('dispatches', 0)}",
                       f"traffic_bytes_per_launch: {out.get('traffic_bytes_per_launch', 'nan')}", "```"]
     return "\n".join(lines)
 
 
 def committed_traffic(workload):
     """HBM traffic per launch of the workload's dominant kernel from its committed counter summary
-    (profiles/<kernel>_<workload>_traffic.md), or None when missing or taken on other sources."""
+    (profiles/<kernel>_<workload>_traffic.md) and the dispatches it covers, or (None, None) when
+    missing or taken on other sources."""
     try:
         files = [f for f in os.listdir(PROFILES) if f.endswith(f"_{workload}_traffic.md")]
     except OSError:
-        return None
+        return None, None
     for f in files:
         kv = {}
         for line in open(os.path.join(PROFILES, f)).read().splitlines():
-            if ": " in line and line.split(": ", 1)[0] in ("source_hash", "traffic_bytes_per_launch", "grid"):
+            if ": " in line and line.split(": ", 1)[0] in ("source_hash", "traffic_bytes_per_launch", "grid", "scope"):
                 kv[line.split(": ", 1)[0]] = line.split(": ", 1)[1]
         if kv.get("source_hash") == source_hash():
             try:
-                return float(kv["traffic_bytes_per_launch"])
+                return float(kv["traffic_bytes_per_launch"]), kv.get("scope")
             except (KeyError, ValueError):
-                return None
-    return None
+                return None, None
+    return None, None
 
 
 # ---------------------------------------------------------------------------
@@ -455,7 +493,9 @@ def run_config(cfg, args, headline):
         achieved = rd_fl / len(rd) / (rd_launch_us * 1e-6) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4)}
-    roof["traffic"] = committed_traffic(WORKLOAD_TAG[cfg]) if headline else None
+    roof["traffic"], scope = committed_traffic(WORKLOAD_TAG[cfg])
+    if scope:
+        roof["traffic_scope"] = scope
     roof.update({
         "kernel": "the RD ops' launches (gemm_kernel; conv3_halo_kernel for patch-staged 3x3 convs), one "
                   "launch per RD op holding its k sub-slices: " + rd_names(m, rd),
@@ -591,14 +631,16 @@ def main():
     ap.add_argument("--summarize-trace", nargs=3, metavar=("CSV", "TITLE", "CMD"),
                     help="print a markdown summary of a rocprofv3 kernel-trace csv and exit")
     ap.add_argument("--summarize-pmc", nargs="+", metavar="ARG",
-                    help="TITLE CMD COPY_MIB GRID CSV...: markdown summary of rocprofv3 --pmc csv files, and exit")
+                    help="TITLE CMD COPY_MIB SELECT CSV...: markdown summary of rocprofv3 --pmc csv files, and "
+                         "exit; SELECT = '|'-separated [kernel-name part][@grid][#SQ_INSTS_MFMA] selectors of the "
+                         "dispatches whose mean HBM traffic per launch is reported (0: none)")
     args = ap.parse_args()
     if args.summarize_trace:
         print(summarize_trace(*args.summarize_trace))
         return
     if args.summarize_pmc:
         title, cmd, mib, grid, *paths = args.summarize_pmc
-        print(summarize_pmc(paths, title, cmd, int(mib), int(grid) or None))
+        print(summarize_pmc(paths, title, cmd, int(mib), grid if grid not in ("", "0") else None))
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
