@@ -364,3 +364,21 @@ def test_k_override_beyond_measured_tables_refused_by_both_planners():
                        OP.PlanOpts(k_max=2, tp_table=tp, k_override=[0, 4, 0]))
     # without tables the analytic t_p applies to any k
     assert P.mopar_plan_slices(prof, k_max=2, k_override=[0, 4, 0]).k[1] == 4
+
+
+def test_split_k_factor_never_exceeds_what_the_reduce_handles():
+    # the split-K reduce keeps every split's partial in flight at once, for at most 16 splits;
+    # the factor the executor asks for (a host function of the library) must stay in 1..16, a
+    # power of two, and above 1 only for long K loops (at least 24 stages of 64 bf16 / 32 fp32)
+    fn = getattr(L.lib(), "_ZN5mopar11gemm_splitsEliiii")
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int]
+    for dtype, bk in ((L.MOPAR_BF16, 64), (L.MOPAR_F32, 32)):
+        for M in (1, 16, 63, 64, 392, 1568, 25088, 1 << 20):
+            for N in (1, 16, 100, 4096, 32000):
+                for K in (1, 64, 1535, 1536, 4608, 25088, 1 << 20):
+                    s = fn(M, N, K, dtype, 0)
+                    assert 1 <= s <= 16 and s & (s - 1) == 0, (M, N, K, s)
+                    if (K + bk - 1) // bk < 24:
+                        assert s == 1, (M, N, K, s)
+                    assert fn(M, N, K, dtype, 1) == 1   # the LSTM epilogue never splits
