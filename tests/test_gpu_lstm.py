@@ -53,6 +53,9 @@ def canon(t):
     (64, 5, 128, 256),
     (5, 9, 1024, 1024),    # the LSTM LM's hidden size: 32 weight fragments per lane
     (3, 4, 24, 40),        # hidden size off the 16-unit tile: one GEMM per step
+    (2, 7, 8, 16),         # the smallest hidden size: one gate slice, one tile per batch group
+    (1, 4096, 8, 16),      # the longest sequence of one launch
+    (1, 4097, 8, 16),      # one step more: one GEMM per step
 ])
 def test_lstm_recurrence_parity(b, t, e, h):
     m, ids = lstm_model(b, t, e, h)
