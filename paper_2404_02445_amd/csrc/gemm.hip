@@ -821,6 +821,340 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
     }
 }
 
+// Wide products (bf16, dense A, large M, N and K; see gemm_wide_class): 256 x 256 block tiles on
+// v_mfma_f32_32x32x16_bf16.  Four waves each own a 128 x 128 quadrant -- 16 accumulator tiles of
+// 32 x 32, 256 registers per lane, which the compiler keeps in the accumulation half of the
+// register file -- so one block fills a CU, one wave per SIMD.  (A single wave per SIMD issues
+// the 32 x 32 x 16 MFMA at ~90 % of the peak rate but the 16 x 16 x 32 one at ~55 %, measured.)
+// A stage holds 64 k (64 KB: 256 rows of A and of B, one cache line each) and costs one
+// barrier; two stages in LDS.  Per stage a CU moves 64 KB for 8.4 MFLOP (128 FLOP/B, twice the
+// 128 x 128 tile's) and a wave reads 32 KB of fragments for 64 MFMAs.  Each 16-wide k step's
+// MFMAs run while the next step's fragments are read, so LDS reads always overlap MFMAs, and the
+// next stage's loads are spread over the first k step.  Operand loads (whole-line rows into
+// XOR-swizzled LDS blocks) are gemm_kernel's; the MFMA shape is not, so an operator whose
+// (M, N, K) puts it here runs here for every sub-slice launch, and every output element sees the
+// same operations in the same order whatever the sub-slice count.
+constexpr int kWideRowB = 256 * 2 + 16, kWideRowF = 256 * 4 + 16;   // staged output row strides, bytes
+// An accumulator read out where it is used (left to itself the compiler copies many accumulator
+// tiles to ordinary registers at once, and spills them)
+__device__ __forceinline__ float acc_read(float a) {
+    float v;
+    asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v) : "a"(a));
+    return v;
+}
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+__global__ __launch_bounds__(256, 1) void gemm_wide_kernel(const GemmParams p) {
+    using T = __bf16;
+    constexpr int BM = 256, BN = 256, TM = 128, TN = 128;
+    constexpr int FM = TM / 32, FN = TN / 32;   // 32 x 32 MFMA tiles per wave
+    constexpr int NBA = BM / 8, NBB = BN / 8;   // 1 KB blocks (8 rows x 128 bytes) per stage
+    constexpr int NW = 4;
+    constexpr int LA = NBA / NW, LB = NBB / NW; // load slots per wave (8 + 8)
+    constexpr int STAGE = (NBA + NBB) * 64;     // uint4 per stage
+    constexpr int BK = 64;
+    // the epilogue's staged tile: 256 rows of bf16 or 128 rows of float32, rows padded by 16 bytes
+    constexpr int TILE_U4 = (BM * kWideRowB > TM * kWideRowF ? BM * kWideRowB : TM * kWideRowF) / 16;
+    __shared__ uint4 lds[2 * STAGE > TILE_U4 ? 2 * STAGE : TILE_U4];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wm = wave >> 1, wn = wave & 1;
+
+    touch_kernargs<sizeof(GemmParams)>();
+    const unsigned t = (blockIdx.x % 8) * static_cast<unsigned>(p.g_per_xcd) + blockIdx.x / 8;
+    if (t >= static_cast<unsigned>(p.g_total)) return;
+    constexpr int GM = kGroupM;
+    const unsigned group = p.g_div_group.div(t);
+    const unsigned within = t - group * static_cast<unsigned>(GM * p.g_cols);
+    const bool last = static_cast<int>(group) == (p.g_mt - 1) / GM;
+    const unsigned gm = last ? static_cast<unsigned>(p.g_mt - group * GM) : GM;
+    const unsigned colu = last ? p.g_div_last.div(within) : within / GM;
+    const int mti = static_cast<int>(group * GM + (within - colu * gm));
+    const unsigned c1 = p.g_div_nt.div(colu);
+    const int nti = static_cast<int>(colu - c1 * static_cast<unsigned>(p.g_nt));
+    const int j = static_cast<int>(c1);         // one split: the column index is the sub-slice
+
+    const int q = p.g_q, rr = p.g_rr;
+    const int n_lo = j * q + min(j, rr), n_hi = (j + 1) * q + min(j + 1, rr);
+    const int n0 = n_lo + nti * BN;
+    if (n0 >= n_hi) return;
+    const int Mi = static_cast<int>(p.M);
+    const int m0 = mti * BM;
+    const int nk = p.g_nk;                      // >= 1 (K >= 64 here)
+
+    // operand loads: gemm_kernel's layout (8 whole rows per 1 KB block, chunk (l % 8) ^ row)
+    const int cl = (lane & 7) ^ (lane >> 3);
+    unsigned voffA[LA], voffB[LB];
+#pragma unroll
+    for (int i = 0; i < LA; ++i) {
+        const int m = m0 + (wave + NW * i) * 8 + (lane >> 3);
+        const int mc = m < Mi ? m : Mi - 1;
+        voffA[i] = static_cast<unsigned>(mc) * static_cast<unsigned>(p.lda * sizeof(T)) + static_cast<unsigned>(cl * 16);
+    }
+#pragma unroll
+    for (int i = 0; i < LB; ++i) {
+        const int n = n0 + (wave + NW * i) * 8 + (lane >> 3);
+        const int nc = n < n_hi ? n : n_hi - 1;
+        voffB[i] = static_cast<unsigned>(nc) * static_cast<unsigned>(p.K * sizeof(T)) + static_cast<unsigned>(cl * 16);
+    }
+    const int ktail = (p.K % BK) ? nk - 1 : nk;
+    // load slots 2 i and 2 i + 1 (A blocks wave + 4 s, B blocks wave + 4 s) of stage kt into LDS at dst
+    auto issue_pair = [&](int kt, uint4* dst, int i) __attribute__((always_inline)) {
+        const unsigned soff = static_cast<unsigned>(kt) * (BK * sizeof(T));
+        const bool kin = kt != ktail || kt * BK + cl * 8 < p.K;
+#pragma unroll
+        for (int s2 = 2 * i; s2 < 2 * i + 2; ++s2) {
+            buffer_load_lds(p.A, p.a_bytes, (lds_ptr_t)(dst + (wave + NW * s2) * 64), kin ? voffA[s2] : kOOB, soff);
+            buffer_load_lds(p.B, p.b_bytes, (lds_ptr_t)(dst + (NBA + wave + NW * s2) * 64), kin ? voffB[s2] : kOOB, soff);
+        }
+    };
+    static_assert(LA == LB && LA == 2 * FM, "two load slots per row of fragments");
+
+    // MFMA layout (weight fragment first): accumulator register r of tile (a, b) holds output
+    // row m = m0 + wm TM + 32 a + l % 32 and column n = n0 + wn TN + 32 b + 8 (r / 4) + 4 (l / 32)
+    // + r % 4: four groups of four consecutive columns per lane
+    const int lrow = lane & 31, lhalf = lane >> 5;
+    // bias + second bias, as gemm_kernel starts a direct launch (partial groups read up front)
+    const T* biasp = static_cast<const T*>(p.bias);
+    const T* bias2p = static_cast<const T*>(p.bias2);
+    Raw4<T> rb[FN][4], rb2[FN][4];
+    float bslow[FN][4][4];
+#pragma unroll
+    for (int b = 0; b < FN; ++b)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const int n = n0 + wn * TN + b * 32 + g * 8 + lhalf * 4;
+            const int nv = max(0, min(4, n_hi - n));
+            const bool fast = nv == 4;
+            rb[b][g] = load_raw4<T>(fast && biasp ? biasp + n : nullptr, kZeroChunk);
+            rb2[b][g] = load_raw4<T>(fast && bias2p ? bias2p + n : nullptr, kZeroChunk);
+            float bv[4], b2v[4];
+            ld4_or_zero<T>(biasp, n, fast ? 0 : nv, bv);
+            ld4_or_zero<T>(bias2p, n, fast ? 0 : nv, b2v);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) bslow[b][g][e] = bv[e] + b2v[e];
+        }
+
+    static_for<FM>([&](auto i) __attribute__((always_inline)) { issue_pair(0, &lds[0], i); });
+
+    f32x16 acc[FM][FN];
+#pragma unroll
+    for (int b = 0; b < FN; ++b)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const int n = n0 + wn * TN + b * 32 + g * 8 + lhalf * 4;
+            const bool fast = n + 4 <= n_hi;
+            float bv[4], b2v[4];
+            unpack4<T>(rb[b][g], bv);
+            unpack4<T>(rb2[b][g], b2v);
+#pragma unroll
+            for (int a = 0; a < FM; ++a)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) acc[a][b][4 * g + e] = fast ? bv[e] + b2v[e] : bslow[b][g][e];
+        }
+
+    // LDS byte address of this lane's fragment (row l % 32 of a 32-row group, k chunk
+    // 2 kk + l / 32 of the stage) for k step kk, in stage buffer 0, for the wave's first A and
+    // B rows; fragment a (b) of the wave sits 32 a (32 b) rows = 4 KB further
+    const unsigned lds0 = static_cast<unsigned>(reinterpret_cast<size_t>((lds_ptr_t)(&lds[0])));
+    unsigned fa[4], fb[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+        const unsigned f = lds0 + (((lrow >> 3) * 64 + (lrow & 7) * 8 + ((2 * kk + lhalf) ^ (lrow & 7))) * 16);
+        fa[kk] = f + ((wm * TM) >> 3) * 1024;
+        fb[kk] = f + (NBA + ((wn * TN) >> 3)) * 1024;
+    }
+    // One k step: the MFMAs on fragments (ma, mb), row of tiles by row, each row preceded by
+    // the reads of another k step's fragments a and b (into ra, rb, from LDS at ra_base,
+    // rb_base) and, when kt >= 0, by two load slots of stage kt; no scheduling moves them.
+    auto step = [&](u32x4 (&ma)[FM], u32x4 (&mb)[FN], unsigned ra_base, unsigned rb_base, u32x4 (&ra)[FM],
+                    u32x4 (&rb)[FN], int kt, uint4* dst) __attribute__((always_inline)) {
+        static_for<FM>([&](auto a) __attribute__((always_inline)) {
+            ra[a] = lds_read16_at<a * 4096>(ra_base);
+            rb[a] = lds_read16_at<a * 4096>(rb_base);
+            if (kt >= 0) issue_pair(kt, dst, a);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int b = 0; b < FN; ++b)
+                acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, mb[b]),
+                                                                    __builtin_bit_cast(bf16x8, ma[a]), acc[a][b], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+        });
+    };
+    auto read_all = [&](unsigned ra_base, unsigned rb_base, u32x4 (&ra)[FM], u32x4 (&rb)[FN]) __attribute__((always_inline)) {
+        static_for<FM>([&](auto a) __attribute__((always_inline)) {
+            ra[a] = lds_read16_at<a * 4096>(ra_base);
+            rb[a] = lds_read16_at<a * 4096>(rb_base);
+        });
+    };
+    auto pin_all = [&](u32x4 (&af)[FM], u32x4 (&bf)[FN]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int a = 0; a < FM; ++a) pin(af[a]);
+#pragma unroll
+        for (int b = 0; b < FN; ++b) pin(bf[b]);
+    };
+
+    // Stage st sits in buffer st % 2.  Iteration st: wait for it, barrier, then four k steps;
+    // step kk multiplies the fragments of the step before it (step 3 of stage st - 1 for kk = 0)
+    // while it reads its own, and step 0 also loads stage st + 1 into the other buffer.
+    u32x4 f0a[FM], f0b[FN], f1a[FM], f1b[FN];
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    read_all(fa[0], fb[0], f0a, f0b);
+    lds_wait();
+    pin_all(f0a, f0b);
+    step(f0a, f0b, fa[1], fb[1], f1a, f1b, nk > 1 ? 1 : -1, &lds[STAGE]);
+    lds_wait();
+    pin_all(f1a, f1b);
+    step(f1a, f1b, fa[2], fb[2], f0a, f0b, -1, nullptr);
+    lds_wait();
+    pin_all(f0a, f0b);
+    step(f0a, f0b, fa[3], fb[3], f1a, f1b, -1, nullptr);
+    lds_wait();
+    pin_all(f1a, f1b);
+    for (int st = 1; st < nk; ++st) {
+        const int buf = st & 1;
+        const unsigned sbase = buf * STAGE * 16;
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's share of stage st has landed
+        __builtin_amdgcn_s_barrier();                      // every wave's has; stage st - 1 fully read
+        step(f1a, f1b, sbase + fa[0], sbase + fb[0], f0a, f0b, st + 1 < nk ? st + 1 : -1, &lds[(buf ^ 1) * STAGE]);
+        lds_wait();
+        pin_all(f0a, f0b);
+        step(f0a, f0b, sbase + fa[1], sbase + fb[1], f1a, f1b, -1, nullptr);
+        lds_wait();
+        pin_all(f1a, f1b);
+        step(f1a, f1b, sbase + fa[2], sbase + fb[2], f0a, f0b, -1, nullptr);
+        lds_wait();
+        pin_all(f0a, f0b);
+        step(f0a, f0b, sbase + fa[3], sbase + fb[3], f1a, f1b, -1, nullptr);
+        lds_wait();
+        pin_all(f1a, f1b);
+    }
+#pragma unroll
+    for (int a = 0; a < FM; ++a)
+#pragma unroll
+        for (int b = 0; b < FN; ++b)
+            acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, f1b[b]),
+                                                                __builtin_bit_cast(bf16x8, f1a[a]), acc[a][b], 0, 0, 0);
+
+    // --- epilogue ---------------------------------------------------------------------------
+    // Without a residual and with a bf16 output, v = act(acc) is rounded in the MFMA layout and
+    // the bf16 tile is staged in LDS in one pass; otherwise the float32 sums are staged in two
+    // passes of 128 rows and finished in 8-column chunks as gemm_kernel finishes them (residual,
+    // activation, rounding).  Either way the stores are whole 16-byte chunks along rows, and a
+    // pass reads all its residual chunks before its first store, so that no wait in the epilogue
+    // waits for a store.
+    __syncthreads();                                   // every wave is done with the operand stages
+    unsigned char* tile = reinterpret_cast<unsigned char*>(lds);
+    const int tid = threadIdx.x;
+    const T* resp = static_cast<const T*>(p.res);
+    if (!resp && !p.out_f32) {
+        // (one copy of the unrolled tile per activation: a per-element choice would evaluate
+        // every activation for all 256 values)
+        auto stage_bf16 = [&](auto act) __attribute__((always_inline)) {
+            static_for<FM>([&](auto a) __attribute__((always_inline)) {
+                static_for<FN>([&](auto b) __attribute__((always_inline)) {
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        float v[4];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) v[e] = act_f(acc_read(acc[a][b][4 * g + e]) + 0.0f, decltype(act)::value);
+                        const int row = wm * TM + a * 32 + lrow, col = wn * TN + b * 32 + g * 8 + lhalf * 4;
+                        *reinterpret_cast<bf16x4*>(tile + row * kWideRowB + col * 2) =
+                            bf16x4{(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
+                    }
+                    // one tile at a time: the accumulators are read out only when they are used
+                    __builtin_amdgcn_sched_barrier(0);
+                });
+            });
+        };
+        if (p.act == MOPAR_ACT_RELU)
+            stage_bf16(std::integral_constant<int, MOPAR_ACT_RELU>{});
+        else if (p.act == MOPAR_ACT_GELU)
+            stage_bf16(std::integral_constant<int, MOPAR_ACT_GELU>{});
+        else
+            stage_bf16(std::integral_constant<int, MOPAR_ACT_NONE>{});
+        __syncthreads();
+        T* C = static_cast<T*>(p.C);
+        for (int i = 0; i < BM / 8; ++i) {
+            const int r = i * 8 + (tid >> 5), c = (tid & 31) * 8;
+            const int m = m0 + r, n = n0 + c;
+            if (m >= Mi || n >= n_hi) continue;
+            const uint4 w = *reinterpret_cast<const uint4*>(tile + r * kWideRowB + c * 2);
+            T* dst = C + static_cast<int64_t>(m) * p.ldc + n;
+            const int nv = min(8, n_hi - n);
+            if (nv == 8 && aligned16(dst)) {
+                *reinterpret_cast<uint4*>(dst) = w;
+            } else {
+                const unsigned short* h = reinterpret_cast<const unsigned short*>(&w);
+                for (int e = 0; e < nv; ++e) reinterpret_cast<unsigned short*>(dst)[e] = h[e];
+            }
+        }
+        return;
+    }
+    constexpr int NCH = TM * BN / 8 / 256;             // 8-column chunks per thread and pass
+    const int cc = tid & 31, cr = tid >> 5;            // chunk column; first row (then every 8th)
+    const int c0 = n0 + cc * 8;
+    const int cval = max(0, min(8, n_hi - c0));
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        if (h) __syncthreads();                        // the first half's rows are all read
+        if (wm == h) {
+            static_for<FM>([&](auto a) __attribute__((always_inline)) {
+                static_for<FN>([&](auto b) __attribute__((always_inline)) {
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const int row = a * 32 + lrow, col = wn * TN + b * 32 + g * 8 + lhalf * 4;
+                        *reinterpret_cast<f32x4*>(tile + row * kWideRowF + col * 4) =
+                            f32x4{acc_read(acc[a][b][4 * g]), acc_read(acc[a][b][4 * g + 1]),
+                                  acc_read(acc[a][b][4 * g + 2]), acc_read(acc[a][b][4 * g + 3])};
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                });
+            });
+        }
+        __syncthreads();
+        Raw8<T> rraw[NCH];
+        bool rfast[NCH];
+        if (resp) {
+#pragma unroll
+            for (int i = 0; i < NCH; ++i) {
+                const int m = m0 + h * TM + cr + 8 * i;
+                const int64_t idx = static_cast<int64_t>(m) * p.ldc + c0;
+                rfast[i] = m < Mi && cval == 8 && aligned16(resp + idx);
+                rraw[i] = load_raw8<T>(rfast[i] ? resp + idx : nullptr, kZeroChunk);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < NCH; ++i) {
+            const int r = cr + 8 * i;
+            const int m = m0 + h * TM + r;
+            if (m >= Mi || cval == 0) continue;
+            float v[8], rsd[8];
+            const f32x4 lo = *reinterpret_cast<const f32x4*>(tile + r * kWideRowF + cc * 32);
+            const f32x4 hi = *reinterpret_cast<const f32x4*>(tile + r * kWideRowF + cc * 32 + 16);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = lo[e], v[4 + e] = hi[e];
+            const int64_t idx = static_cast<int64_t>(m) * p.ldc + c0;
+            if (resp && rfast[i])
+                unpack8<T>(rraw[i], rsd);
+            else
+                load8<T>(resp, idx, resp ? cval : 0, rsd);
+            if (p.act == MOPAR_ACT_NONE) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[e] = v[e] + rsd[e];
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[e] = act_f(v[e] + rsd[e], p.act);
+            }
+            if (p.out_f32)
+                store8<float>(static_cast<float*>(p.C), idx, v, cval);
+            else
+                store8<T>(static_cast<T*>(p.C), idx, v, cval);
+        }
+    }
+}
+
 // Split-K finish: sum the partials in split order, then the usual epilogue.
 template <typename T>
 __global__ void splitk_reduce_kernel(const GemmParams p) {
@@ -1106,9 +1440,45 @@ static hipError_t launch_cfg(const GemmParams& params, int width, hipStream_t st
     return hipGetLastError();
 }
 
+// 256 x 256 tiles (bf16, dense A, one split, standard epilogue)
+static hipError_t launch_wide(const GemmParams& params, int width, hipStream_t st) {
+    GemmParams p = params;
+    const int64_t mt = (p.M + 255) / 256, nt = (width + 255) / 256;
+    const int64_t total = mt * nt * p.ksub;
+    if (total >= (int64_t(1) << 31) / kGroupM) return hipErrorInvalidValue;
+    p.g_mt = static_cast<int>(mt);
+    p.g_nt = static_cast<int>(nt);
+    p.g_total = static_cast<int>(total);
+    p.g_per_xcd = static_cast<int>((total + 7) / 8);
+    p.g_cols = static_cast<int>(nt * p.ksub);
+    p.g_nk = (p.K + 63) / 64;
+    p.g_q = p.N / p.ksub;
+    p.g_rr = p.N % p.ksub;
+    p.g_div_group = FastDiv(static_cast<unsigned>(kGroupM * p.g_cols));
+    const int last = static_cast<int>(mt - (mt - 1) / kGroupM * kGroupM);
+    p.g_div_last = FastDiv(static_cast<unsigned>(last));
+    p.g_div_nt = FastDiv(static_cast<unsigned>(nt));
+    const int64_t grid = (total + 7) / 8 * 8;
+    launch_kernel(gemm_wide_kernel, dim3(static_cast<unsigned>(grid)), dim3(256), 0, st, p);
+    return hipGetLastError();
+}
+
+// Whether an operator runs on gemm_wide_kernel (and so on the 32 x 32 x 16 MFMA): dense bf16
+// with the standard epilogue, not a boundary codec layer, K of at least 256, and at least four
+// rounds of 256 x 256 tiles over the whole (M, N) -- with fewer, the block's unhidden set-up and
+// epilogue cost more than its faster K loop saves (measured).  A function of the operator's
+// (M, N, K) alone, never of the sub-slice count, so all its sub-slice launches take the same path.
+static bool wide_class(const GemmParams& p) {
+    return !p.conv && !p.thin && p.epi == EPI_STD && p.splits == 1 && p.K >= 256 && p.M >= 512 && p.N >= 512 &&
+           ((p.M + 255) / 256) * ((p.N + 255) / 256) >= 4 * kCUs;
+}
+
 template <typename T>
 static hipError_t dispatch(const GemmParams& p, hipStream_t st) {
     const int width = (p.N + p.ksub - 1) / p.ksub;   // widest sub-slice
+    if constexpr (sizeof(T) == 2) {
+        if (wide_class(p)) return launch_wide(p, width, st);
+    }
     // few rows: the four waves split K (four 64-wide sub-stages per stage) instead of the tile
     if (p.M <= 16) return launch_cfg<T, 16, 64, 1, 1, 3, 4, 4>(p, width, st);
     // the LSTM step: 32 x 16 tiles (twice the blocks of 64 x 16, less LDS each) measured

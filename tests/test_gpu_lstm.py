@@ -21,13 +21,13 @@ pytestmark = pytest.mark.gpu
 P = pytest.importorskip("paper_2404_02445_amd")
 
 
-def lstm_model(b, t, e, h, seed=3, layers=1):
+def lstm_model(b, t, e, h, seed=3, layers=1, w=0.3):
     bld = synth._Builder("lstm", "bf16", b, seed)
     ids = bld.tensor((b, t), "i32")
     bld.new_layer("L0")
     x = bld.embed(ids, b * t, e, "src", -1.0, 1.0)
     for i in range(layers):
-        x = bld.lstm(x, h, f"lstm{i}", -0.3, 0.3)
+        x = bld.lstm(x, h, f"lstm{i}", -w, w)
     return bld.finish(x, 1), np.arange(b * t, dtype=np.int32).reshape(b, t)
 
 
@@ -47,18 +47,22 @@ def canon(t):
     return t.float().cpu().numpy()
 
 
-@pytest.mark.parametrize("b,t,e,h", [
-    (37, 6, 64, 48),       # ragged batch group (37 = 2 x 16 + 5), K padded to a whole MFMA step
-    (17, 1, 16, 32),       # a single step
-    (64, 5, 128, 256),
-    (5, 9, 1024, 1024),    # the LSTM LM's hidden size: 32 weight fragments per lane
-    (3, 4, 24, 40),        # hidden size off the 16-unit tile: one GEMM per step
-    (2, 7, 8, 16),         # the smallest hidden size: one gate slice, one tile per batch group
-    (1, 4096, 8, 16),      # the longest sequence of one launch
-    (1, 4097, 8, 16),      # one step more: one GEMM per step
+@pytest.mark.parametrize("b,t,e,h,w", [
+    (37, 6, 64, 48, 0.3),       # ragged batch group (37 = 2 x 16 + 5), K padded to a whole MFMA step
+    (17, 1, 16, 32, 0.3),       # a single step
+    (64, 5, 128, 256, 0.3),
+    (5, 9, 1024, 1024, 0.3),    # the LSTM LM's hidden size: 32 weight fragments per lane
+    (3, 4, 24, 40, 0.3),        # hidden size off the 16-unit tile: one GEMM per step
+    (2, 7, 8, 16, 0.3),         # the smallest hidden size: one gate slice, one tile per batch group
+    (1, 4096, 8, 16, 0.3),      # the longest sequence of one launch
+    (1, 4097, 8, 16, 0.3),      # one step more: one GEMM per step
+    # the input projection (16384 x 256 x 4096, float32 out) on 256 x 256 tiles; recurrent weights
+    # small enough that the 1024-step recurrence contracts (with weights of +-0.3 at this hidden
+    # size it is chaotic, and rounding differences grow until any two implementations disagree)
+    (16, 1024, 256, 1024, 0.03),
 ])
-def test_lstm_recurrence_parity(b, t, e, h):
-    m, ids = lstm_model(b, t, e, h)
+def test_lstm_recurrence_parity(b, t, e, h, w):
+    m, ids = lstm_model(b, t, e, h, w=w)
     y, _ = forward(m, ids)
     torch.cuda.synchronize()
     assert rel_err(canon(y), oracle.forward(m, ids)) <= TOL["bf16"]

@@ -157,6 +157,12 @@ def seq_ids(b, s):
     # M = 40: the 64x64 and 64x16 K-split tiles (k = 1 vs k = 4) must agree bit for bit
     ("bf16", 5, 8, 1504, 70, "gelu", True, 4),
     ("f32", 4, 4, 700, 33, "none", True, 2),
+    # products with at least 1024 tiles of 256 x 256 run on the 32 x 32 MFMA kernel, every
+    # sub-slice launch included: 8192 x 256 x 8192 against 1024-column sub-slices
+    ("bf16", 16, 512, 256, 8192, "none", False, 8),
+    # ragged M (33 tile rows), N and K (312 = 4 x 64 + 56) with residual and GELU, against
+    # 500-column sub-slices
+    ("bf16", 3, 2743, 312, 8000, "gelu", True, 16),
 ])
 def test_linear_parity_and_subslice_bitwise(dt, b, s, k, nout, act, res, ksub):
     bld, x = seq_input_model(dt, b, s, k)
