@@ -835,6 +835,7 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
 // (M, N, K) puts it here runs here for every sub-slice launch, and every output element sees the
 // same operations in the same order whatever the sub-slice count.
 constexpr int kWideRowB = 256 * 2 + 16, kWideRowF = 256 * 4 + 16;   // staged output row strides, bytes
+constexpr int kWideBStages = 2;                                      // B stages in LDS
 // An accumulator read out where it is used (left to itself the compiler copies many accumulator
 // tiles to ordinary registers at once, and spills them)
 __device__ __forceinline__ float acc_read(float a) {
@@ -843,18 +844,23 @@ __device__ __forceinline__ float acc_read(float a) {
     return v;
 }
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+template <int NB>
 __global__ __launch_bounds__(256, 1) void gemm_wide_kernel(const GemmParams p) {
     using T = __bf16;
     constexpr int BM = 256, BN = 256, TM = 128, TN = 128;
     constexpr int FM = TM / 32, FN = TN / 32;   // 32 x 32 MFMA tiles per wave
-    constexpr int NBA = BM / 8, NBB = BN / 8;   // 1 KB blocks (8 rows x 128 bytes) per stage
+    constexpr int NBA = BM / 8, NBB = BN / 8;   // 1 KB blocks (8 rows x 128 bytes) per operand stage
     constexpr int NW = 4;
     constexpr int LA = NBA / NW, LB = NBB / NW; // load slots per wave (8 + 8)
-    constexpr int STAGE = (NBA + NBB) * 64;     // uint4 per stage
+    constexpr int SA = NBA * 64, SB = NBB * 64; // uint4 per A stage and per B stage (32 KB each)
     constexpr int BK = 64;
-    // the epilogue's staged tile: 256 rows of bf16 or 128 rows of float32, rows padded by 16 bytes
+    static_assert(NB == 2 || NB == 3, "B stages in LDS");
+    // LDS: two A stages, then NB B stages; the epilogue's staged tile (256 rows of bf16 or 128 rows
+    // of float32, rows padded by 16 bytes) reuses the space
+    constexpr int OPS_U4 = 2 * SA + NB * SB;
     constexpr int TILE_U4 = (BM * kWideRowB > TM * kWideRowF ? BM * kWideRowB : TM * kWideRowF) / 16;
-    __shared__ uint4 lds[2 * STAGE > TILE_U4 ? 2 * STAGE : TILE_U4];
+    __shared__ uint4 lds[OPS_U4 > TILE_U4 ? OPS_U4 : TILE_U4];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -898,15 +904,26 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_kernel(const GemmParams p) {
         voffB[i] = static_cast<unsigned>(nc) * static_cast<unsigned>(p.K * sizeof(T)) + static_cast<unsigned>(cl * 16);
     }
     const int ktail = (p.K % BK) ? nk - 1 : nk;
-    // load slots 2 i and 2 i + 1 (A blocks wave + 4 s, B blocks wave + 4 s) of stage kt into LDS at dst
-    auto issue_pair = [&](int kt, uint4* dst, int i) __attribute__((always_inline)) {
+    uint4* const ldsA = &lds[0];
+    uint4* const ldsB = &lds[2 * SA];
+    // Load slots 2 i, 2 i + 1 of operand X's stage kt into LDS stage buffer buf.  A stage past
+    // the last one re-reads the last one (into a buffer nobody reads), so that every iteration
+    // issues the same loads and the wait counts stay exact.
+    auto issue_a = [&](int kt, int buf, int i) __attribute__((always_inline)) {
+        kt = kt < nk ? kt : nk - 1;
         const unsigned soff = static_cast<unsigned>(kt) * (BK * sizeof(T));
         const bool kin = kt != ktail || kt * BK + cl * 8 < p.K;
 #pragma unroll
-        for (int s2 = 2 * i; s2 < 2 * i + 2; ++s2) {
-            buffer_load_lds(p.A, p.a_bytes, (lds_ptr_t)(dst + (wave + NW * s2) * 64), kin ? voffA[s2] : kOOB, soff);
-            buffer_load_lds(p.B, p.b_bytes, (lds_ptr_t)(dst + (NBA + wave + NW * s2) * 64), kin ? voffB[s2] : kOOB, soff);
-        }
+        for (int s2 = 2 * i; s2 < 2 * i + 2; ++s2)
+            buffer_load_lds(p.A, p.a_bytes, (lds_ptr_t)(ldsA + buf * SA + (wave + NW * s2) * 64), kin ? voffA[s2] : kOOB, soff);
+    };
+    auto issue_b = [&](int kt, int buf, int i) __attribute__((always_inline)) {
+        kt = kt < nk ? kt : nk - 1;
+        const unsigned soff = static_cast<unsigned>(kt) * (BK * sizeof(T));
+        const bool kin = kt != ktail || kt * BK + cl * 8 < p.K;
+#pragma unroll
+        for (int s2 = 2 * i; s2 < 2 * i + 2; ++s2)
+            buffer_load_lds(p.B, p.b_bytes, (lds_ptr_t)(ldsB + buf * SB + (wave + NW * s2) * 64), kin ? voffB[s2] : kOOB, soff);
     };
     static_assert(LA == LB && LA == 2 * FM, "two load slots per row of fragments");
 
@@ -935,7 +952,10 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_kernel(const GemmParams p) {
             for (int e = 0; e < 4; ++e) bslow[b][g][e] = bv[e] + b2v[e];
         }
 
-    static_for<FM>([&](auto i) __attribute__((always_inline)) { issue_pair(0, &lds[0], i); });
+    // prologue: B stage 0, A stage 0 and, with three B buffers, B stage 1
+    static_for<FM>([&](auto i) __attribute__((always_inline)) { issue_b(0, 0, i); });
+    static_for<FM>([&](auto i) __attribute__((always_inline)) { issue_a(0, 0, i); });
+    if constexpr (NB == 3) static_for<FM>([&](auto i) __attribute__((always_inline)) { issue_b(1, 1, i); });
 
     f32x16 acc[FM][FN];
 #pragma unroll
@@ -953,26 +973,35 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_kernel(const GemmParams p) {
                 for (int e = 0; e < 4; ++e) acc[a][b][4 * g + e] = fast ? bv[e] + b2v[e] : bslow[b][g][e];
         }
 
-    // LDS byte address of this lane's fragment (row l % 32 of a 32-row group, k chunk
-    // 2 kk + l / 32 of the stage) for k step kk, in stage buffer 0, for the wave's first A and
-    // B rows; fragment a (b) of the wave sits 32 a (32 b) rows = 4 KB further
-    const unsigned lds0 = static_cast<unsigned>(reinterpret_cast<size_t>((lds_ptr_t)(&lds[0])));
+    // LDS byte offset of this lane's fragment (row l % 32 of a 32-row group, k chunk 2 kk + l / 32
+    // of the stage) for k step kk, within stage buffer 0 of A (fa) and of B (fb), for the wave's
+    // first rows; fragment a (b) of the wave sits 32 a (32 b) rows = 4 KB further
+    const unsigned ldsa0 = static_cast<unsigned>(reinterpret_cast<size_t>((lds_ptr_t)ldsA));
+    const unsigned ldsb0 = static_cast<unsigned>(reinterpret_cast<size_t>((lds_ptr_t)ldsB));
     unsigned fa[4], fb[4];
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-        const unsigned f = lds0 + (((lrow >> 3) * 64 + (lrow & 7) * 8 + ((2 * kk + lhalf) ^ (lrow & 7))) * 16);
-        fa[kk] = f + ((wm * TM) >> 3) * 1024;
-        fb[kk] = f + (NBA + ((wn * TN) >> 3)) * 1024;
+        const unsigned f = ((lrow >> 3) * 64 + (lrow & 7) * 8 + ((2 * kk + lhalf) ^ (lrow & 7))) * 16;
+        fa[kk] = ldsa0 + f + ((wm * TM) >> 3) * 1024;
+        fb[kk] = ldsb0 + f + ((wn * TN) >> 3) * 1024;
     }
     // One k step: the MFMAs on fragments (ma, mb), row of tiles by row, each row preceded by
     // the reads of another k step's fragments a and b (into ra, rb, from LDS at ra_base,
-    // rb_base) and, when kt >= 0, by two load slots of stage kt; no scheduling moves them.
+    // rb_base) and, when kt >= 0, by load slots: rows 0 and 1 load A stage kt + 1 into A buffer
+    // (kt + 1) % 2, rows 2 and 3 load B stage kt + NB - 1 into B buffer (kt + NB - 1) % NB (the
+    // B loads go out last, so that a wait for all but them covers the A loads).  Nothing is
+    // scheduled across the rows.
     auto step = [&](u32x4 (&ma)[FM], u32x4 (&mb)[FN], unsigned ra_base, unsigned rb_base, u32x4 (&ra)[FM],
-                    u32x4 (&rb)[FN], int kt, uint4* dst) __attribute__((always_inline)) {
+                    u32x4 (&rb)[FN], int kt, int bbuf_next) __attribute__((always_inline)) {
         static_for<FM>([&](auto a) __attribute__((always_inline)) {
             ra[a] = lds_read16_at<a * 4096>(ra_base);
             rb[a] = lds_read16_at<a * 4096>(rb_base);
-            if (kt >= 0) issue_pair(kt, dst, a);
+            if (kt >= 0) {
+                if constexpr (a < 2)
+                    issue_a(kt + 1, (kt + 1) & 1, 2 * a), issue_a(kt + 1, (kt + 1) & 1, 2 * a + 1);
+                else
+                    issue_b(kt + NB - 1, bbuf_next, 2 * (a - 2)), issue_b(kt + NB - 1, bbuf_next, 2 * (a - 2) + 1);
+            }
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int b = 0; b < FN; ++b)
@@ -993,40 +1022,51 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_kernel(const GemmParams p) {
 #pragma unroll
         for (int b = 0; b < FN; ++b) pin(bf[b]);
     };
+    // wait until this wave's loads of A stage st and B stage st have landed: with three B
+    // buffers the eight B loads issued last (B stage st + 1) may still be in flight
+    auto wait_stage = [&]() __attribute__((always_inline)) {
+        if constexpr (NB == 3)
+            asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+        else
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    };
 
-    // Stage st sits in buffer st % 2.  Iteration st: wait for it, barrier, then four k steps;
-    // step kk multiplies the fragments of the step before it (step 3 of stage st - 1 for kk = 0)
-    // while it reads its own, and step 0 also loads stage st + 1 into the other buffer.
+    // Stage st sits in A buffer st % 2 and B buffer st % NB.  Iteration st: wait for it, barrier
+    // (every wave's share has landed; stage st - 1 is fully read), then four k steps; step kk
+    // multiplies the fragments of the step before it (step 3 of stage st - 1 for kk = 0) while it
+    // reads its own, and step 0 also loads A stage st + 1 and B stage st + NB - 1.
     u32x4 f0a[FM], f0b[FN], f1a[FM], f1b[FN];
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    wait_stage();
     __builtin_amdgcn_s_barrier();
     read_all(fa[0], fb[0], f0a, f0b);
     lds_wait();
     pin_all(f0a, f0b);
-    step(f0a, f0b, fa[1], fb[1], f1a, f1b, nk > 1 ? 1 : -1, &lds[STAGE]);
+    step(f0a, f0b, fa[1], fb[1], f1a, f1b, 0, (NB - 1) % NB);
     lds_wait();
     pin_all(f1a, f1b);
-    step(f1a, f1b, fa[2], fb[2], f0a, f0b, -1, nullptr);
+    step(f1a, f1b, fa[2], fb[2], f0a, f0b, -1, 0);
     lds_wait();
     pin_all(f0a, f0b);
-    step(f0a, f0b, fa[3], fb[3], f1a, f1b, -1, nullptr);
+    step(f0a, f0b, fa[3], fb[3], f1a, f1b, -1, 0);
     lds_wait();
     pin_all(f1a, f1b);
+    int bcur = 0;                                      // B buffer of stage st
     for (int st = 1; st < nk; ++st) {
-        const int buf = st & 1;
-        const unsigned sbase = buf * STAGE * 16;
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's share of stage st has landed
-        __builtin_amdgcn_s_barrier();                      // every wave's has; stage st - 1 fully read
-        step(f1a, f1b, sbase + fa[0], sbase + fb[0], f0a, f0b, st + 1 < nk ? st + 1 : -1, &lds[(buf ^ 1) * STAGE]);
+        bcur = bcur == NB - 1 ? 0 : bcur + 1;
+        const int bnext = bcur == 0 ? NB - 1 : bcur - 1;   // (st + NB - 1) % NB: stage st - 1's buffer
+        const unsigned abase = (st & 1) * SA * 16, bbase = bcur * SB * 16;
+        wait_stage();                                  // this wave's share of stage st has landed
+        __builtin_amdgcn_s_barrier();                  // every wave's has; stage st - 1 fully read
+        step(f1a, f1b, abase + fa[0], bbase + fb[0], f0a, f0b, st, bnext);
         lds_wait();
         pin_all(f0a, f0b);
-        step(f0a, f0b, sbase + fa[1], sbase + fb[1], f1a, f1b, -1, nullptr);
+        step(f0a, f0b, abase + fa[1], bbase + fb[1], f1a, f1b, -1, 0);
         lds_wait();
         pin_all(f1a, f1b);
-        step(f1a, f1b, sbase + fa[2], sbase + fb[2], f0a, f0b, -1, nullptr);
+        step(f1a, f1b, abase + fa[2], bbase + fb[2], f0a, f0b, -1, 0);
         lds_wait();
         pin_all(f0a, f0b);
-        step(f0a, f0b, sbase + fa[3], sbase + fb[3], f1a, f1b, -1, nullptr);
+        step(f0a, f0b, abase + fa[3], bbase + fb[3], f1a, f1b, -1, 0);
         lds_wait();
         pin_all(f1a, f1b);
     }
@@ -1036,6 +1076,7 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_kernel(const GemmParams p) {
         for (int b = 0; b < FN; ++b)
             acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, f1b[b]),
                                                                 __builtin_bit_cast(bf16x8, f1a[a]), acc[a][b], 0, 0, 0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the last (unread) loads land before LDS is reused
 
     // --- epilogue ---------------------------------------------------------------------------
     // Without a residual and with a bf16 output, v = act(acc) is rounded in the MFMA layout and
@@ -1152,6 +1193,379 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_kernel(const GemmParams p) {
             else
                 store8<T>(static_cast<T*>(p.C), idx, v, cval);
         }
+    }
+}
+
+// Persistent form of gemm_wide_kernel, used when the launch brings tile counters (one word per
+// XCD, zeroed by the launcher before the launch): one block per CU, fed from a queue.  The blocks
+// of XCD x take x's run of tiles, first one each by block index, then from x's counter, so that a
+// block whose CU is busy with another stream's kernel when the launch starts takes fewer tiles,
+// and the blocks an XCD runs together still work on neighbouring tiles.  Per tile the MFMA
+// arithmetic is gemm_wide_kernel's.  What changes is the hand-over between tiles: the next
+// tile's number is fetched while the current tile's first stage runs, its first stage is loaded
+// during the current tile's last stage, its bias while the current tile is stored, and the
+// epilogue stores straight from the accumulators (one store per group of four columns, an
+// out-of-range offset for the groups that are not written, so that every tile issues the same
+// number of stores and the next tile waits for its first stage without waiting for them).  It
+// takes products without a residual or an activation (the others run on gemm_wide_kernel).
+__global__ __launch_bounds__(256, 1) void gemm_wide_persistent(const GemmParams p) {
+    using T = __bf16;
+    constexpr int BM = 256, BN = 256, TM = 128, TN = 128;
+    constexpr int FM = TM / 32, FN = TN / 32;
+    constexpr int NBA = BM / 8, NBB = BN / 8;
+    constexpr int NW = 4;
+    constexpr int LA = NBA / NW, LB = NBB / NW;
+    constexpr int SA = NBA * 64, SB = NBB * 64;
+    constexpr int BK = 64;
+    constexpr int NSTORE = FM * FN * 4;          // stores per lane and tile (regular tiles)
+    static_assert(LA == LB && LA == 2 * FM, "two load slots per row of fragments");
+    static_assert(NSTORE == 64, "the first-stage wait below lets 63 stores stay in flight");
+    __shared__ uint4 lds[2 * SA + 2 * SB];
+    __shared__ int s_ticket;
+    __shared__ __attribute__((aligned(16))) float s_bias[BN];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wm = wave >> 1, wn = wave & 1;
+    const int lrow = lane & 31, lhalf = lane >> 5;
+    touch_kernargs<sizeof(GemmParams)>();
+
+    const int xcd = blockIdx.x & 7, gx = static_cast<int>(gridDim.x >> 3);
+    const int t_lo = xcd * p.g_per_xcd;
+    const int cx = min(p.g_per_xcd, p.g_total - t_lo);   // tiles of this XCD's run
+    unsigned* const ctr = p.wide_ctr + xcd;
+    const int Mi = static_cast<int>(p.M);
+    const int nk = p.g_nk;                               // >= 2 (checked at launch)
+    const int ktail = (p.K % BK) ? nk - 1 : nk;
+    const int cl = (lane & 7) ^ (lane >> 3);
+
+    // tile li of this XCD's run -> rows m0.., columns n0 .. n_hi - 1; false when the tile lies
+    // past a narrower sub-slice's last column
+    auto decode = [&](int li, int& m0, int& n0, int& n_hi) __attribute__((always_inline)) -> bool {
+        const unsigned t = static_cast<unsigned>(t_lo + li);
+        constexpr int GM = kGroupM;
+        const unsigned group = p.g_div_group.div(t);
+        const unsigned within = t - group * static_cast<unsigned>(GM * p.g_cols);
+        const bool last = static_cast<int>(group) == (p.g_mt - 1) / GM;
+        const unsigned gm = last ? static_cast<unsigned>(p.g_mt - group * GM) : GM;
+        const unsigned colu = last ? p.g_div_last.div(within) : within / GM;
+        const int mti = static_cast<int>(group * GM + (within - colu * gm));
+        const unsigned c1 = p.g_div_nt.div(colu);
+        const int nti = static_cast<int>(colu - c1 * static_cast<unsigned>(p.g_nt));
+        const int j = static_cast<int>(c1);
+        const int n_lo = j * p.g_q + min(j, p.g_rr);
+        n_hi = (j + 1) * p.g_q + min(j + 1, p.g_rr);
+        n0 = n_lo + nti * BN;
+        m0 = mti * BM;
+        return n0 < n_hi;
+    };
+    // one more tile number from the queue, the same for every thread of the block
+    auto fetch_now = [&]() __attribute__((always_inline)) -> int {
+        if (threadIdx.x == 0) s_ticket = gx + static_cast<int>(__hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+        __syncthreads();
+        const int v = __builtin_amdgcn_readfirstlane(s_ticket);
+        __syncthreads();
+        return v;
+    };
+    auto offsets = [&](int m0, int n0, int n_hi, unsigned (&va)[LA], unsigned (&vb)[LB]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < LA; ++i) {
+            const int m = m0 + (wave + NW * i) * 8 + (lane >> 3);
+            const int mc = m < Mi ? m : Mi - 1;
+            va[i] = static_cast<unsigned>(mc) * static_cast<unsigned>(p.lda * sizeof(T)) + static_cast<unsigned>(cl * 16);
+        }
+#pragma unroll
+        for (int i = 0; i < LB; ++i) {
+            const int n = n0 + (wave + NW * i) * 8 + (lane >> 3);
+            const int nc = n < n_hi ? n : n_hi - 1;
+            vb[i] = static_cast<unsigned>(nc) * static_cast<unsigned>(p.K * sizeof(T)) + static_cast<unsigned>(cl * 16);
+        }
+    };
+    uint4* const ldsA = &lds[0];
+    uint4* const ldsB = &lds[2 * SA];
+    // load slots 4 r .. 4 r + 3 of one operand's stage kt (clamped to the last stage) into buffer buf
+    auto load_a = [&](const unsigned (&va)[LA], int kt, int buf, int r) __attribute__((always_inline)) {
+        kt = kt < nk ? kt : nk - 1;
+        const unsigned soff = static_cast<unsigned>(kt) * (BK * sizeof(T));
+        const bool kin = kt != ktail || kt * BK + cl * 8 < p.K;
+#pragma unroll
+        for (int s2 = 4 * r; s2 < 4 * r + 4; ++s2)
+            buffer_load_lds(p.A, p.a_bytes, (lds_ptr_t)(ldsA + buf * SA + (wave + NW * s2) * 64), kin ? va[s2] : kOOB, soff);
+    };
+    auto load_b = [&](const unsigned (&vb)[LB], int kt, int buf, int r) __attribute__((always_inline)) {
+        kt = kt < nk ? kt : nk - 1;
+        const unsigned soff = static_cast<unsigned>(kt) * (BK * sizeof(T));
+        const bool kin = kt != ktail || kt * BK + cl * 8 < p.K;
+#pragma unroll
+        for (int s2 = 4 * r; s2 < 4 * r + 4; ++s2)
+            buffer_load_lds(p.B, p.b_bytes, (lds_ptr_t)(ldsB + buf * SB + (wave + NW * s2) * 64), kin ? vb[s2] : kOOB, soff);
+    };
+    // Bias + second bias of a tile: thread t reads column n0 + t (zero past n_hi) and the sums go
+    // through LDS (s_bias), from which every wave starts its accumulators -- the same float
+    // additions as gemm_kernel's, per column.
+    const T* biasp = static_cast<const T*>(p.bias);
+    const T* bias2p = static_cast<const T*>(p.bias2);
+    auto bias_col = [&](int n0, int n_hi, float& bv, float& b2v) __attribute__((always_inline)) {
+        const int n = n0 + static_cast<int>(threadIdx.x);
+        bv = (biasp && n < n_hi) ? ld_f(biasp, n) : 0.0f;
+        b2v = (bias2p && n < n_hi) ? ld_f(bias2p, n) : 0.0f;
+    };
+    f32x16 acc[FM][FN];
+    auto bias_init = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int b = 0; b < FN; ++b)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const f32x4 bsum = *reinterpret_cast<const f32x4*>(&s_bias[wn * TN + b * 32 + g * 8 + lhalf * 4]);
+#pragma unroll
+                for (int a = 0; a < FM; ++a)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) acc[a][b][4 * g + e] = bsum[e];
+            }
+    };
+
+    const unsigned ldsa0 = static_cast<unsigned>(reinterpret_cast<size_t>((lds_ptr_t)ldsA));
+    const unsigned ldsb0 = static_cast<unsigned>(reinterpret_cast<size_t>((lds_ptr_t)ldsB));
+    unsigned fa[4], fb[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+        const unsigned f = ((lrow >> 3) * 64 + (lrow & 7) * 8 + ((2 * kk + lhalf) ^ (lrow & 7))) * 16;
+        fa[kk] = ldsa0 + f + ((wm * TM) >> 3) * 1024;
+        fb[kk] = ldsb0 + f + ((wn * TN) >> 3) * 1024;
+    }
+    // one k step: MFMAs on (ma, mb) row by row, each row preceded by the reads of the next k step's
+    // fragments and by loads(a)
+    auto step = [&](u32x4 (&ma)[FM], u32x4 (&mb)[FN], unsigned ra_base, unsigned rb_base, u32x4 (&ra)[FM],
+                    u32x4 (&rb_)[FN], auto&& loads) __attribute__((always_inline)) {
+        static_for<FM>([&](auto a) __attribute__((always_inline)) {
+            ra[a] = lds_read16_at<a * 4096>(ra_base);
+            rb_[a] = lds_read16_at<a * 4096>(rb_base);
+            loads(a);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int b = 0; b < FN; ++b)
+                acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, mb[b]),
+                                                                    __builtin_bit_cast(bf16x8, ma[a]), acc[a][b], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+        });
+    };
+    auto no_loads = [](int) __attribute__((always_inline)) {};
+    auto pin_all = [&](u32x4 (&af)[FM], u32x4 (&bf)[FN]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int a = 0; a < FM; ++a) pin(af[a]);
+#pragma unroll
+        for (int b = 0; b < FN; ++b) pin(bf[b]);
+    };
+
+    // --- first tile -------------------------------------------------------------------------
+    int li = static_cast<int>(blockIdx.x >> 3);
+    int m0 = 0, n0 = 0, n_hi = 0;
+    for (;;) {                                          // (block-uniform)
+        if (li >= cx) return;
+        if (decode(li, m0, n0, n_hi)) break;
+        li = fetch_now();
+    }
+    unsigned va[LA], vb[LB];
+    offsets(m0, n0, n_hi, va, vb);
+    int par = 0;                                        // stage s of the tile sits in buffers (par + s) & 1
+    {
+        float bv, b2v;
+        bias_col(n0, n_hi, bv, b2v);
+        s_bias[threadIdx.x] = bv + b2v;
+    }
+#pragma unroll
+    for (int r = 0; r < 2; ++r) load_b(vb, 0, 0, r);
+#pragma unroll
+    for (int r = 0; r < 2; ++r) load_a(va, 0, 0, r);
+    bool wait_all = true;                               // the first stage's loads are the newest in flight
+
+    const uint32_t esz = p.out_f32 ? 4u : 2u;
+    const __amdgpu_buffer_rsrc_t crs = __builtin_amdgcn_make_buffer_rsrc(p.C, static_cast<short>(0),
+                                                                         static_cast<int>(p.c_bytes), kRsrcWord3);
+    const bool c_aligned = (reinterpret_cast<uintptr_t>(p.C) & (4 * esz - 1)) == 0 && (p.ldc & 3) == 0;
+
+    for (;;) {
+        u32x4 f0a[FM], f0b[FN], f1a[FM], f1b[FN];
+        int li_next = cx;                               // the next tile (>= cx: none)
+        int m0n = 0, n0n = 0, n_hin = 0;
+        bool next_ok = false;
+        unsigned van[LA], vbn[LB];
+        int ticket_v = 0;
+        float nbv = 0.0f, nb2v = 0.0f;                  // the next tile's bias column
+        auto take_ticket = [&]() __attribute__((always_inline)) {
+            // (the ticket's load was issued in stage 0; this wait is the stage wait's)
+            if (threadIdx.x == 0) s_ticket = ticket_v;
+        };
+        auto read_ticket = [&]() __attribute__((always_inline)) {
+            li_next = __builtin_amdgcn_readfirstlane(s_ticket);
+            next_ok = li_next < cx && decode(li_next, m0n, n0n, n_hin);
+            if (next_ok) offsets(m0n, n0n, n_hin, van, vbn);
+        };
+
+        // stage 0
+        if (wait_all)
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        else
+            asm volatile("s_waitcnt vmcnt(63)" ::: "memory");
+        __builtin_amdgcn_s_barrier();                  // (also: s_bias holds this tile's bias)
+        bias_init();
+        {
+            const unsigned ab = (par & 1) * SA * 16, bb = (par & 1) * SB * 16;
+            const int nb = (par + 1) & 1;
+            if (threadIdx.x == 0)
+                ticket_v = gx + static_cast<int>(__hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+            static_for<FM>([&](auto a) __attribute__((always_inline)) {
+                f0a[a] = lds_read16_at<a * 4096>(ab + fa[0]);
+                f0b[a] = lds_read16_at<a * 4096>(bb + fb[0]);
+            });
+            lds_wait();
+            pin_all(f0a, f0b);
+            auto ld1 = [&](auto a) __attribute__((always_inline)) {
+                if constexpr (a < 2) load_a(va, 1, nb, a); else load_b(vb, 1, nb, a - 2);
+            };
+            step(f0a, f0b, ab + fa[1], bb + fb[1], f1a, f1b, ld1);
+            lds_wait();
+            pin_all(f1a, f1b);
+            step(f1a, f1b, ab + fa[2], bb + fb[2], f0a, f0b, no_loads);
+            lds_wait();
+            pin_all(f0a, f0b);
+            step(f0a, f0b, ab + fa[3], bb + fb[3], f1a, f1b, no_loads);
+            lds_wait();
+            pin_all(f1a, f1b);
+        }
+        // stages 1 .. nk - 2: this tile's next stage
+        for (int st = 1; st < nk - 1; ++st) {
+            const int buf = (par + st) & 1;
+            const unsigned ab = buf * SA * 16, bb = buf * SB * 16;
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            if (st == 1) take_ticket();
+            __builtin_amdgcn_s_barrier();
+            if (st == 1) read_ticket();
+            auto ldn = [&](auto a) __attribute__((always_inline)) {
+                if constexpr (a < 2) load_a(va, st + 1, buf ^ 1, a); else load_b(vb, st + 1, buf ^ 1, a - 2);
+            };
+            step(f1a, f1b, ab + fa[0], bb + fb[0], f0a, f0b, ldn);
+            lds_wait();
+            pin_all(f0a, f0b);
+            step(f0a, f0b, ab + fa[1], bb + fb[1], f1a, f1b, no_loads);
+            lds_wait();
+            pin_all(f1a, f1b);
+            step(f1a, f1b, ab + fa[2], bb + fb[2], f0a, f0b, no_loads);
+            lds_wait();
+            pin_all(f0a, f0b);
+            step(f0a, f0b, ab + fa[3], bb + fb[3], f1a, f1b, no_loads);
+            lds_wait();
+            pin_all(f1a, f1b);
+        }
+        // last stage: the next tile's first stage (or, without one, this stage again, unread)
+        {
+            const int buf = (par + nk - 1) & 1;
+            const unsigned ab = buf * SA * 16, bb = buf * SB * 16;
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            if (nk == 2) take_ticket();
+            __builtin_amdgcn_s_barrier();
+            if (nk == 2) read_ticket();
+            if (next_ok) bias_col(n0n, n_hin, nbv, nb2v);  // used in the epilogue
+            auto ldx = [&](auto a) __attribute__((always_inline)) {
+                if (next_ok) {
+                    if constexpr (a < 2) load_a(van, 0, buf ^ 1, a); else load_b(vbn, 0, buf ^ 1, a - 2);
+                } else {
+                    if constexpr (a < 2) load_a(va, nk - 1, buf ^ 1, a); else load_b(vb, nk - 1, buf ^ 1, a - 2);
+                }
+            };
+            step(f1a, f1b, ab + fa[0], bb + fb[0], f0a, f0b, ldx);
+            lds_wait();
+            pin_all(f0a, f0b);
+            step(f0a, f0b, ab + fa[1], bb + fb[1], f1a, f1b, no_loads);
+            lds_wait();
+            pin_all(f1a, f1b);
+            step(f1a, f1b, ab + fa[2], bb + fb[2], f0a, f0b, no_loads);
+            lds_wait();
+            pin_all(f0a, f0b);
+            step(f0a, f0b, ab + fa[3], bb + fb[3], f1a, f1b, no_loads);
+            lds_wait();
+            pin_all(f1a, f1b);
+        }
+#pragma unroll
+        for (int a = 0; a < FM; ++a)
+#pragma unroll
+            for (int b = 0; b < FN; ++b)
+                acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, f1b[b]),
+                                                                    __builtin_bit_cast(bf16x8, f1a[a]), acc[a][b], 0, 0, 0);
+
+        // --- epilogue of this tile ---------------------------------------------------------
+        // (every wave has read the bias of this tile long ago: s_bias takes the next one's)
+        if (next_ok) s_bias[threadIdx.x] = nbv + nb2v;
+        // a tile is regular when every group of four columns is whole or absent and aligned:
+        // then one 8-byte (bf16) or 16-byte (float32) store per group, else one per element
+        const bool regular = c_aligned && (n0 & 3) == 0 && (n_hi & 3) == 0;
+        static_for<FM>([&](auto a) __attribute__((always_inline)) {
+            static_for<FN>([&](auto b) __attribute__((always_inline)) {
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int m = m0 + wm * TM + a * 32 + lrow;
+                    const int n = n0 + wn * TN + b * 32 + g * 8 + lhalf * 4;
+                    const int nv = m < Mi ? max(0, min(4, n_hi - n)) : 0;
+                    const unsigned off = (static_cast<unsigned>(m) * static_cast<unsigned>(p.ldc) + static_cast<unsigned>(n)) * esz;
+                    float v[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] = acc_read(acc[a][b][4 * g + e]) + 0.0f;
+                    if (regular) {
+                        const unsigned o = nv == 4 ? off : kOOB;
+                        if (p.out_f32) {
+                            __builtin_amdgcn_raw_buffer_store_b128(u32x4{__float_as_uint(v[0]), __float_as_uint(v[1]),
+                                                                         __float_as_uint(v[2]), __float_as_uint(v[3])},
+                                                                   crs, static_cast<int>(o), 0, 0);
+                        } else {
+                            const bf16x4 h = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
+                            __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, h), crs, static_cast<int>(o), 0, 0);
+                        }
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const unsigned o = e < nv ? off + e * esz : kOOB;
+                            if (p.out_f32)
+                                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v[e]), crs, static_cast<int>(o), 0, 0);
+                            else
+                                __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, (__bf16)v[e]),
+                                                                      crs, static_cast<int>(o), 0, 0);
+                        }
+                    }
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            });
+        });
+
+        // --- the next tile -------------------------------------------------------------------
+        if (next_ok) {
+            m0 = m0n, n0 = n0n, n_hi = n_hin;
+#pragma unroll
+            for (int i = 0; i < LA; ++i) va[i] = van[i], vb[i] = vbn[i];
+            par = (par + nk) & 1;
+            // its first stage went out before this tile's 64 stores (irregular tiles issue more)
+            wait_all = !regular;
+            continue;
+        }
+        // no prefetched tile: take numbers until one is not empty (or the run is done)
+        li = li_next;
+        for (;;) {
+            if (li >= cx) return;
+            if (decode(li, m0, n0, n_hi)) break;
+            li = fetch_now();
+        }
+        offsets(m0, n0, n_hi, va, vb);
+        par = 0;
+        __syncthreads();                                // every wave is done with both buffers
+        {
+            float bv, b2v;
+            bias_col(n0, n_hi, bv, b2v);
+            s_bias[threadIdx.x] = bv + b2v;
+        }
+#pragma unroll
+        for (int r = 0; r < 2; ++r) load_b(vb, 0, 0, r);
+#pragma unroll
+        for (int r = 0; r < 2; ++r) load_a(va, 0, 0, r);
+        wait_all = true;
     }
 }
 
@@ -1443,6 +1857,7 @@ static hipError_t launch_cfg(const GemmParams& params, int width, hipStream_t st
 // 256 x 256 tiles (bf16, dense A, one split, standard epilogue)
 static hipError_t launch_wide(const GemmParams& params, int width, hipStream_t st) {
     GemmParams p = params;
+    p.c_bytes = static_cast<uint32_t>(((p.M - 1) * p.ldc + p.N) * (p.out_f32 ? 4 : 2));
     const int64_t mt = (p.M + 255) / 256, nt = (width + 255) / 256;
     const int64_t total = mt * nt * p.ksub;
     if (total >= (int64_t(1) << 31) / kGroupM) return hipErrorInvalidValue;
@@ -1458,8 +1873,16 @@ static hipError_t launch_wide(const GemmParams& params, int width, hipStream_t s
     const int last = static_cast<int>(mt - (mt - 1) / kGroupM * kGroupM);
     p.g_div_last = FastDiv(static_cast<unsigned>(last));
     p.g_div_nt = FastDiv(static_cast<unsigned>(nt));
+    if (p.wide_ctr && !p.res && p.act == MOPAR_ACT_NONE) {
+        // persistent: one block per CU, tiles from per-XCD counters zeroed here
+        if (p.g_nk < 2) return hipErrorInvalidValue;
+        const hipError_t e = launch_fill_zero(p.wide_ctr, kWideCtrBytes, st);
+        if (e != hipSuccess) return e;
+        launch_kernel(gemm_wide_persistent, dim3(static_cast<unsigned>(kCUs)), dim3(256), 0, st, p);
+        return hipGetLastError();
+    }
     const int64_t grid = (total + 7) / 8 * 8;
-    launch_kernel(gemm_wide_kernel, dim3(static_cast<unsigned>(grid)), dim3(256), 0, st, p);
+    launch_kernel(gemm_wide_kernel<kWideBStages>, dim3(static_cast<unsigned>(grid)), dim3(256), 0, st, p);
     return hipGetLastError();
 }
 
@@ -1469,8 +1892,10 @@ static hipError_t launch_wide(const GemmParams& params, int width, hipStream_t s
 // epilogue cost more than its faster K loop saves (measured).  A function of the operator's
 // (M, N, K) alone, never of the sub-slice count, so all its sub-slice launches take the same path.
 static bool wide_class(const GemmParams& p) {
+    // (the output span is addressed with 32-bit offsets, below the out-of-range offset 2^31)
+    const int64_t c_span = ((p.M - 1) * p.ldc + p.N) * (p.out_f32 ? 4 : 2);
     return !p.conv && !p.thin && p.epi == EPI_STD && p.splits == 1 && p.K >= 256 && p.M >= 512 && p.N >= 512 &&
-           ((p.M + 255) / 256) * ((p.N + 255) / 256) >= 4 * kCUs;
+           ((p.M + 255) / 256) * ((p.N + 255) / 256) >= 4 * kCUs && c_span < (int64_t(1) << 31);
 }
 
 template <typename T>

@@ -119,7 +119,12 @@ struct GemmParams {
     // patch-staged 3x3 conv: spatial tiles per image and per tile row, and their divisors
     int h_tiles, h_tx;
     FastDiv h_div_tiles, h_div_tx;
+    // 256 x 256 tiles: kWideCtrBytes of tile counters (optional; with them the launch is
+    // persistent), and the output span in bytes (set by the launcher)
+    unsigned* wide_ctr;
+    uint32_t c_bytes;
 };
+constexpr size_t kWideCtrBytes = 256;
 
 // Split-K factor used for an (M, N, K) product.  A function of the shape
 // only -- never of the sub-slice count -- so sub-sliced launches reduce in

@@ -36,6 +36,7 @@ struct TempReq {
 struct OpInfo {
     int splits = 1;                // conv / linear: split-K factor of the GEMM
     int partial_temp = -1;         // index into temps of the split-K partial sums
+    int ctr_temp = -1;             // index into temps of the 256 x 256 GEMM tile counters
     int cs = 0;                    // conv: input channel storage stride (padded for the model input)
     bool input_is_model = false;   // conv: reads the NCHW float32 model input
     int64_t K = 0, M = 0;          // GEMM sizes (conv / linear)
@@ -368,6 +369,8 @@ static int validate_and_build(mopar_model_s& m) {
                     inf.partial_temp = static_cast<int>(inf.temps.size());
                     inf.temps.push_back(gemm_partial_bytes(M, op.n_out, inf.splits));
                 }
+                inf.ctr_temp = static_cast<int>(inf.temps.size());
+                inf.temps.push_back(kWideCtrBytes);
                 break;
             }
             case MOPAR_OP_MAXPOOL: {
@@ -440,6 +443,8 @@ static int validate_and_build(mopar_model_s& m) {
                     inf.temps.push_back(lstm_recurrence_sync_bytes(x.dims[0], x.dims[1], h));   // step sync
                 else
                     inf.temps.push_back(static_cast<size_t>(x.dims[0] * h) * es);   // h_0 = 0
+                inf.ctr_temp = static_cast<int>(inf.temps.size());
+                inf.temps.push_back(kWideCtrBytes);                               // input projection tiles
                 break;
             }
             default: return set_error(MOPAR_E_ARG, nm + ": unknown op kind");
@@ -654,6 +659,7 @@ static hipError_t run_op(const mopar_model_s& m, int i, const Ptrs& P, int ksub,
             g.ksub = ksub;
             g.splits = inf.splits;
             g.partial = inf.partial_temp >= 0 ? reinterpret_cast<float*>(P.ws + inf.temp_off[inf.partial_temp]) : nullptr;
+            g.wide_ctr = reinterpret_cast<unsigned*>(P.ws + inf.temp_off[inf.ctr_temp]);
             return launch_gemm(g, dt, s);
         }
         case MOPAR_OP_MAXPOOL:
@@ -706,6 +712,7 @@ static hipError_t run_op(const mopar_model_s& m, int i, const Ptrs& P, int ksub,
             g.K = E;
             g.ksub = 1;
             g.out_f32 = 1;
+            g.wide_ctr = reinterpret_cast<unsigned*>(P.ws + inf.temp_off[inf.ctr_temp]);
             e = launch_gemm(g, dt, s);
             if (e != hipSuccess) return e;
             if (one_launch) return launch_lstm_recurrence(gx, W(m, op.w2), P.get(op.out), cst, h0, B, T, H, s);

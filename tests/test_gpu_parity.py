@@ -163,6 +163,9 @@ def seq_ids(b, s):
     # ragged M (33 tile rows), N and K (312 = 4 x 64 + 56) with residual and GELU, against
     # 500-column sub-slices
     ("bf16", 3, 2743, 312, 8000, "gelu", True, 16),
+    # the persistent launch with groups of four columns cut by the sub-slice edge (2 x 4001
+    # columns: element stores)
+    ("bf16", 4, 2048, 256, 8002, "none", False, 2),
 ])
 def test_linear_parity_and_subslice_bitwise(dt, b, s, k, nout, act, res, ksub):
     bld, x = seq_input_model(dt, b, s, k)
