@@ -836,6 +836,7 @@ __global__ __launch_bounds__(WM * WN * KS * 64) void gemm_kernel(const GemmParam
 // same operations in the same order whatever the sub-slice count.
 constexpr int kWideRowB = 256 * 2 + 16, kWideRowF = 256 * 4 + 16;   // staged output row strides, bytes
 constexpr int kWideBStages = 2;                                      // B stages in LDS
+constexpr int kWideGroupM = 8;                                       // m tiles per group in the block order
 // An accumulator read out where it is used (left to itself the compiler copies many accumulator
 // tiles to ordinary registers at once, and spills them)
 __device__ __forceinline__ float acc_read(float a) {
@@ -869,7 +870,7 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_kernel(const GemmParams p) {
     touch_kernargs<sizeof(GemmParams)>();
     const unsigned t = (blockIdx.x % 8) * static_cast<unsigned>(p.g_per_xcd) + blockIdx.x / 8;
     if (t >= static_cast<unsigned>(p.g_total)) return;
-    constexpr int GM = kGroupM;
+    constexpr int GM = kWideGroupM;
     const unsigned group = p.g_div_group.div(t);
     const unsigned within = t - group * static_cast<unsigned>(GM * p.g_cols);
     const bool last = static_cast<int>(group) == (p.g_mt - 1) / GM;
@@ -1243,7 +1244,7 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_persistent(const GemmParams 
     // past a narrower sub-slice's last column
     auto decode = [&](int li, int& m0, int& n0, int& n_hi) __attribute__((always_inline)) -> bool {
         const unsigned t = static_cast<unsigned>(t_lo + li);
-        constexpr int GM = kGroupM;
+        constexpr int GM = kWideGroupM;
         const unsigned group = p.g_div_group.div(t);
         const unsigned within = t - group * static_cast<unsigned>(GM * p.g_cols);
         const bool last = static_cast<int>(group) == (p.g_mt - 1) / GM;
@@ -1283,22 +1284,28 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_persistent(const GemmParams 
     };
     uint4* const ldsA = &lds[0];
     uint4* const ldsB = &lds[2 * SA];
-    // load slots 4 r .. 4 r + 3 of one operand's stage kt (clamped to the last stage) into buffer buf
-    auto load_a = [&](const unsigned (&va)[LA], int kt, int buf, int r) __attribute__((always_inline)) {
-        kt = kt < nk ? kt : nk - 1;
+    // Load slot s2 of one operand's stage kt (clamped to the last stage) into buffer buf.  (Issuing
+    // one of these 1 KB loads holds the wave for ~50 cycles, measured; the K loop puts one after
+    // every second MFMA, so that the MFMAs already issued keep the matrix unit busy meanwhile.)
+    auto load_a = [&](const unsigned (&va)[LA], int kt, int buf, int s2) __attribute__((always_inline)) {
+        kt = __builtin_amdgcn_readfirstlane(kt < nk ? kt : nk - 1);
         const unsigned soff = static_cast<unsigned>(kt) * (BK * sizeof(T));
         const bool kin = kt != ktail || kt * BK + cl * 8 < p.K;
-#pragma unroll
-        for (int s2 = 4 * r; s2 < 4 * r + 4; ++s2)
-            buffer_load_lds(p.A, p.a_bytes, (lds_ptr_t)(ldsA + buf * SA + (wave + NW * s2) * 64), kin ? va[s2] : kOOB, soff);
+        // (the offset is settled before the load: a branch around the load would turn the
+        // scalar offset into a per-lane one, which the compiler then loops over)
+        unsigned v = kin ? va[s2] : kOOB;
+        asm volatile("" : "+v"(v));
+        buffer_load_lds(p.A, p.a_bytes, (lds_ptr_t)(ldsA + buf * SA + (wave + NW * s2) * 64), v, soff);
     };
-    auto load_b = [&](const unsigned (&vb)[LB], int kt, int buf, int r) __attribute__((always_inline)) {
-        kt = kt < nk ? kt : nk - 1;
+    auto load_b = [&](const unsigned (&vb)[LB], int kt, int buf, int s2) __attribute__((always_inline)) {
+        kt = __builtin_amdgcn_readfirstlane(kt < nk ? kt : nk - 1);
         const unsigned soff = static_cast<unsigned>(kt) * (BK * sizeof(T));
         const bool kin = kt != ktail || kt * BK + cl * 8 < p.K;
-#pragma unroll
-        for (int s2 = 4 * r; s2 < 4 * r + 4; ++s2)
-            buffer_load_lds(p.B, p.b_bytes, (lds_ptr_t)(ldsB + buf * SB + (wave + NW * s2) * 64), kin ? vb[s2] : kOOB, soff);
+        // (the offset is settled before the load: a branch around the load would turn the
+        // scalar offset into a per-lane one, which the compiler then loops over)
+        unsigned v = kin ? vb[s2] : kOOB;
+        asm volatile("" : "+v"(v));
+        buffer_load_lds(p.B, p.b_bytes, (lds_ptr_t)(ldsB + buf * SB + (wave + NW * s2) * 64), v, soff);
     };
     // Bias + second bias of a tile: thread t reads column n0 + t (zero past n_hi) and the sums go
     // through LDS (s_bias), from which every wave starts its accumulators -- the same float
@@ -1333,20 +1340,20 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_persistent(const GemmParams 
         fa[kk] = ldsa0 + f + ((wm * TM) >> 3) * 1024;
         fb[kk] = ldsb0 + f + ((wn * TN) >> 3) * 1024;
     }
-    // one k step: MFMAs on (ma, mb) row by row, each row preceded by the reads of the next k step's
-    // fragments and by loads(a)
+    // One k step: MFMAs on (ma, mb) row by row, each row preceded by the reads of the next k step's
+    // fragments; loads(2 a + h) after the row's MFMA 2 h + 1.  Nothing is scheduled across.
     auto step = [&](u32x4 (&ma)[FM], u32x4 (&mb)[FN], unsigned ra_base, unsigned rb_base, u32x4 (&ra)[FM],
                     u32x4 (&rb_)[FN], auto&& loads) __attribute__((always_inline)) {
         static_for<FM>([&](auto a) __attribute__((always_inline)) {
             ra[a] = lds_read16_at<a * 4096>(ra_base);
             rb_[a] = lds_read16_at<a * 4096>(rb_base);
-            loads(a);
             __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int b = 0; b < FN; ++b)
+            static_for<FN>([&](auto b) __attribute__((always_inline)) {
                 acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, mb[b]),
                                                                     __builtin_bit_cast(bf16x8, ma[a]), acc[a][b], 0, 0, 0);
-            __builtin_amdgcn_sched_barrier(0);
+                if constexpr (b % 2 == 1) loads(2 * a + b / 2);
+                __builtin_amdgcn_sched_barrier(0);
+            });
         });
     };
     auto no_loads = [](int) __attribute__((always_inline)) {};
@@ -1374,9 +1381,9 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_persistent(const GemmParams 
         s_bias[threadIdx.x] = bv + b2v;
     }
 #pragma unroll
-    for (int r = 0; r < 2; ++r) load_b(vb, 0, 0, r);
+    for (int s2 = 0; s2 < LB; ++s2) load_b(vb, 0, 0, s2);
 #pragma unroll
-    for (int r = 0; r < 2; ++r) load_a(va, 0, 0, r);
+    for (int s2 = 0; s2 < LA; ++s2) load_a(va, 0, 0, s2);
     bool wait_all = true;                               // the first stage's loads are the newest in flight
 
     const uint32_t esz = p.out_f32 ? 4u : 2u;
@@ -1398,7 +1405,12 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_persistent(const GemmParams 
         };
         auto read_ticket = [&]() __attribute__((always_inline)) {
             li_next = __builtin_amdgcn_readfirstlane(s_ticket);
-            next_ok = li_next < cx && decode(li_next, m0n, n0n, n_hin);
+            // (uniform values, kept in scalar registers: otherwise the compiler may treat the
+            // branches on them as divergent and loop over the loads' scalar offsets)
+            next_ok = __builtin_amdgcn_readfirstlane((li_next < cx && decode(li_next, m0n, n0n, n_hin)) ? 1 : 0) != 0;
+            m0n = __builtin_amdgcn_readfirstlane(m0n);
+            n0n = __builtin_amdgcn_readfirstlane(n0n);
+            n_hin = __builtin_amdgcn_readfirstlane(n_hin);
             if (next_ok) offsets(m0n, n0n, n_hin, van, vbn);
         };
 
@@ -1420,13 +1432,12 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_persistent(const GemmParams 
             });
             lds_wait();
             pin_all(f0a, f0b);
-            auto ld1 = [&](auto a) __attribute__((always_inline)) {
-                if constexpr (a < 2) load_a(va, 1, nb, a); else load_b(vb, 1, nb, a - 2);
-            };
-            step(f0a, f0b, ab + fa[1], bb + fb[1], f1a, f1b, ld1);
+            auto ld1b = [&](int s2) __attribute__((always_inline)) { load_b(vb, 1, nb, s2); };
+            auto ld1a = [&](int s2) __attribute__((always_inline)) { load_a(va, 1, nb, s2); };
+            step(f0a, f0b, ab + fa[1], bb + fb[1], f1a, f1b, ld1b);
             lds_wait();
             pin_all(f1a, f1b);
-            step(f1a, f1b, ab + fa[2], bb + fb[2], f0a, f0b, no_loads);
+            step(f1a, f1b, ab + fa[2], bb + fb[2], f0a, f0b, ld1a);
             lds_wait();
             pin_all(f0a, f0b);
             step(f0a, f0b, ab + fa[3], bb + fb[3], f1a, f1b, no_loads);
@@ -1441,13 +1452,12 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_persistent(const GemmParams 
             if (st == 1) take_ticket();
             __builtin_amdgcn_s_barrier();
             if (st == 1) read_ticket();
-            auto ldn = [&](auto a) __attribute__((always_inline)) {
-                if constexpr (a < 2) load_a(va, st + 1, buf ^ 1, a); else load_b(vb, st + 1, buf ^ 1, a - 2);
-            };
-            step(f1a, f1b, ab + fa[0], bb + fb[0], f0a, f0b, ldn);
+            auto ldnb = [&](int s2) __attribute__((always_inline)) { load_b(vb, st + 1, buf ^ 1, s2); };
+            auto ldna = [&](int s2) __attribute__((always_inline)) { load_a(va, st + 1, buf ^ 1, s2); };
+            step(f1a, f1b, ab + fa[0], bb + fb[0], f0a, f0b, ldnb);
             lds_wait();
             pin_all(f0a, f0b);
-            step(f0a, f0b, ab + fa[1], bb + fb[1], f1a, f1b, no_loads);
+            step(f0a, f0b, ab + fa[1], bb + fb[1], f1a, f1b, ldna);
             lds_wait();
             pin_all(f1a, f1b);
             step(f1a, f1b, ab + fa[2], bb + fb[2], f0a, f0b, no_loads);
@@ -1466,17 +1476,16 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_persistent(const GemmParams 
             __builtin_amdgcn_s_barrier();
             if (nk == 2) read_ticket();
             if (next_ok) bias_col(n0n, n_hin, nbv, nb2v);  // used in the epilogue
-            auto ldx = [&](auto a) __attribute__((always_inline)) {
-                if (next_ok) {
-                    if constexpr (a < 2) load_a(van, 0, buf ^ 1, a); else load_b(vbn, 0, buf ^ 1, a - 2);
-                } else {
-                    if constexpr (a < 2) load_a(va, nk - 1, buf ^ 1, a); else load_b(vb, nk - 1, buf ^ 1, a - 2);
-                }
+            auto ldxb = [&](int s2) __attribute__((always_inline)) {
+                if (next_ok) load_b(vbn, 0, buf ^ 1, s2); else load_b(vb, nk - 1, buf ^ 1, s2);
             };
-            step(f1a, f1b, ab + fa[0], bb + fb[0], f0a, f0b, ldx);
+            auto ldxa = [&](int s2) __attribute__((always_inline)) {
+                if (next_ok) load_a(van, 0, buf ^ 1, s2); else load_a(va, nk - 1, buf ^ 1, s2);
+            };
+            step(f1a, f1b, ab + fa[0], bb + fb[0], f0a, f0b, ldxb);
             lds_wait();
             pin_all(f0a, f0b);
-            step(f0a, f0b, ab + fa[1], bb + fb[1], f1a, f1b, no_loads);
+            step(f0a, f0b, ab + fa[1], bb + fb[1], f1a, f1b, ldxa);
             lds_wait();
             pin_all(f1a, f1b);
             step(f1a, f1b, ab + fa[2], bb + fb[2], f0a, f0b, no_loads);
@@ -1562,9 +1571,9 @@ __global__ __launch_bounds__(256, 1) void gemm_wide_persistent(const GemmParams 
             s_bias[threadIdx.x] = bv + b2v;
         }
 #pragma unroll
-        for (int r = 0; r < 2; ++r) load_b(vb, 0, 0, r);
+        for (int s2 = 0; s2 < LB; ++s2) load_b(vb, 0, 0, s2);
 #pragma unroll
-        for (int r = 0; r < 2; ++r) load_a(va, 0, 0, r);
+        for (int s2 = 0; s2 < LA; ++s2) load_a(va, 0, 0, s2);
         wait_all = true;
     }
 }
@@ -1860,7 +1869,7 @@ static hipError_t launch_wide(const GemmParams& params, int width, hipStream_t s
     p.c_bytes = static_cast<uint32_t>(((p.M - 1) * p.ldc + p.N) * (p.out_f32 ? 4 : 2));
     const int64_t mt = (p.M + 255) / 256, nt = (width + 255) / 256;
     const int64_t total = mt * nt * p.ksub;
-    if (total >= (int64_t(1) << 31) / kGroupM) return hipErrorInvalidValue;
+    if (total >= (int64_t(1) << 31) / kWideGroupM) return hipErrorInvalidValue;
     p.g_mt = static_cast<int>(mt);
     p.g_nt = static_cast<int>(nt);
     p.g_total = static_cast<int>(total);
@@ -1869,8 +1878,8 @@ static hipError_t launch_wide(const GemmParams& params, int width, hipStream_t s
     p.g_nk = (p.K + 63) / 64;
     p.g_q = p.N / p.ksub;
     p.g_rr = p.N % p.ksub;
-    p.g_div_group = FastDiv(static_cast<unsigned>(kGroupM * p.g_cols));
-    const int last = static_cast<int>(mt - (mt - 1) / kGroupM * kGroupM);
+    p.g_div_group = FastDiv(static_cast<unsigned>(kWideGroupM * p.g_cols));
+    const int last = static_cast<int>(mt - (mt - 1) / kWideGroupM * kWideGroupM);
     p.g_div_last = FastDiv(static_cast<unsigned>(last));
     p.g_div_nt = FastDiv(static_cast<unsigned>(nt));
     if (p.wide_ctr && !p.res && p.act == MOPAR_ACT_NONE) {
