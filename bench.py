@@ -307,7 +307,12 @@ def run_config(cfg, args, headline):
 
     measured = None
     if headline and not args.no_measured_plan:
-        mplan, tp, _ = sm.measured_plan(x, k_max=args.k_max, reps=3)
+        # on a stream of its own, so that a kernel trace tells its launches (every sub-slice
+        # count up to k_max) from the timed ones on the default stream
+        mstream = torch.cuda.Stream(device=dev)
+        mstream.wait_stream(torch.cuda.current_stream(dev))
+        mplan, tp, _ = sm.measured_plan(x, k_max=args.k_max, reps=3, stream=mstream)
+        torch.cuda.synchronize(dev)
         measured = {"k_max": args.k_max, "n_slices": mplan.n_slices, "slice_end": mplan.slice_end,
                     "k": mplan.k, "t_tau_ms": round(mplan.t_tau * 1e3, 4),
                     "tp_ms_by_k": [round(sum(r[e] for r in tp) * 1e3, 4) for e in range(args.k_max)]}

@@ -410,10 +410,10 @@ class SlicedModel:
                                         _stream_ptr(stream), tab))
         return [list(tab[l * k_max:(l + 1) * k_max]) for l in range(n)]
 
-    def measured_plan(self, x, k_max=4, reps=3, **opts):
+    def measured_plan(self, x, k_max=4, reps=3, stream=None, **opts):
         """Plan from the measured profile: each node's time t_l := t_p(l, 1) measured, the
         parallelism search over t_p(l, eta) (t_a = 0).  Returns (plan, t_p table)."""
-        tp = self.measure(x, k_max=k_max, reps=reps)
+        tp = self.measure(x, k_max=k_max, reps=reps, stream=stream)
         prof = [(mem, tp[l][0], ob, rdw) for l, (mem, _, ob, rdw) in enumerate(self.profile())]
         kw = dict(elim_tau=0.05)
         kw.update(opts)
