@@ -37,11 +37,13 @@
  *            given at mopar_op.
  * Determinism. Plans and sub-slice ranges are pure functions of their
  *            inputs, and a forward pass is bitwise reproducible: no kernel
- *            accumulates through atomics, and the one-launch LSTM recurrence,
- *            whose blocks claim (step, tile) work with atomics, computes a
- *            tile with the same operands and operation order whichever block
- *            claims it.  The k-way sub-sliced RD kernels produce the same bits
- *            as the unsplit kernel.
+ *            accumulates through atomics.  Two kernels hand out work with
+ *            atomics -- the one-launch LSTM recurrence, whose blocks claim
+ *            (step, tile) work, and the persistent GEMM, whose blocks take
+ *            tiles from a counter -- and both compute a tile with the same
+ *            operands and operation order whichever block takes it.  The k-way
+ *            sub-sliced RD kernels produce the same bits as the unsplit
+ *            kernel.
  */
 #ifndef MOPAR_H
 #define MOPAR_H
@@ -242,7 +244,8 @@ int mopar_model_profile_dominant(mopar_model_t model, double frac, mopar_layer_p
  * under `plan`: the tensors that live inside slices, the boundary tensors
  * before encode and after decode (the hand-off of Sec. III-D goes through the
  * caller's code buffers, not this workspace) and op scratch (split-K partial
- * sums, the LSTM gate pre-activations and cell state).  The caller allocates it
+ * sums, the LSTM gate pre-activations and cell state, the tile counters of a
+ * persistent GEMM launch).  The caller allocates it
  * (Memory convention); one workspace serves one forward at a time.  Errors:
  * MOPAR_E_ARG (null pointers, a plan for another model or with an invalid k). */
 int mopar_model_workspace_bytes(mopar_model_t model, const mopar_plan* plan, size_t* bytes);
