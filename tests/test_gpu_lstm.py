@@ -2,10 +2,12 @@
 
 bf16 layers whose hidden size is a multiple of 16 (up to 1024) run the whole
 recurrence in one launch; others run one GEMM per step.  Both are checked
-against the oracle.  The one-launch kernel lets any resident block compute a
-tile whose owner is not running; the tests force that from the host (hooks make
-some blocks exit at once, or start late) and require the same output bits, and
-run two layers concurrently on two streams.
+against the oracle; so are stacked layers, whose outputs must not depend on the
+schedule (the same bits with per-op timing, with the no-allocation forward, and
+with a slice cut between the layers).  The one-launch kernel lets any resident block compute a tile whose owner
+is not running; the tests force that from the host (hooks make some blocks exit
+at once, or start late) and require the same output bits, and run two models
+concurrently on two streams.
 """
 import os
 
@@ -16,17 +18,21 @@ import torch
 import oracle
 import synth
 from tests.helpers import TOL, rel_err
+from paper_2404_02445_amd._lib import STATIC_WORKSPACE_BYTES
 
 pytestmark = pytest.mark.gpu
 P = pytest.importorskip("paper_2404_02445_amd")
 
 
-def lstm_model(b, t, e, h, seed=3, layers=1, w=0.3):
+def lstm_model(b, t, e, h, seed=3, layers=1, w=0.3, nodes=False):
+    """An embedding and `layers` stacked LSTM layers (each its own planning node if `nodes`)."""
     bld = synth._Builder("lstm", "bf16", b, seed)
     ids = bld.tensor((b, t), "i32")
     bld.new_layer("L0")
     x = bld.embed(ids, b * t, e, "src", -1.0, 1.0)
     for i in range(layers):
+        if nodes:
+            bld.new_layer(f"L{i + 1}")
         x = bld.lstm(x, h, f"lstm{i}", -w, w)
     return bld.finish(x, 1), np.arange(b * t, dtype=np.int32).reshape(b, t)
 
@@ -115,3 +121,65 @@ def test_two_layers_running_concurrently_on_two_streams():
     torch.cuda.synchronize()
     for o in outs:
         assert torch.equal(o, ref)
+
+
+STACKED = [
+    (37, 6, 64, 48, 2),      # ragged batch groups (37 = 2 x 16 + 5)
+    (2, 7, 8, 16, 2),        # the smallest hidden size
+    (64, 40, 128, 256, 3),   # three layers
+    (40, 50, 64, 256, 2),
+    (5, 9, 1024, 1024, 2),   # the LSTM LM's widths
+    (64, 128, 1024, 1024, 2),  # the LSTM LM's layers
+]
+
+
+@pytest.mark.parametrize("b,t,e,h,layers", STACKED)
+def test_stacked_layers_parity_and_schedule_independence(b, t, e, h, layers):
+    m, ids = lstm_model(b, t, e, h, layers=layers, nodes=True, w=0.1 if t < 64 else 0.05)
+    n = len(m.layers)
+    sm = P.SlicedModel(m)
+    x = torch.from_numpy(ids).cuda()
+    whole = P.make_plan(n, [n - 1], [1] * n)
+    ws = sm.alloc_workspace(whole)
+    ref = oracle.forward(m, ids)
+
+    def run(plan, timing=False, static=False):
+        out = sm.alloc_output()
+        sm.set_timing(timing)
+        try:
+            if plan.n_slices == 1 and static:
+                sm.forward_static(plan, x, out)
+            elif plan.n_slices == 1:
+                sm.forward(plan, x, out, None, None, ws)
+            else:
+                codecs, keep = sm.codecs(plan, "raw")
+                codes = sm.alloc_codes(plan, codecs)
+                sm.forward(plan, x, out, codecs, codes, sm.alloc_workspace(plan))
+            torch.cuda.synchronize()
+        finally:
+            sm.set_timing(False)
+        return out
+
+    y = run(whole)
+    assert rel_err(canon(y), ref) <= TOL["bf16"]
+    assert torch.equal(run(whole), y), "not deterministic"
+    assert torch.equal(run(whole, timing=True), y), "one after the other (per-op timing) differs"
+    if sm.workspace_bytes(whole) <= STATIC_WORKSPACE_BYTES:
+        assert torch.equal(run(whole, static=True), y), "the no-allocation forward differs"
+    every_cut = P.make_plan(n, list(range(n)), [1] * n)   # a slice per layer, raw codecs
+    assert torch.equal(run(every_cut), y), "a slice cut between the layers changes the bits"
+
+
+@pytest.mark.parametrize("absent", [2, 3])
+def test_stacked_layers_with_absent_blocks(absent):
+    # blocks of both layers never run; the rest compute their tiles
+    m, ids = lstm_model(64, 20, 256, 512, layers=2)
+    ref, _ = forward(m, ids)
+    torch.cuda.synchronize()
+    os.environ["MOPAR_TEST_LSTM_ABSENT"] = str(absent)
+    try:
+        got, _ = forward(m, ids)
+        torch.cuda.synchronize()
+    finally:
+        del os.environ["MOPAR_TEST_LSTM_ABSENT"]
+    assert torch.equal(got, ref)
