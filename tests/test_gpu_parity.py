@@ -166,6 +166,8 @@ def seq_ids(b, s):
     # the persistent launch with groups of four columns cut by the sub-slice edge (2 x 4001
     # columns: element stores)
     ("bf16", 4, 2048, 256, 8002, "none", False, 2),
+    # BERT-base's FFN1 (4096 x 768 -> 3072, GELU) in its four 768-column sub-slices
+    ("bf16", 32, 128, 768, 3072, "gelu", False, 4),
 ])
 def test_linear_parity_and_subslice_bitwise(dt, b, s, k, nout, act, res, ksub):
     bld, x = seq_input_model(dt, b, s, k)
