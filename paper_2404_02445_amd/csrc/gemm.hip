@@ -1635,15 +1635,19 @@ __global__ void splitk_reduce_kernel(const GemmParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// 3x3 convolutions (stride 1, padding 1) over 64- or 128-channel bf16 images,
-// patch-staged.  The implicit GEMM above fetches every input pixel once per
-// tap (nine times); here a block owns a TH x 8 tile of output pixels of one
-// image (8 x 8 in use) and BN output channels of one sub-slice, and for each
-// 64-channel chunk it stages the (TH + 2) x 10 input patch around its tile (one
-// pixel of halo each way, zeros outside the image) once, with the nine taps'
-// weight rows, then forms all nine taps' A fragments from that patch in LDS
-// (about a sixth of the A bytes; the win is largest on narrow sub-slices, whose
-// A traffic dominates).  Loads use the same whole-line, XOR-swizzled layout as
+// 3x3 convolutions (stride 1, padding 1) over bf16 images of 64 to 512 channels
+// (multiples of 64) and at most 56 x 56 pixels, patch-staged.  The implicit
+// GEMM above fetches every input pixel once per tap (nine times); here a block
+// owns a TH x 8 tile of output pixels of one image (8 x 8 in use) and BN output
+// channels of one sub-slice, and for each 64-channel chunk it stages the
+// (TH + 2) x 10 input patch around its tile (one pixel of halo each way, zeros
+// outside the image) once, with the nine taps' weight rows, then forms all nine
+// taps' A fragments from that patch in LDS (about a sixth of the A bytes; the
+// win is largest on narrow sub-slices, whose A traffic dominates).  Images of
+// more than two chunks take two chunk buffers, the next chunk's loads going out
+// before the current chunk's products (64 KB of LDS per block; with fewer chunks
+// one buffer, which leaves room for more resident blocks: measured faster on
+// ResNet-50's stages 1 and 2, 7.7-8.9 us against 10.8-14.1 us).  Loads use the same whole-line, XOR-swizzled layout as
 // above (patch pixels and weight rows in place of tile rows).  The k order is
 // chunk, then tap, then the two 32-wide steps; it depends only on the op, not
 // on BN, TH or the sub-slice, so sub-sliced and unsplit launches agree bit for
@@ -1654,14 +1658,16 @@ __global__ void splitk_reduce_kernel(const GemmParams p) {
 constexpr int HTW = 8;                       // output tile width; its height TH is a parameter
 
 bool conv_halo_ok(int dtype, int kh, int kw, int stride, int pad, int cs, int n_out, int out_h, int out_w) {
-    // (convs with more than 128 outputs, or over images above 56 x 56 -- VGG-16's first three
-    // blocks -- ran slower here than on the implicit GEMM's larger tiles, measured: the patch is
-    // re-read for every 16 output channels, and small tiles multiply the per-block costs)
-    return dtype == MOPAR_BF16 && kh == 3 && kw == 3 && stride == 1 && pad == 1 && cs % 64 == 0 && cs <= 128 &&
-           n_out <= 128 && out_h >= 16 && out_w >= 16 && out_h * out_w <= 56 * 56;
+    // (convs over images above 56 x 56 -- VGG-16's first three blocks, 64 to 256 channels --
+    // ran slower here than on the implicit GEMM's larger tiles, measured: the patch is re-read
+    // for every 16 output channels, and small tiles multiply the per-block costs.  On the small
+    // images of ResNet-50's stages 3 and 4 (14 x 14 x 256, 7 x 7 x 512) this kernel needs no
+    // split-K and no second launch: 12.9 -> 8.8 and 14.7 -> 13.4 us before double-buffering)
+    return dtype == MOPAR_BF16 && kh == 3 && kw == 3 && stride == 1 && pad == 1 && cs % 64 == 0 && cs <= 512 &&
+           n_out <= 512 && out_h >= 7 && out_w >= 7 && out_h * out_w <= 56 * 56;
 }
 
-template <int BN, int TH>
+template <int BN, int TH, int NBUF>
 __global__ __launch_bounds__(TH * HTW / 16 * 64) void conv3_halo_kernel(const GemmParams p) {
     using T = __bf16;
     constexpr int NW = TH * HTW / 16;           // waves: 16 tile pixels (two tile rows) each
@@ -1671,7 +1677,12 @@ __global__ __launch_bounds__(TH * HTW / 16 * 64) void conv3_halo_kernel(const Ge
     constexpr int BPT = BN / 8;                 // weight load blocks per tap
     constexpr int NBB = 9 * BPT;                // weight load blocks per chunk
     constexpr int LP = (HPBLK + NW - 1) / NW, LB = (NBB + NW - 1) / NW;   // load slots per wave
-    __shared__ uint4 lds[(HPBLK + NBB) * 64];   // one chunk: patch blocks, then weight blocks
+    // NBUF chunk buffers: patch blocks, weight blocks and, with two buffers, one block for the
+    // load slots past the last block (a wave whose share ends early still issues LP + LB loads,
+    // of zeros, there, so that every wave's wait count is the same)
+    static_assert(NBUF == 1 || NBUF == 2, "chunk buffers");
+    constexpr int CHB = HPBLK + NBB + (NBUF == 2 ? 1 : 0);
+    __shared__ uint4 lds[NBUF * CHB * 64];
     touch_kernargs<sizeof(GemmParams)>();
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -1735,23 +1746,46 @@ __global__ __launch_bounds__(TH * HTW / 16 * 64) void conv3_halo_kernel(const Ge
         for (int e = 0; e < 4; ++e) acc[b][e] = bv[e] + b2v[e];
     }
 
-    const unsigned lds0 = static_cast<unsigned>(reinterpret_cast<size_t>((lds_ptr_t)(&lds[0])));
     const int nq = p.cs / 64;
-    for (int qc = 0; qc < nq; ++qc) {
-        if (qc > 0) __syncthreads();            // the previous chunk's fragments have been read
+    // chunk qc's loads into buffer buf (LP + LB per wave, always)
+    auto issue = [&](int qc, int buf) __attribute__((always_inline)) {
         const unsigned soff = static_cast<unsigned>(qc) * 128u;
+        uint4* const base = &lds[buf * CHB * 64];
 #pragma unroll
         for (int i = 0; i < LP; ++i) {
-            if (HPBLK % NW != 0 && i == LP - 1 && wave + NW * i >= HPBLK) break;   // wave-uniform
-            buffer_load_lds(p.A, p.a_bytes, (lds_ptr_t)(&lds[(wave + NW * i) * 64]), voffP[i], soff);
+            const int b = wave + NW * i;        // wave-uniform
+            const bool dead = HPBLK % NW != 0 && b >= HPBLK;
+            if (NBUF == 1 && dead) break;
+            buffer_load_lds(p.A, p.a_bytes, (lds_ptr_t)(base + (dead ? CHB - 1 : b) * 64), dead ? kOOB : voffP[i], soff);
         }
 #pragma unroll
         for (int i = 0; i < LB; ++i) {
-            if (NBB % NW != 0 && i == LB - 1 && wave + NW * i >= NBB) break;
-            buffer_load_lds(p.B, p.b_bytes, (lds_ptr_t)(&lds[(HPBLK + wave + NW * i) * 64]), voffB[i], soff);
+            const int b = wave + NW * i;
+            const bool dead = NBB % NW != 0 && b >= NBB;
+            if (NBUF == 1 && dead) break;
+            buffer_load_lds(p.B, p.b_bytes, (lds_ptr_t)(base + (dead ? CHB - 1 : HPBLK + b) * 64), dead ? kOOB : voffB[i],
+                            soff);
         }
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __builtin_amdgcn_s_barrier();
+    };
+    static_assert(LP + LB <= 63, "the wait below counts the next chunk's loads");
+    if constexpr (NBUF == 2) issue(0, 0);
+    for (int qc = 0; qc < nq; ++qc) {
+        if constexpr (NBUF == 2) {
+            // the next chunk goes out before this one is waited for; its loads are the last issued
+            if (qc + 1 < nq) {
+                issue(qc + 1, (qc + 1) & 1);
+                asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LP + LB) : "memory");
+            } else {
+                asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            }
+        } else {
+            if (qc > 0) __syncthreads();        // the previous chunk's fragments have been read
+            issue(qc, 0);
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        }
+        __builtin_amdgcn_s_barrier();           // every wave's share of chunk qc has landed
+        const unsigned lds0 =
+            static_cast<unsigned>(reinterpret_cast<size_t>((lds_ptr_t)(&lds[(NBUF == 2 ? qc & 1 : 0) * CHB * 64])));
 #pragma unroll
         for (int tap = 0; tap < 9; ++tap) {
             const int pp = ((pix >> 3) + tap / 3) * PW + (pix & 7) + tap % 3;
@@ -1775,6 +1809,7 @@ __global__ __launch_bounds__(TH * HTW / 16 * 64) void conv3_halo_kernel(const Ge
                 }
             }
         }
+        if constexpr (NBUF == 2) __syncthreads();   // chunk qc's buffer is read before chunk qc + 2 reuses it
     }
 
     if (!row_ok) return;
@@ -1794,7 +1829,7 @@ __global__ __launch_bounds__(TH * HTW / 16 * 64) void conv3_halo_kernel(const Ge
     }
 }
 
-template <int BN, int TH>
+template <int BN, int TH, int NBUF>
 static hipError_t launch_halo(const GemmParams& params, int width, hipStream_t st) {
     GemmParams p = params;
     const int64_t nt = (width + BN - 1) / BN;
@@ -1816,7 +1851,8 @@ static hipError_t launch_halo(const GemmParams& params, int width, hipStream_t s
     p.h_div_tiles = FastDiv(static_cast<unsigned>(ty * tx));
     p.h_div_tx = FastDiv(static_cast<unsigned>(tx));
     const int64_t grid = (total + 7) / 8 * 8;
-    launch_kernel(conv3_halo_kernel<BN, TH>, dim3(static_cast<unsigned>(grid)), dim3(TH * HTW / 16 * 64), 0, st, p);
+    launch_kernel(conv3_halo_kernel<BN, TH, NBUF>, dim3(static_cast<unsigned>(grid)), dim3(TH * HTW / 16 * 64), 0, st,
+                  p);
     return hipGetLastError();
 }
 
@@ -1981,7 +2017,8 @@ hipError_t launch_gemm(const GemmParams& params, int dtype, hipStream_t stream) 
     if (p.conv && conv_halo_ok(dtype, p.kh, p.kw, p.stride, p.pad, p.cs, p.N, p.out_h, p.out_w)) {
         if (p.splits != 1 || p.epi != EPI_STD) return hipErrorInvalidValue;
         // 16-column tiles at every width (measured at least as fast as 32 on 32-wide sub-slices)
-        return launch_halo<16, 8>(p, (p.N + p.ksub - 1) / p.ksub, stream);
+        const int width = (p.N + p.ksub - 1) / p.ksub;
+        return p.cs / 64 > 2 ? launch_halo<16, 8, 2>(p, width, stream) : launch_halo<16, 8, 1>(p, width, stream);
     }
     hipError_t e = dtype == MOPAR_BF16 ? dispatch<__bf16>(p, stream) : dispatch<float>(p, stream);
     if (e != hipSuccess || p.splits == 1) return e;
