@@ -1657,14 +1657,17 @@ __global__ void splitk_reduce_kernel(const GemmParams p) {
 // ---------------------------------------------------------------------------
 constexpr int HTW = 8;                       // output tile width; its height TH is a parameter
 
-bool conv_halo_ok(int dtype, int kh, int kw, int stride, int pad, int cs, int n_out, int out_h, int out_w) {
-    // (convs over images above 56 x 56 -- VGG-16's first three blocks, 64 to 256 channels --
-    // ran slower here than on the implicit GEMM's larger tiles, measured: the patch is re-read
-    // for every 16 output channels, and small tiles multiply the per-block costs.  On the small
-    // images of ResNet-50's stages 3 and 4 (14 x 14 x 256, 7 x 7 x 512) this kernel needs no
-    // split-K and no second launch: 12.9 -> 8.8 and 14.7 -> 13.4 us before double-buffering)
+bool conv_halo_ok(int dtype, int kh, int kw, int stride, int pad, int cs, int n_out, int out_h, int out_w, int64_t m) {
+    // Small convs only: at most 2^31 multiply-adds (M x N x K; each of ResNet-50's stride-1 3x3
+    // convs at batch 8 is 0.92 G).  On those the implicit GEMM's large tiles leave CUs idle or
+    // need split-K and a second launch, and this kernel is faster (stages 3 and 4: 9.0-10.0
+    // against 13.5-16.6 us and 12.1-12.2 against 14.6-15.2 us).  On larger convs the patch,
+    // re-read for every 16 output channels, and the small tiles lose to the GEMM, measured:
+    // VGG-16 at batch 16, 7.4-29.6 G multiply-adds, 51-192 us here against 36-74 us; and over
+    // images above 56 x 56.
+    const int64_t macs = m * n_out * (int64_t(kh) * kw * cs);
     return dtype == MOPAR_BF16 && kh == 3 && kw == 3 && stride == 1 && pad == 1 && cs % 64 == 0 && cs <= 512 &&
-           n_out <= 512 && out_h >= 7 && out_w >= 7 && out_h * out_w <= 56 * 56;
+           n_out <= 512 && out_h >= 7 && out_w >= 7 && out_h * out_w <= 56 * 56 && macs <= (int64_t(1) << 31);
 }
 
 template <int BN, int TH, int NBUF>
@@ -2014,7 +2017,7 @@ hipError_t launch_gemm(const GemmParams& params, int dtype, hipStream_t stream) 
     // the reduce keeps every split's partial in flight at once, for at most 16 splits
     if (p.splits < 1 || p.splits > 16 || (p.splits > 1 && (!p.partial || p.epi != EPI_STD)))
         return hipErrorInvalidValue;
-    if (p.conv && conv_halo_ok(dtype, p.kh, p.kw, p.stride, p.pad, p.cs, p.N, p.out_h, p.out_w)) {
+    if (p.conv && conv_halo_ok(dtype, p.kh, p.kw, p.stride, p.pad, p.cs, p.N, p.out_h, p.out_w, p.M)) {
         if (p.splits != 1 || p.epi != EPI_STD) return hipErrorInvalidValue;
         // 16-column tiles at every width (measured at least as fast as 32 on 32-wide sub-slices)
         const int width = (p.N + p.ksub - 1) / p.ksub;

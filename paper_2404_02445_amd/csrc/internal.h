@@ -136,11 +136,13 @@ inline size_t gemm_partial_bytes(int64_t M, int N, int splits) {
 
 enum { EPI_STD = 0, EPI_LSTM = 1 };
 
-// Whether a conv runs on the patch-staged 3x3 kernel (bf16, 3x3, stride 1, padding 1, 64 or 128
-// input channels, at most 128 outputs, output from 16 x 16 up to 56 x 56 pixels).  A function of
-// the op's geometry only -- never of the sub-slice count -- so sub-sliced and unsplit launches of
-// one op take the same path; such convs never split K.
-bool conv_halo_ok(int dtype, int kh, int kw, int stride, int pad, int cs, int n_out, int out_h, int out_w);
+// Whether a conv runs on the patch-staged 3x3 kernel (bf16, 3x3, stride 1, padding 1, a multiple
+// of 64 up to 512 input channels, at most 512 outputs, output from 7 x 7 up to 56 x 56 pixels, at
+// most 2^31 multiply-adds over the m output pixels of the batch).  A function of the op's
+// geometry only -- never of the sub-slice count -- so sub-sliced and unsplit launches of one op
+// take the same path; such convs never split K.
+bool conv_halo_ok(int dtype, int kh, int kw, int stride, int pad, int cs, int n_out, int out_h, int out_w,
+                  int64_t m);
 
 hipError_t launch_gemm(const GemmParams& p, int dtype, hipStream_t stream);
 

@@ -339,7 +339,7 @@ static int validate_and_build(mopar_model_s& m) {
                     return set_error(MOPAR_E_ARG, nm + ": weight offsets out of range or not 16-byte aligned");
                 if (xin) inf.temps.push_back(static_cast<size_t>(x.dims[0] * x.dims[2] * x.dims[3] * inf.cs) * es);
                 inf.splits = conv_halo_ok(m.dtype, op.kh, op.kw, op.stride, op.pad, inf.cs, op.n_out,
-                                          static_cast<int>(ho), static_cast<int>(wo))
+                                          static_cast<int>(ho), static_cast<int>(wo), inf.M)
                                  ? 1
                                  : gemm_splits(inf.M, op.n_out, static_cast<int>(inf.K), m.dtype, EPI_STD);
                 if (inf.splits > 1) {

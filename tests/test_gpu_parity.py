@@ -72,6 +72,9 @@ CONV_CASES = [
     ("bf16", 1, 64, 19, 48, 3, 1, 1, True, True),     # 3x3, residual, ragged N tile (patch-staged)
     ("bf16", 2, 128, 20, 64, 3, 1, 1, False, True),   # patch-staged 3x3: two channel chunks, ragged tiles
     ("bf16", 1, 64, 16, 120, 3, 1, 1, True, True),    # patch-staged 3x3: whole tiles, ragged sub-slices
+    ("bf16", 2, 192, 12, 40, 3, 1, 1, True, True),    # patch-staged, two chunk buffers: an odd chunk count
+    ("bf16", 2, 256, 14, 256, 3, 1, 1, True, True),   # ResNet-50's stage-3 3x3 (four chunks)
+    ("bf16", 1, 512, 7, 512, 3, 1, 1, True, True),    # stage 4: eight chunks, a 7 x 7 image in one ragged tile
     ("bf16", 2, 32, 14, 96, 3, 2, 1, True, True),     # strided 3x3
     ("bf16", 1, 128, 9, 256, 1, 1, 0, True, True),    # 1x1 wide
     ("bf16", 3, 16, 11, 20, 1, 2, 0, False, True),    # strided 1x1, N=20
