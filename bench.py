@@ -426,6 +426,29 @@ def run_config(cfg, args, headline):
     per = [evs[i].elapsed_time(evs[i + 1]) for i in range(n_lat)]
     seq_value = m.batch / (statistics.median(per) / 1e3)
 
+    # --- the same, with RAW codecs (a bit copy of each boundary tensor): what the AE codec saves
+    #     or costs against handing the tensor over as it is ------------------------------------
+    raw_codec = None
+    if args.codec == "ae":
+        rcodecs, rkeep = sm.codecs(plan, "raw")
+        rcodes = sm.alloc_codes(plan, rcodecs)
+        rout = sm.alloc_output()
+        for _ in range(2):
+            sm.forward(plan, x, rout, rcodecs, rcodes, ws)
+        revs = [torch.cuda.Event(enable_timing=True) for _ in range(n_lat + 1)]
+        torch.cuda.synchronize()
+        revs[0].record(stream)
+        for i in range(n_lat):
+            sm.forward(plan, x, rout, rcodecs, rcodes, ws)
+            revs[i + 1].record(stream)
+        torch.cuda.synchronize()
+        rper = [revs[i].elapsed_time(revs[i + 1]) for i in range(n_lat)]
+        raw_codec = {"sequential_value": round(m.batch / (statistics.median(rper) / 1e3), 2),
+                     "latency_ms": {"p50": round(statistics.median(rper), 4),
+                                    "p95": round(float(np.percentile(rper, 95)), 4)},
+                     "code_bytes_per_batch": int(sum(b.numel() * b.element_size() for b in rcodes))}
+        del rcodes, rout, rkeep
+
     flop_step = sum(op_flops(m, op) for op in m.ops)
     codec_fl, codec_by = [], []
     for c, li in enumerate(cuts):
@@ -445,6 +468,7 @@ def run_config(cfg, args, headline):
         "slices": plan.n_slices, "k": plan.k,
         "latency_ms": {"p50": round(statistics.median(per), 4), "p95": round(float(np.percentile(per, 95)), 4)},
         "sequential_value": round(seq_value, 2),
+        "raw_codec": raw_codec,
         "mode": (f"slice pipeline: {replicas} instance(s) x {plan.n_slices} slices, one stream each, HIP graphs "
                  f"replayed, {depth} code slots and {replicas * depth} output buffers per (instance, slot); "
                  f"latency_ms is one batch at a time") if pipe is not None else "sequential",
