@@ -281,6 +281,18 @@ def committed_traffic(workload):
 WORKLOAD_TAG = {1: "tinyvgg_b1", 2: "resnet50_b8", 3: "vgg16_b16", 4: "bertbase_b32", 5: "lstmlm_b64"}
 
 
+def cpu_model():
+    """The host CPU's model name, as the kernel reports it (None where it does not)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
@@ -630,7 +642,7 @@ def run_config(cfg, args, headline):
                 break
         el = time.perf_counter() - t0
         res["cpu_baseline"] = {"value": round(done / el, 4), "unit": "inferences/s", "cores": cores,
-                               "kind": "oracle",
+                               "kind": "oracle", "cpu": cpu_model(),
                                "sample": f"{done} single-{'image' if cfg <= 3 else 'sequence'} forward(s) of the "
                                          f"same sliced workload (same plan, codecs and weights), {el:.1f} s"}
     if pipe is not None:
