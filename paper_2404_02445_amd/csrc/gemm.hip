@@ -1665,9 +1665,12 @@ bool conv_halo_ok(int dtype, int kh, int kw, int stride, int pad, int cs, int n_
     // re-read for every 16 output channels, and the small tiles lose to the GEMM, measured:
     // VGG-16 at batch 16, 7.4-29.6 G multiply-adds, 51-192 us here against 36-74 us; and over
     // images above 56 x 56.
-    const int64_t macs = m * n_out * (int64_t(kh) * kw * cs);
-    return dtype == MOPAR_BF16 && kh == 3 && kw == 3 && stride == 1 && pad == 1 && cs % 64 == 0 && cs <= 512 &&
-           n_out <= 512 && out_h >= 7 && out_w >= 7 && out_h * out_w <= 56 * 56 && macs <= (int64_t(1) << 31);
+    if (!(dtype == MOPAR_BF16 && kh == 3 && kw == 3 && stride == 1 && pad == 1 && cs % 64 == 0 && cs <= 512 &&
+          n_out >= 1 && n_out <= 512 && out_h >= 7 && out_w >= 7 && int64_t(out_h) * out_w <= 56 * 56 && m >= 0 &&
+          m < (int64_t(1) << 31)))
+        return false;
+    // (the checks above bound the product below 2^53)
+    return m * n_out * (int64_t(kh) * kw * cs) <= (int64_t(1) << 31);
 }
 
 template <int BN, int TH, int NBUF>
